@@ -1,0 +1,269 @@
+"""Benchmark of the stage forward pass on one MI355X.
+
+Workload (the metric's configuration): a Llama-3.1-70B-shaped stage of 20
+consecutive layers, [20, 40), bf16 random-init weights N(0, 0.02^2); decode
+batch of 64 sequences with contexts uniform on 512..2048 tokens, paged KV in
+16-token blocks with shuffled block tables. One step = one stage_decode call
+(every layer: RMSNorm, QKV, q/k-RoPE + KV write, split-K paged attention,
+O-proj, RMSNorm, gate-up + SwiGLU, down). The same stage then runs a chunked
+prefill of 8 prompts of 1024..4096 tokens with a 2048-token budget per step.
+
+Prints one JSON line: decode tok/s as `value`, the roofline of the dominant
+kernel (timed with HIP events on the launch stream), the prefill figures,
+and the CPU oracle timed on a bounded sample on the host.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+METRIC = "stage decode tok/s + prefill tok/s on 1 GPU; % of HBM / MFMA roofline"
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def gemm_bytes(M, N, K, out_bytes):
+    """Algorithmic HBM bytes of one GEMM launch: W and A (bf16) read once,
+    the output written once."""
+    return N * K * 2 + M * K * 2 + M * N * out_bytes
+
+
+def decode_step_bytes(shape, n_layers, ctx_lens):
+    """Algorithmic bytes of one decode step: every weight once, the valid KV
+    of every sequence once per layer, the new KV and the hidden rows in/out."""
+    B = len(ctx_lens)
+    kv_tok = 2 * shape.n_kv_heads * shape.head_dim * 2
+    w = shape.params_per_layer() * 2
+    per_layer = w + int(np.sum(ctx_lens + 1)) * kv_tok
+    return n_layers * per_layer + 2 * B * shape.hidden * 2
+
+
+def prefill_flops(shape, n_layers, chunks):
+    """Algorithmic FLOPs of a chunked prefill: 2 * weights per token for the
+    GEMMs plus causal attention, 4 * d * n_q per (query, visible key)."""
+    lin = 2 * (shape.params_per_layer() - 2 * shape.hidden)
+    f = 0
+    for ctx, q in chunks:
+        pairs = q * ctx + q * (q + 1) / 2
+        f += q * lin + 4 * shape.head_dim * shape.n_q_heads * pairs
+    return n_layers * f
+
+
+def cpu_baseline(shape, ctx_lens, seed):
+    """The oracle (float32) on the host: one decode step of one layer for the
+    whole batch, scaled by the stage's 20 layers (every layer costs the same)."""
+    import torch
+    from oracle import stage_oracle as O
+    from paper_2606_18600_amd import synth
+    cfg = O.OracleConfig(shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
+                         shape.ffn, shape.rms_eps, shape.rope_theta)
+    w = synth.host_layer_weights(shape, seed, 20, dtype=np.float32)
+    B = len(ctx_lens)
+    nbps = (ctx_lens + 1 + 15) // 16
+    nb = int(nbps.sum())
+    kv = O.new_kv_cache(cfg, 1, nb, np.float32)
+    r = np.random.default_rng(seed)
+    kv[0]["k"][:] = r.standard_normal(kv[0]["k"].shape, dtype=np.float32)
+    kv[0]["v"][:] = r.standard_normal(kv[0]["v"].shape, dtype=np.float32)
+    starts = np.concatenate([[0], np.cumsum(nbps)])
+    seqs = [O.SeqSpec(int(c), 1, list(range(starts[i], starts[i + 1])))
+            for i, c in enumerate(ctx_lens)]
+    x = synth.hidden_states(seed, 9, B, shape.hidden)
+    O.stage_forward(cfg, [w], x[:2], seqs[:2], kv, dtype=np.float32)  # warm caches
+    t0 = time.perf_counter()
+    O.stage_forward(cfg, [w], x, seqs, kv, dtype=np.float32)
+    dt = time.perf_counter() - t0
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count()
+    step_s = dt * 20
+    return {"value": B / step_s, "unit": "tok/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"one decode step of one layer, batch {B} (contexts as the workload), "
+                      f"float32, {dt:.2f} s, scaled x20 layers"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--seed", type=int, default=2606)
+    ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: the stage runs on a single MI355X and this build "
+              f"has no multi-GPU path (asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_18600_amd import stage as S
+    from paper_2606_18600_amd import synth
+    from paper_2606_18600_amd.harness import DeviceStage, device_layer_weights
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    shape = synth.LLAMA70B
+    wl = synth.WORKLOADS["l70-decode"]
+    L0, L1 = wl.layer_begin, wl.layer_end
+    nL = L1 - L0
+    seed = args.seed
+    B, K, W = 64, args.steps, args.warmup
+
+    log(f"[bench] generating {nL} layers of {shape.name} weights on the device")
+    weights = [device_layer_weights(shape, seed, l, "bf16") for l in range(L0, L1)]
+    ctx0 = synth.uniform_lengths(seed, 1, B, 512, 2048)
+    steps_total = W + 2 * K
+    dec_final = ctx0 + steps_total + 1
+    dec_blocks = int(((dec_final + 15) // 16).sum())
+    p_lens = synth.uniform_lengths(seed, 2, 8, 1024, 4096)
+    pf_blocks = int(((p_lens + 15) // 16).sum())
+    num_blocks = dec_blocks + pf_blocks + 1
+    alloc = synth.BlockAllocator(num_blocks, seed)
+    dec_bt_np = synth.make_block_tables(dec_final, int(((dec_final + 15) // 16).max()), alloc)
+    pf_bt_np = synth.make_block_tables(p_lens, int(((p_lens + 15) // 16).max()), alloc)
+
+    st = DeviceStage(shape, "bf16", L0, weights, num_blocks, max_tokens=2048, max_seqs=B)
+    # Context KV: random N(0,1) values (decode cost does not depend on them).
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    st.kv_pool.normal_(0.0, 1.0, generator=g)
+    dec_bt = torch.from_numpy(dec_bt_np).to(dev)
+    xs = torch.empty((steps_total, B, shape.hidden), dtype=torch.bfloat16, device=dev)
+    xs.normal_(0.0, 1.0, generator=g)
+    out = torch.empty((B, shape.hidden), dtype=torch.bfloat16, device=dev)
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+
+    log(f"[bench] decode: B={B} ctx U[512,2048] mean {ctx0.mean():.0f}, warmup {W}, steps {K}")
+    i = 0
+    for _ in range(W):
+        st.decode(ctx0 + i, dec_bt, xs[i], out, stream=sp)
+        i += 1
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    ctx_timed = []
+    e0.record(stream)
+    for _ in range(K):
+        st.decode(ctx0 + i, dec_bt, xs[i], out, stream=sp)
+        ctx_timed.append(ctx0 + i)
+        i += 1
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / K
+    assert torch.isfinite(out.float()).all(), "non-finite stage output"
+    dec_tok_s = B / (ms / 1e3)
+    step_bytes = float(np.mean([decode_step_bytes(shape, nL, c) for c in ctx_timed]))
+    log(f"[bench] decode {ms:.3f} ms/step, {dec_tok_s:.0f} tok/s, "
+        f"{step_bytes / (ms / 1e3) / 1e9:.0f} GB/s algorithmic")
+
+    # per-op timing pass (HIP events on the launch stream, inside the library)
+    S.stage_set_op_timing(st.handle, True)
+    for _ in range(K):
+        st.decode(ctx0 + i, dec_bt, xs[i], out, stream=sp)
+        i += 1
+    op_ms, op_n = S.stage_read_op_times(st.handle)
+    S.stage_set_op_timing(st.handle, False)
+    ops = {S.OP_NAMES[j]: {"ms_per_step": op_ms[j] / K, "launches_per_step": op_n[j] / K}
+           for j in range(len(op_ms))}
+    gu_avg_ms = op_ms[S.OP_NAMES.index("gate_up")] / op_n[S.OP_NAMES.index("gate_up")]
+    gu_bytes = gemm_bytes(B, 2 * shape.ffn, shape.hidden, 4)
+    gu_gbs = gu_bytes / (gu_avg_ms / 1e3) / 1e9
+    log(f"[bench] ops ms/step: " + ", ".join(f"{k}={v['ms_per_step']:.3f}" for k, v in ops.items()))
+    log(f"[bench] gate_up split-K GEMM: {gu_avg_ms * 1e3:.1f} us/launch, {gu_gbs:.0f} GB/s")
+
+    result = {
+        "metric": METRIC, "value": round(dec_tok_s, 1), "unit": "tok/s", "n_gpus": 1,
+        "steps": K, "warmup": W, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic: random-init weights N(0,0.02^2) (gains 1+N(0,0.02^2)), "
+                "N(0,1) hidden inputs, random context KV, shuffled block tables",
+        "config": {"workload": "l70-decode: Llama-3.1-70B-shaped stage, layers [20,40), "
+                               "decode batch 64, contexts uniform 512-2048, KV block 16",
+                   "layers": nL, "batch": B, "hidden": shape.hidden, "block": 16},
+        "roofline": {"bound": "hbm", "kernel": "gemm_skinny_bf16 (gate-up, split-K)",
+                     "achieved": round(gu_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gu_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "bytes_per_launch": gu_bytes, "us_per_launch": round(gu_avg_ms * 1e3, 2)},
+        "step_roofline": {"bound": "hbm", "algorithmic_bytes": step_bytes,
+                          "roofline_ms": round(step_bytes / (HBM_PEAK_GBS * 1e9) * 1e3, 4),
+                          "measured_ms": round(ms, 4),
+                          "frac": round(step_bytes / (HBM_PEAK_GBS * 1e9) / (ms / 1e3), 4)},
+        "ops_ms_per_step": {k: round(v["ms_per_step"], 4) for k, v in ops.items()},
+    }
+
+    if not args.no_prefill:
+        pf_bt = torch.from_numpy(pf_bt_np).to(dev)
+        steps = synth.chunk_schedule(p_lens, 2048)
+        xin = torch.empty((2048, shape.hidden), dtype=torch.bfloat16, device=dev)
+        xin.normal_(0.0, 1.0, generator=g)
+        pout = torch.empty_like(xin)
+
+        def run_prefill():
+            for stp in steps:
+                idx = [s[0] for s in stp]
+                T = sum(s[2] for s in stp)
+                st.prefill([s[2] for s in stp], [s[1] for s in stp], pf_bt[idx].contiguous(),
+                           xin[:T], pout[:T], stream=sp)
+
+        log(f"[bench] prefill: 8 prompts, {int(p_lens.sum())} tokens, {len(steps)} chunks")
+        run_prefill()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        run_prefill()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        pms = e0.elapsed_time(e1)
+        ptok = float(p_lens.sum())
+        chunks = [(s[1], s[2]) for stp in steps for s in stp]
+        pfl = prefill_flops(shape, nL, chunks)
+        S.stage_set_op_timing(st.handle, True)
+        run_prefill()
+        op_ms, op_n = S.stage_read_op_times(st.handle)
+        S.stage_set_op_timing(st.handle, False)
+        j = S.OP_NAMES.index("gate_up")
+        # full 2048-token chunks dominate; FLOPs per launch from the mean chunk size
+        mean_T = ptok / len(steps)
+        gu_fl = 2.0 * mean_T * 2 * shape.ffn * shape.hidden
+        gu_tfs = gu_fl / (op_ms[j] / op_n[j] / 1e3) / 1e12
+        result["prefill"] = {
+            "workload": "l70-prefill: same stage, 8 prompts uniform 1024-4096, chunked prefill, "
+                        "2048-token budget",
+            "tok_s": round(ptok / (pms / 1e3), 1), "ms_total": round(pms, 3),
+            "algorithmic_tflop": round(pfl / 1e12, 2),
+            "tflops": round(pfl / (pms / 1e3) / 1e12, 1),
+            "frac_mfma_peak": round(pfl / (pms / 1e3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+            "ops_ms": {S.OP_NAMES[k]: round(op_ms[k], 3) for k in range(len(op_ms))},
+            "gate_up_tflops": round(gu_tfs, 1),
+        }
+        log(f"[bench] prefill {pms:.1f} ms, {ptok / (pms / 1e3):.0f} tok/s, "
+            f"{pfl / (pms / 1e3) / 1e12:.0f} TFLOP/s; gate_up {gu_tfs:.0f} TFLOP/s")
+
+    st.close()
+    del weights
+    torch.cuda.empty_cache()
+
+    if not args.no_cpu:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(shape, ctx0, seed)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,202 @@
+/*
+ * stage.h -- C ABI of the MI355X pipeline-stage forward pass.
+ *
+ * What a stage is. ShuntServe splits a decoder-only LLM into pipeline stages,
+ * each a contiguous range of transformer layers placed on one device
+ * (Sec. 2.3, "Uneven Layer Partitioning in PP"; Algorithm 1 adds one stage of
+ * l - l' consecutive layers at a time). Stages exchange only hidden states of
+ * B*S*H*E bytes (Sec. 4.1.2, Eq. 2). Per layer the work is the QKV
+ * projection, attention, output projection, up-and-gate projection and down
+ * projection of Table 2 (Sec. 4.1.1), with prefill compute-bound and decode
+ * memory-bound (Sec. 2.3, "The Optimization Challenge"; Sec. 4.2.2). The
+ * weights and the KV-cache space live in a store separate from the engine
+ * and are referenced zero-copy (Sec. 5.2, "Shared Tensor Store"); this ABI
+ * therefore only borrows device memory and never allocates it.
+ *
+ * A layer is the pre-norm Llama-3 / Qwen3 block of the models the paper
+ * serves (Sec. 7): RMSNorm -> fused QKV projection -> (Qwen3: per-head q/k
+ * RMSNorm) -> rotary embedding (rotate-half pairing, angle p*theta^(-2j/d))
+ * -> causal grouped-query attention over a paged KV cache (query head h reads
+ * kv head h / (n_q/n_kv), scale 1/sqrt(d)) -> output projection + residual
+ * -> RMSNorm -> SwiGLU FFN (silu(x Wg^T) * (x Wu^T)) -> down projection +
+ * residual.
+ *
+ * Conventions shared by every entry point:
+ *  - Weights are row-major [N, K] and applied as y = x W^T. w_qkv stacks the
+ *    n_q*d query rows, then n_kv*d key rows, then n_kv*d value rows;
+ *    w_gate_up stacks ffn gate rows then ffn up rows. Norm gains are [hidden];
+ *    q/k-norm gains are [head_dim]. All weights are stored in the mode dtype.
+ *  - KV pool (one allocation for the stage's layers):
+ *      [n_layers][num_blocks][n_kv][2][block_size][head_dim]
+ *    in the mode dtype. Plane 0 holds K as [token][d]; plane 1 holds V
+ *    transposed, [d][token]. Token p of a sequence with block table bt lives
+ *    in block bt[p / block_size] at offset p % block_size. Block ids index
+ *    the same blocks in every layer of the stage.
+ *  - hidden_in / hidden_out: [T, hidden] in the mode dtype, rows packed
+ *    sequence by sequence in batch order (for stage_step_mixed: all prefill
+ *    rows first, then the decode rows). hidden_out may alias hidden_in.
+ *    Inside a call the residual stream is kept in fp32.
+ *  - Every call only enqueues work on `stream` (a hipStream_t; NULL = the
+ *    default stream) and returns; outputs are valid once the stream has
+ *    reached that point. Host arrays may be reused as soon as the call
+ *    returns.
+ *  - Errors: host-side arguments are validated before anything is enqueued;
+ *    on failure the call returns a non-zero stage_status, enqueues nothing
+ *    and stage_last_error() describes the failure. Device faults surface at
+ *    stream synchronisation as HIP errors. No entry point throws or aborts.
+ *  - A stage_t is not thread-safe; distinct stages may be used from
+ *    different threads.
+ */
+#ifndef STAGE_H_
+#define STAGE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct stage stage_t; /* opaque */
+
+typedef enum {
+  STAGE_OK = 0,
+  STAGE_ERR_INVALID_ARG = 1, /* null pointer, bad length, inconsistent batch */
+  STAGE_ERR_UNSUPPORTED = 2, /* shape or dtype this build does not implement */
+  STAGE_ERR_OUT_OF_MEMORY = 3, /* host allocation failed */
+  STAGE_ERR_DEVICE = 4,      /* a HIP call failed (no device, launch error) */
+  STAGE_ERR_CAPACITY = 5     /* batch exceeds max_tokens / max_seqs / table
+                                capacity / max_position / workspace */
+} stage_status;
+
+typedef enum { STAGE_F32 = 0, STAGE_BF16 = 1 } stage_dtype;
+
+/* Shape and constants of one decoder layer.
+ * Supported: head_dim in {64, 128}; n_q_heads % n_kv_heads == 0 with group
+ * size n_q/n_kv in {1, 2, 4, 8, 16}; block_size == 16; hidden % 128 == 0;
+ * (n_q_heads * head_dim) % 128 == 0; ffn % 64 == 0. */
+typedef struct {
+  int32_t hidden;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t ffn;
+  int32_t qk_norm;      /* 1: per-head RMSNorm of q and k (Qwen3), else 0 */
+  int32_t block_size;   /* KV block size in tokens; must be 16 */
+  float rms_eps;        /* epsilon of the two layer RMSNorms */
+  float qk_rms_eps;     /* epsilon of the q/k RMSNorm */
+  double rope_theta;    /* rotary base */
+  int32_t max_position; /* positions are in [0, max_position) */
+  stage_dtype dtype;    /* storage dtype of weights, KV and hidden states */
+} stage_model_config;
+
+/* Device pointers to one layer's weights (q_norm/k_norm may be NULL unless
+ * qk_norm is set). */
+typedef struct {
+  const void* attn_norm; /* [hidden] */
+  const void* w_qkv;     /* [(n_q + 2 n_kv) * head_dim, hidden] */
+  const void* q_norm;    /* [head_dim] */
+  const void* k_norm;    /* [head_dim] */
+  const void* w_o;       /* [hidden, n_q * head_dim] */
+  const void* ffn_norm;  /* [hidden] */
+  const void* w_gate_up; /* [2 * ffn, hidden] */
+  const void* w_down;    /* [hidden, ffn] */
+} stage_layer_weights;
+
+/* One request batch. q_lens/ctx_lens are HOST arrays; block_tables is a
+ * DEVICE array. Sequence i contributes q_lens[i] consecutive rows to
+ * hidden_in, at positions ctx_lens[i] .. ctx_lens[i] + q_lens[i] - 1; its
+ * first ctx_lens[i] tokens must already be in the KV cache (written by
+ * earlier calls), and the call writes the keys and values of the new ones. */
+typedef struct {
+  int32_t num_seqs;
+  const int32_t* q_lens;        /* host [num_seqs], each >= 1 */
+  const int32_t* ctx_lens;      /* host [num_seqs], each >= 0 */
+  const int32_t* block_tables;  /* device [num_seqs][max_blocks_per_seq] */
+  int32_t max_blocks_per_seq;
+} stage_batch;
+
+/* Create a stage over layers [layer_begin, layer_end) of a model.
+ *  layers:   host array of layer_end - layer_begin weight sets (device
+ *            pointers, borrowed: they must outlive the stage).
+ *  kv_pool:  device pointer to the KV pool (layout above), borrowed.
+ *  num_blocks: blocks per layer in kv_pool.
+ *  max_tokens: largest T of any call; max_seqs: largest number of sequences
+ *            (prefill + decode) of any call. They size the workspace.
+ * The stage keeps host-side state only (including a small pinned staging
+ * buffer); device scratch memory is supplied by stage_bind_workspace.
+ * Returns STAGE_ERR_DEVICE if no HIP device is usable. */
+stage_status stage_create(const stage_model_config* cfg, int32_t layer_begin, int32_t layer_end,
+                          const stage_layer_weights* layers, void* kv_pool, int32_t num_blocks,
+                          int32_t max_tokens, int32_t max_seqs, stage_t** out);
+
+/* Bytes of device workspace the stage needs (activations, metadata, decode
+ * split partials, the rotary cos/sin table). */
+size_t stage_workspace_bytes(const stage_t* st);
+
+/* Bind caller-owned device memory of at least stage_workspace_bytes() bytes
+ * (256-byte aligned). Synchronously uploads the rotary table and clears the
+ * accumulators. Must be called before the first forward call; may be called
+ * again to move the workspace. */
+stage_status stage_bind_workspace(stage_t* st, void* dev, size_t bytes);
+
+/* Prefill (or chunked prefill / recomputation): every sequence has
+ * q_lens >= 1 new tokens. */
+stage_status stage_prefill(stage_t* st, const stage_batch* batch, const void* hidden_in,
+                           void* hidden_out, void* stream);
+
+/* Decode: every sequence has exactly one new token (q_lens[i] == 1). */
+stage_status stage_decode(stage_t* st, const stage_batch* batch, const void* hidden_in,
+                          void* hidden_out, void* stream);
+
+/* One continuous-batching step: a prefill batch (may be NULL or empty) and a
+ * decode batch (may be NULL or empty) in one pass over the layers. Rows of
+ * hidden_in: prefill rows first, then decode rows. A sequence must not
+ * appear in both batches. */
+stage_status stage_step_mixed(stage_t* st, const stage_batch* prefill, const stage_batch* decode,
+                              const void* hidden_in, void* hidden_out, void* stream);
+
+/* Destroy a stage (does not free any borrowed memory). NULL is allowed. */
+stage_status stage_destroy(stage_t* st);
+
+/* Description of the last failure on this thread ("" if none). */
+const char* stage_last_error(void);
+
+/* Host-only check of a step against a configuration and the stage limits,
+ * with exactly the checks (and return codes) the forward entry points apply
+ * before enqueuing anything. Touches no device memory (block_tables is only
+ * checked for NULL). Useful for admission control in a scheduler. */
+stage_status stage_validate_step(const stage_model_config* cfg, int32_t max_tokens,
+                                 int32_t max_seqs, const stage_batch* prefill,
+                                 const stage_batch* decode);
+
+/* ---- measurement hooks ------------------------------------------------ */
+
+/* Operation classes timed by the op-timing hook. */
+typedef enum {
+  STAGE_OP_NORM = 0,      /* RMSNorms, input/output conversion, SwiGLU */
+  STAGE_OP_QKV = 1,       /* QKV projection */
+  STAGE_OP_ROPE_KV = 2,   /* q/k norm + RoPE + KV write */
+  STAGE_OP_ATTN = 3,      /* attention (prefill + decode + merge) */
+  STAGE_OP_O = 4,         /* output projection + residual */
+  STAGE_OP_GATE_UP = 5,   /* gate-up projection (+ SwiGLU when fused) */
+  STAGE_OP_DOWN = 6,      /* down projection + residual */
+  STAGE_OP_COUNT = 7
+} stage_op;
+
+/* Enable (1) or disable (0) HIP-event timing of each op class. While
+ * enabled, every launch of the stage is bracketed by events on the call's
+ * stream (adding a little overhead). */
+stage_status stage_set_op_timing(stage_t* st, int32_t enable);
+
+/* Synchronise the recorded events and return, per op class, the summed
+ * milliseconds and the number of launches since timing was enabled or last
+ * read; then reset the counters. ms and launches have STAGE_OP_COUNT
+ * entries. */
+stage_status stage_read_op_times(stage_t* st, double* ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* STAGE_H_ */

@@ -1,0 +1,418 @@
+// Causal grouped-query attention over the paged KV cache.
+//
+// Cache geometry per layer: [num_blocks][n_kv][2][16][d]; plane 0 holds K as
+// [token][d], plane 1 holds V transposed as [d][token]. With that layout every
+// MFMA operand is a contiguous load:
+//   S^T[key][row] = K[key][:] . Q[row][:]        v_mfma_f32_16x16x32_bf16
+//   O^T[d][row]  += V^T[d][key] . P^T[key][row]  v_mfma_f32_16x16x16_bf16
+// The C layout of the first product (lane l: row l%16, keys (l/16)*4 + r) is
+// exactly the B layout the second needs, and each lane keeps the online
+// softmax statistics of its own row, so no cross-lane shuffles are needed
+// beyond the 4-lane row reductions.
+//
+// * attn_decode_bf16: one wave per (decode token, kv head, key split); the 16
+//   MFMA rows are the G query heads sharing the kv head (padded to 16).
+//   Partial (max, sum, unnormalised output) go to a workspace, and
+//   attn_merge_kernel combines the splits.
+// * attn_prefill_bf16: one wave per (query chunk of a sequence, kv head);
+//   rows are (position, head) pairs of the chunk, keys run from 0 to the
+//   last position of the chunk (the chunk's own keys are already in the
+//   cache), with the causal mask applied per row.
+// * attn_f32_kernel: plain fp32 SIMT attention, one wave per (token, head),
+//   for the fp32 mode.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace stage_k {
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ __forceinline__ const int32_t* seq_table(const SegTables& t, int seq) {
+  return seq < t.nseq0 ? t.bt0 + (size_t)seq * t.stride0
+                       : t.bt1 + (size_t)(seq - t.nseq0) * t.stride1;
+}
+
+// K fragment of one 16-token block: lane l holds token l%16, d offsets
+// (l/16)*(D/4) .. +D/4 (NJ chunks of 8).
+template <int D>
+struct KFrag {
+  static constexpr int NJ = D / 32;
+  u32x4_t v[NJ];
+  __device__ __forceinline__ void load(const bf16_t* kplane, int lane) {
+    const bf16_t* p = kplane + (lane & 15) * D + (lane >> 4) * (D / 4);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) v[j] = ldg128(p + j * 8);
+  }
+};
+
+// V^T fragments of one block: for d tile dt, lane l holds d = dt*16 + l%16,
+// tokens (l/16)*4 .. +3.
+template <int D>
+struct VFrag {
+  static constexpr int NT = D / 16;
+  u32x2_t v[NT];
+  __device__ __forceinline__ void load(const bf16_t* vplane, int lane) {
+    const bf16_t* p = vplane + (lane & 15) * kBlock + (lane >> 4) * 4;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) v[t] = ldg64(p + t * 16 * kBlock);
+  }
+};
+
+// Online-softmax state of the row owned by this lane (row l%16 of a tile).
+struct RowState {
+  float m, l;
+};
+
+// Process one key block for one 16-row tile: scores -> P -> O^T update.
+// `s` holds the 4 raw scores (already scaled to log2 units and masked).
+template <int D>
+__device__ __forceinline__ void softmax_pv(f32x4_t s, RowState& st, f32x4_t* oacc,
+                                           const VFrag<D>& vf) {
+  float bm = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
+  bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
+  bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
+  const float mn = fmaxf(st.m, bm);
+  // A row can only be fully masked in a block after an earlier block gave it
+  // a finite max, so mn is finite here.
+  const float alpha = exp2f(st.m - mn);
+  float p[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) p[r] = exp2f(s[r] - mn);
+  float ps = p[0] + p[1] + p[2] + p[3];
+  ps += __shfl_xor(ps, 16, 64);
+  ps += __shfl_xor(ps, 32, 64);
+  st.l = st.l * alpha + ps;
+  st.m = mn;
+  u32x2_t pb;
+  pb[0] = pack_bf16x2(p[0], p[1]);
+  pb[1] = pack_bf16x2(p[2], p[3]);
+#pragma unroll
+  for (int t = 0; t < D / 16; ++t) {
+    oacc[t] *= alpha;
+    oacc[t] = mfma16x16x16(vf.v[t], pb, oacc[t]);
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void attn_decode_bf16(const bf16_t* __restrict__ q,
+                                                        const bf16_t* __restrict__ kv, int n_kv,
+                                                        SegTables tabs,
+                                                        const DecodeItem* __restrict__ items,
+                                                        int n_q, float* __restrict__ part_o,
+                                                        float* __restrict__ part_ml) {
+  const int lane = threadIdx.x & 63;
+  const int kvh = blockIdx.y * 4 + (threadIdx.x >> 6);
+  if (kvh >= n_kv) return;
+  const DecodeItem it = items[blockIdx.x];
+  const int G = n_q / n_kv;
+  const int row = lane & 15;  // query head within the group
+  const bool row_ok = row < G;
+  const float scale = kLog2e / sqrtf((float)D);
+
+  // Q^T fragments (B operand): lane l holds head row, same d offsets as K.
+  constexpr int NJ = D / 32;
+  u32x4_t qf[NJ];
+  {
+    const bf16_t* qp = q + ((size_t)it.tok * n_q + kvh * G + (row_ok ? row : 0)) * D +
+                       (lane >> 4) * (D / 4);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) qf[j] = row_ok ? ldg128(qp + j * 8) : u32x4_t{0u, 0u, 0u, 0u};
+  }
+
+  const int32_t* bt = seq_table(tabs, it.seq);
+  const size_t plane = (size_t)kBlock * D;
+  const size_t head_stride = 2 * plane;
+  RowState st{-INFINITY, 0.f};
+  f32x4_t oacc[D / 16];
+#pragma unroll
+  for (int t = 0; t < D / 16; ++t) oacc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int b0 = it.k0 / kBlock, b1 = (it.k1 + kBlock - 1) / kBlock;
+  KFrag<D> kf;
+  VFrag<D> vf;
+  {
+    const bf16_t* kp = kv + ((size_t)bt[b0] * n_kv + kvh) * head_stride;
+    kf.load(kp, lane);
+    vf.load(kp + plane, lane);
+  }
+  for (int b = b0; b < b1; ++b) {
+    KFrag<D> kn;
+    VFrag<D> vn;
+    if (b + 1 < b1) {
+      const bf16_t* kp = kv + ((size_t)bt[b + 1] * n_kv + kvh) * head_stride;
+      kn.load(kp, lane);
+      vn.load(kp + plane, lane);
+    }
+    f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) s = mfma16x16x32(kf.v[j], qf[j], s);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int key = b * kBlock + (lane >> 4) * 4 + r;
+      s[r] = key < it.k1 ? s[r] * scale : -INFINITY;
+    }
+    softmax_pv<D>(s, st, oacc, vf);
+    if (b + 1 < b1) {
+      kf = kn;
+      vf = vn;
+    }
+  }
+
+  if (!row_ok) return;
+  const size_t ob = ((size_t)blockIdx.x * n_q + kvh * G + row);
+  float* po = part_o + ob * D;
+#pragma unroll
+  for (int t = 0; t < D / 16; ++t)
+    *(f32x4_t*)(po + t * 16 + (lane >> 4) * 4) = oacc[t];
+  if (lane < 16) {
+    part_ml[ob * 2 + 0] = st.m;
+    part_ml[ob * 2 + 1] = st.l;
+  }
+}
+
+// Combine the key splits of each decode token: one wave per (token, head).
+template <typename OutT>
+__global__ __launch_bounds__(256) void attn_merge_kernel(const float* __restrict__ part_o,
+                                                         const float* __restrict__ part_ml,
+                                                         const int32_t* __restrict__ item_start,
+                                                         const int32_t* __restrict__ tok_rows,
+                                                         int n_q, int D, OutT* __restrict__ out) {
+  const int t = blockIdx.x;
+  const int h = blockIdx.y * 4 + (threadIdx.x >> 6);
+  if (h >= n_q) return;
+  const int lane = threadIdx.x & 63;
+  const int i0 = item_start[t], i1 = item_start[t + 1];
+  float M = -INFINITY;
+  for (int i = i0; i < i1; ++i) M = fmaxf(M, part_ml[((size_t)i * n_q + h) * 2]);
+  float L = 0.f, o0 = 0.f, o1 = 0.f;
+  for (int i = i0; i < i1; ++i) {
+    const size_t b = (size_t)i * n_q + h;
+    const float w = exp2f(part_ml[b * 2] - M);
+    L += w * part_ml[b * 2 + 1];
+    o0 += w * part_o[b * D + lane];
+    if (D > 64) o1 += w * part_o[b * D + lane + 64];
+  }
+  const float inv = 1.0f / L;
+  OutT* op = out + ((size_t)tok_rows[t] * n_q + h) * D;
+  elem<OutT>::store(op, lane, o0 * inv);
+  if (D > 64) elem<OutT>::store(op, lane + 64, o1 * inv);
+}
+
+// Prefill: one wave per (item, kv head); RT tiles of 16 rows, row r of the
+// wave is position r / G and head kvh*G + r % G.
+template <int D, int RT>
+__global__ __launch_bounds__(256) void attn_prefill_bf16(const bf16_t* __restrict__ q,
+                                                         const bf16_t* __restrict__ kv, int n_kv,
+                                                         SegTables tabs,
+                                                         const PrefillItem* __restrict__ items,
+                                                         int n_q, bf16_t* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const int kvh = blockIdx.y * 4 + (threadIdx.x >> 6);
+  if (kvh >= n_kv) return;
+  const PrefillItem it = items[blockIdx.x];
+  const int G = n_q / n_kv;
+  const float scale = kLog2e / sqrtf((float)D);
+  constexpr int NJ = D / 32;
+
+  int rpos[RT];  // position of this lane's row in each tile
+  bool rok[RT];
+  u32x4_t qf[RT][NJ];
+#pragma unroll
+  for (int i = 0; i < RT; ++i) {
+    const int r = i * 16 + (lane & 15);
+    const int pi = r / G;
+    rok[i] = pi < it.npos;
+    const int pc = rok[i] ? pi : it.npos - 1;
+    rpos[i] = it.p0 + pc;
+    const bf16_t* qp = q + ((size_t)(it.t0 + pc) * n_q + kvh * G + r % G) * D +
+                       (lane >> 4) * (D / 4);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) qf[i][j] = ldg128(qp + j * 8);
+  }
+
+  const int32_t* bt = seq_table(tabs, it.seq);
+  const size_t plane = (size_t)kBlock * D;
+  const size_t head_stride = 2 * plane;
+  RowState st[RT];
+  f32x4_t oacc[RT][D / 16];
+#pragma unroll
+  for (int i = 0; i < RT; ++i) {
+    st[i] = RowState{-INFINITY, 0.f};
+#pragma unroll
+    for (int t = 0; t < D / 16; ++t) oacc[i][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  }
+
+  const int kend = it.p0 + it.npos;  // keys [0, kend)
+  const int nb = (kend + kBlock - 1) / kBlock;
+  KFrag<D> kf;
+  VFrag<D> vf;
+  {
+    const bf16_t* kp = kv + ((size_t)bt[0] * n_kv + kvh) * head_stride;
+    kf.load(kp, lane);
+    vf.load(kp + plane, lane);
+  }
+  for (int b = 0; b < nb; ++b) {
+    KFrag<D> kn;
+    VFrag<D> vn;
+    if (b + 1 < nb) {
+      const bf16_t* kp = kv + ((size_t)bt[b + 1] * n_kv + kvh) * head_stride;
+      kn.load(kp, lane);
+      vn.load(kp + plane, lane);
+    }
+#pragma unroll
+    for (int i = 0; i < RT; ++i) {
+      f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) s = mfma16x16x32(kf.v[j], qf[i][j], s);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int key = b * kBlock + (lane >> 4) * 4 + r;
+        s[r] = key <= rpos[i] ? s[r] * scale : -INFINITY;
+      }
+      softmax_pv<D>(s, st[i], oacc[i], vf);
+    }
+    if (b + 1 < nb) {
+      kf = kn;
+      vf = vn;
+    }
+  }
+
+#pragma unroll
+  for (int i = 0; i < RT; ++i) {
+    if (!rok[i]) continue;
+    const int r = i * 16 + (lane & 15);
+    const float inv = 1.0f / st[i].l;
+    bf16_t* op = out + ((size_t)(it.t0 + r / G) * n_q + kvh * G + r % G) * D + (lane >> 4) * 4;
+#pragma unroll
+    for (int t = 0; t < D / 16; ++t) {
+      u32x2_t w;
+      w[0] = pack_bf16x2(oacc[i][t][0] * inv, oacc[i][t][1] * inv);
+      w[1] = pack_bf16x2(oacc[i][t][2] * inv, oacc[i][t][3] * inv);
+      *(u32x2_t*)(op + t * 16) = w;
+    }
+  }
+}
+
+// fp32 mode: one wave per (token, query head), keys [0, pos] of its sequence.
+__global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__ q,
+                                                       const float* __restrict__ kv, int n_kv,
+                                                       int D, SegTables tabs,
+                                                       const int32_t* __restrict__ tok_seq,
+                                                       const int32_t* __restrict__ tok_pos,
+                                                       int t_begin, int n_q,
+                                                       float* __restrict__ out) {
+  const int t = t_begin + blockIdx.x;
+  const int h = blockIdx.y * 4 + (threadIdx.x >> 6);
+  if (h >= n_q) return;
+  const int lane = threadIdx.x & 63;
+  const int kvh = h / (n_q / n_kv);
+  const int pos = tok_pos[t];
+  const int32_t* bt = seq_table(tabs, tok_seq[t]);
+  const float* qp = q + ((size_t)t * n_q + h) * D;
+  const float scale = 1.0f / sqrtf((float)D);
+  const size_t plane = (size_t)kBlock * D;
+  float m = -INFINITY, l = 0.f, o0 = 0.f, o1 = 0.f;
+  for (int c0 = 0; c0 <= pos; c0 += 64) {
+    const int key = c0 + lane;
+    float s = -INFINITY;
+    if (key <= pos) {
+      const float* kp = kv + ((size_t)bt[key / kBlock] * n_kv + kvh) * 2 * plane +
+                        (key % kBlock) * D;
+      float acc = 0.f;
+      for (int e = 0; e < D; ++e) acc = fmaf(qp[e], kp[e], acc);
+      s = acc * scale;
+    }
+    const float cm = wave_max(s);
+    const float mn = fmaxf(m, cm);
+    const float alpha = expf(m - mn);
+    const float p = key <= pos ? expf(s - mn) : 0.f;
+    l = l * alpha + wave_sum(p);
+    o0 *= alpha;
+    o1 *= alpha;
+    const int nk = min(64, pos + 1 - c0);
+    for (int j = 0; j < nk; ++j) {
+      const float pj = __shfl(p, j, 64);
+      const int kj = c0 + j;
+      const float* vp = kv + ((size_t)bt[kj / kBlock] * n_kv + kvh) * 2 * plane + plane +
+                        (kj % kBlock);
+      o0 = fmaf(pj, vp[(size_t)lane * kBlock], o0);
+      if (D > 64) o1 = fmaf(pj, vp[(size_t)(lane + 64) * kBlock], o1);
+    }
+    m = mn;
+  }
+  float* op = out + ((size_t)t * n_q + h) * D;
+  op[lane] = o0 / l;
+  if (D > 64) op[lane + 64] = o1 / l;
+}
+
+constexpr int kPrefillRT = 2;
+
+}  // namespace
+
+int prefill_item_positions(DType dt, int group) {
+  (void)dt;
+  return kPrefillRT * 16 / group;
+}
+
+hipError_t attn_decode(DType dt, const void* q, KVLayer kv, SegTables tabs,
+                       const DecodeItem* items, int n_items, int n_q, float* part_o,
+                       float* part_ml, hipStream_t s) {
+  if (n_items == 0) return hipSuccess;
+  if (dt != DT_BF16) return hipErrorInvalidValue;
+  dim3 grid(n_items, (kv.n_kv + 3) / 4);
+  if (kv.head_dim == 128)
+    attn_decode_bf16<128><<<grid, 256, 0, s>>>((const bf16_t*)q, (const bf16_t*)kv.base, kv.n_kv,
+                                               tabs, items, n_q, part_o, part_ml);
+  else if (kv.head_dim == 64)
+    attn_decode_bf16<64><<<grid, 256, 0, s>>>((const bf16_t*)q, (const bf16_t*)kv.base, kv.n_kv,
+                                              tabs, items, n_q, part_o, part_ml);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t attn_merge(DType dt, const float* part_o, const float* part_ml,
+                      const int32_t* tok_item_start, const int32_t* tok_rows, int n_tok, int n_q,
+                      int head_dim, void* out, hipStream_t s) {
+  if (n_tok == 0) return hipSuccess;
+  dim3 grid(n_tok, (n_q + 3) / 4);
+  if (dt == DT_BF16)
+    attn_merge_kernel<bf16_t><<<grid, 256, 0, s>>>(part_o, part_ml, tok_item_start, tok_rows, n_q,
+                                                   head_dim, (bf16_t*)out);
+  else
+    attn_merge_kernel<float><<<grid, 256, 0, s>>>(part_o, part_ml, tok_item_start, tok_rows, n_q,
+                                                  head_dim, (float*)out);
+  return hipGetLastError();
+}
+
+hipError_t attn_prefill(DType dt, const void* q, KVLayer kv, SegTables tabs,
+                        const PrefillItem* items, int n_items, int n_q, void* out,
+                        hipStream_t s) {
+  if (n_items == 0) return hipSuccess;
+  if (dt != DT_BF16) return hipErrorInvalidValue;
+  dim3 grid(n_items, (kv.n_kv + 3) / 4);
+  if (kv.head_dim == 128)
+    attn_prefill_bf16<128, kPrefillRT><<<grid, 256, 0, s>>>(
+        (const bf16_t*)q, (const bf16_t*)kv.base, kv.n_kv, tabs, items, n_q, (bf16_t*)out);
+  else if (kv.head_dim == 64)
+    attn_prefill_bf16<64, kPrefillRT><<<grid, 256, 0, s>>>(
+        (const bf16_t*)q, (const bf16_t*)kv.base, kv.n_kv, tabs, items, n_q, (bf16_t*)out);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t attn_f32(const float* q, KVLayer kv, SegTables tabs, const int32_t* tok_seq,
+                    const int32_t* tok_pos, int t_begin, int n_tok, int n_q, float* out,
+                    hipStream_t s) {
+  if (n_tok == 0) return hipSuccess;
+  if (kv.head_dim != 64 && kv.head_dim != 128) return hipErrorInvalidValue;
+  dim3 grid(n_tok, (n_q + 3) / 4);
+  attn_f32_kernel<<<grid, 256, 0, s>>>(q, (const float*)kv.base, kv.n_kv, kv.head_dim, tabs,
+                                       tok_seq, tok_pos, t_begin, n_q, out);
+  return hipGetLastError();
+}
+
+}  // namespace stage_k

@@ -1,0 +1,98 @@
+// Host-side launchers of the stage kernels. Every launcher enqueues on the
+// given stream and returns the launch status; none allocates memory.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace stage_k {
+
+enum DType { DT_F32 = 0, DT_BF16 = 1 };
+
+// GEMM epilogues. The GEMM computes acc[m][n] = sum_k A[m][k] * W[n][k]
+// (A row-major [M,K], W row-major [N,K]).
+enum Epilogue {
+  EPI_STORE_F32 = 0,  // out (fp32, [M, N]) = acc
+  EPI_RESID_ADD = 1,  // out (fp32 residual, [M, N]) += acc
+  EPI_SWIGLU = 2,     // W = [gate (N/2 rows); up (N/2 rows)]; out (mode dtype, [M, N/2]) = silu(g) * u
+  EPI_ATOMIC_F32 = 3  // out (fp32, [M, N]) += acc with atomics (split-K partial sums)
+};
+
+// Block tables of the (at most) two segments of a step: sequences
+// [0, nseq0) read table 0, sequences [nseq0, ...) read table 1.
+struct SegTables {
+  const int32_t* bt0;
+  int32_t stride0;
+  int32_t nseq0;
+  const int32_t* bt1;
+  int32_t stride1;
+};
+
+// KV cache geometry of one layer: [num_blocks][n_kv][2][block][d]; plane 0
+// holds K as [block][d], plane 1 holds V transposed as [d][block].
+struct KVLayer {
+  void* base;
+  int32_t n_kv;
+  int32_t head_dim;
+};
+
+constexpr int kBlock = 16;
+
+// Decode split-K work item: one decode token attending keys [k0, k1).
+struct DecodeItem {
+  int32_t tok;  // row of the token in the step
+  int32_t seq;  // sequence index (segment-global)
+  int32_t k0;
+  int32_t k1;
+};
+
+// Prefill work item: rows t0 .. t0+npos-1 of one sequence, at positions
+// p0 .. p0+npos-1, attending keys [0, p0+npos).
+struct PrefillItem {
+  int32_t seq;
+  int32_t t0;
+  int32_t p0;
+  int32_t npos;
+};
+
+hipError_t embed_norm(DType dt, const void* hidden_in, float* x, void* h, const void* gain,
+                      int T, int H, float eps, hipStream_t s);
+hipError_t rmsnorm(DType dt, const float* x, void* h, const void* gain, int T, int H, float eps,
+                   hipStream_t s);
+hipError_t output_cast(DType dt, const float* x, void* out, size_t n, hipStream_t s);
+hipError_t fill_zero_f32(float* p, size_t n, hipStream_t s);
+
+hipError_t rope_kv_write(DType dt, float* qkv, int zero_after, void* q_out, KVLayer kv,
+                         const int32_t* tok_seq, const int32_t* tok_pos, SegTables tabs,
+                         const float* cos_tab, const float* sin_tab, const void* q_gain,
+                         const void* k_gain, float qk_eps, int T, int n_q, hipStream_t s);
+
+hipError_t swiglu(DType dt, float* gu, void* m, int T, int F, int zero_after, hipStream_t s);
+
+// GEMMs. `skinny` selects the split-K weight-streaming kernel (EPI_ATOMIC_F32
+// or EPI_RESID_ADD only), else the LDS-tiled kernel.
+hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int N, int K,
+                void* out, hipStream_t s);
+hipError_t gemm_skinny(DType dt, const void* A, const void* W, int M, int N, int K, float* out,
+                       int k_split, hipStream_t s);
+
+hipError_t attn_decode(DType dt, const void* q, KVLayer kv, SegTables tabs,
+                       const DecodeItem* items, int n_items, int n_q, float* part_o,
+                       float* part_ml, hipStream_t s);
+hipError_t attn_merge(DType dt, const float* part_o, const float* part_ml,
+                      const int32_t* tok_item_start, const int32_t* tok_rows, int n_tok, int n_q,
+                      int head_dim, void* out, hipStream_t s);
+hipError_t attn_prefill(DType dt, const void* q, KVLayer kv, SegTables tabs,
+                        const PrefillItem* items, int n_items, int n_q, void* out,
+                        hipStream_t s);
+
+// fp32 mode: one wave per (token, head) over rows [t_begin, t_begin + n_tok).
+hipError_t attn_f32(const float* q, KVLayer kv, SegTables tabs, const int32_t* tok_seq,
+                    const int32_t* tok_pos, int t_begin, int n_tok, int n_q, float* out,
+                    hipStream_t s);
+
+// Positions handled by one prefill work item for a GQA group size.
+int prefill_item_positions(DType dt, int group);
+
+}  // namespace stage_k

@@ -1,0 +1,636 @@
+// Stage runtime: argument validation, workspace planning, per-step metadata
+// and the per-layer launch sequence behind the C ABI of include/stage.h.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/stage.h"
+#include "kernels.hpp"
+
+using namespace stage_k;
+
+namespace {
+
+thread_local std::string g_err;
+
+stage_status fail(stage_status code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+constexpr int kRing = 4;             // pinned staging buffers in flight
+constexpr int kMaxSplits = 32;       // decode key splits per sequence, at most
+constexpr int kSplitMinBlocks = 8;   // at least 8 blocks (128 keys) per split
+constexpr int kSkinnyMaxRows = 128;  // decode-sized steps use split-K GEMMs
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+int env_int(const char* name, int dflt) {
+  const char* v = getenv(name);
+  return (v && *v) ? atoi(v) : dflt;
+}
+
+struct Region {
+  size_t off = 0, bytes = 0;
+};
+
+struct PendingTiming {
+  int op;
+  hipEvent_t e0, e1;
+};
+
+}  // namespace
+
+struct stage {
+  stage_model_config cfg{};
+  int32_t layer_begin = 0, n_layers = 0;
+  std::vector<stage_layer_weights> layers;
+  char* kv_pool = nullptr;
+  int32_t num_blocks = 0;
+  int32_t max_tokens = 0, max_seqs = 0;
+  size_t esize = 4;
+  size_t kv_layer_bytes = 0;
+  int device = 0;
+  int skinny_rows = 0;  // rows of the split-K accumulators (0 in fp32 mode)
+  int skinny_waves = 2048;
+
+  // workspace
+  Region r_x, r_h, r_qkv, r_q, r_attn, r_m, r_gu, r_part_o, r_part_ml, r_meta, r_cos, r_sin;
+  size_t ws_bytes = 0;
+  char* ws = nullptr;
+  size_t meta_ints = 0;
+  bool acc_zero = false;  // split-K accumulators known to be all zero
+
+  // pinned staging ring for per-step metadata
+  int32_t* staging[kRing] = {};
+  hipEvent_t staging_ev[kRing] = {};
+  bool staging_used[kRing] = {};
+  int ring = 0;
+
+  // op timing
+  bool timing = false;
+  std::vector<PendingTiming> pending;
+  std::vector<hipEvent_t> free_events;
+  double op_ms[STAGE_OP_COUNT] = {};
+  int64_t op_launches[STAGE_OP_COUNT] = {};
+
+  template <typename T>
+  T* at(const Region& r) const {
+    return reinterpret_cast<T*>(ws + r.off);
+  }
+};
+
+namespace {
+
+bool is_pow2_le16(int g) { return g == 1 || g == 2 || g == 4 || g == 8 || g == 16; }
+
+stage_status check_config(const stage_model_config* c) {
+  if (!c) return fail(STAGE_ERR_INVALID_ARG, "config is NULL");
+  if (c->hidden <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0 ||
+      c->ffn <= 0 || c->max_position <= 0)
+    return fail(STAGE_ERR_INVALID_ARG, "config sizes must be positive");
+  if (!(c->rms_eps >= 0.f) || !(c->qk_rms_eps >= 0.f) || !(c->rope_theta > 0.0))
+    return fail(STAGE_ERR_INVALID_ARG, "eps must be >= 0 and rope_theta > 0");
+  if (c->dtype != STAGE_F32 && c->dtype != STAGE_BF16)
+    return fail(STAGE_ERR_UNSUPPORTED, "dtype %d not supported", (int)c->dtype);
+  if (c->block_size != kBlock)
+    return fail(STAGE_ERR_UNSUPPORTED, "block_size must be %d (got %d)", kBlock, c->block_size);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(STAGE_ERR_UNSUPPORTED, "head_dim must be 64 or 128 (got %d)", c->head_dim);
+  if (c->n_q_heads % c->n_kv_heads != 0 || !is_pow2_le16(c->n_q_heads / c->n_kv_heads))
+    return fail(STAGE_ERR_UNSUPPORTED, "n_q_heads/n_kv_heads must be 1, 2, 4, 8 or 16");
+  if (c->hidden % 128 != 0 || (c->n_q_heads * c->head_dim) % 128 != 0 || c->ffn % 64 != 0)
+    return fail(STAGE_ERR_UNSUPPORTED,
+                "need hidden %% 128 == 0, n_q*head_dim %% 128 == 0, ffn %% 64 == 0");
+  if (c->qk_norm != 0 && c->qk_norm != 1)
+    return fail(STAGE_ERR_INVALID_ARG, "qk_norm must be 0 or 1");
+  return STAGE_OK;
+}
+
+// Validate one batch against the stage limits; `decode` requires q_len == 1.
+stage_status check_batch(const stage_model_config& c, const stage_batch* b, bool decode,
+                         const char* what, long long* tokens) {
+  *tokens = 0;
+  if (!b || b->num_seqs == 0) return STAGE_OK;
+  if (b->num_seqs < 0) return fail(STAGE_ERR_INVALID_ARG, "%s: num_seqs < 0", what);
+  if (!b->q_lens || !b->ctx_lens)
+    return fail(STAGE_ERR_INVALID_ARG, "%s: q_lens/ctx_lens is NULL", what);
+  if (!b->block_tables) return fail(STAGE_ERR_INVALID_ARG, "%s: block_tables is NULL", what);
+  if (b->max_blocks_per_seq <= 0)
+    return fail(STAGE_ERR_INVALID_ARG, "%s: max_blocks_per_seq must be >= 1", what);
+  const long long cap = (long long)b->max_blocks_per_seq * c.block_size;
+  for (int i = 0; i < b->num_seqs; ++i) {
+    const long long q = b->q_lens[i], ctx = b->ctx_lens[i];
+    if (q < 1) return fail(STAGE_ERR_INVALID_ARG, "%s: q_lens[%d] = %lld < 1", what, i, q);
+    if (decode && q != 1)
+      return fail(STAGE_ERR_INVALID_ARG, "%s: decode q_lens[%d] = %lld != 1", what, i, q);
+    if (ctx < 0) return fail(STAGE_ERR_INVALID_ARG, "%s: ctx_lens[%d] < 0", what, i);
+    if (ctx + q > cap)
+      return fail(STAGE_ERR_CAPACITY, "%s: sequence %d needs %lld tokens > table capacity %lld",
+                  what, i, ctx + q, cap);
+    if (ctx + q > c.max_position)
+      return fail(STAGE_ERR_CAPACITY, "%s: sequence %d reaches position %lld >= max_position %d",
+                  what, i, ctx + q - 1, c.max_position);
+    *tokens += q;
+  }
+  return STAGE_OK;
+}
+
+stage_status check_step(const stage_model_config& c, int32_t max_tokens, int32_t max_seqs,
+                        const stage_batch* pf, const stage_batch* dc, long long* T) {
+  long long tp = 0, td = 0;
+  stage_status s = check_batch(c, pf, false, "prefill", &tp);
+  if (s != STAGE_OK) return s;
+  s = check_batch(c, dc, true, "decode", &td);
+  if (s != STAGE_OK) return s;
+  const long long ns = (pf ? pf->num_seqs : 0) + (dc ? dc->num_seqs : 0);
+  if (tp + td > max_tokens)
+    return fail(STAGE_ERR_CAPACITY, "step has %lld tokens > max_tokens %d", tp + td, max_tokens);
+  if (ns > max_seqs)
+    return fail(STAGE_ERR_CAPACITY, "step has %lld sequences > max_seqs %d", ns, max_seqs);
+  *T = tp + td;
+  return STAGE_OK;
+}
+
+stage_status hip_fail(const char* what, hipError_t e) {
+  return fail(STAGE_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+void plan_workspace(stage* st) {
+  const auto& c = st->cfg;
+  const size_t T = st->max_tokens, H = c.hidden, D = c.head_dim;
+  const size_t qw = (size_t)c.n_q_heads * D, qkvw = (size_t)(c.n_q_heads + 2 * c.n_kv_heads) * D;
+  const size_t F = c.ffn, es = st->esize;
+  size_t off = 0;
+  auto take = [&](Region& r, size_t bytes) {
+    r.off = off;
+    r.bytes = bytes;
+    off = align_up(off + bytes, 256);
+  };
+  take(st->r_x, T * H * 4);
+  take(st->r_h, T * H * es);
+  take(st->r_qkv, T * qkvw * 4);
+  take(st->r_q, T * qw * es);
+  take(st->r_attn, T * qw * es);
+  take(st->r_m, T * F * es);
+  const size_t gu_rows = c.dtype == STAGE_F32 ? T : (size_t)st->skinny_rows;
+  take(st->r_gu, gu_rows * 2 * F * 4);
+  const size_t max_items = c.dtype == STAGE_BF16 ? (size_t)st->max_seqs * kMaxSplits : 0;
+  take(st->r_part_o, max_items * qw * 4);
+  take(st->r_part_ml, max_items * c.n_q_heads * 2 * 4);
+  // metadata: tok_seq, tok_pos [T]; decode items [max_items][4];
+  // item_start [max_seqs + 1]; tok_rows [max_seqs]; prefill items [T + max_seqs][4]
+  st->meta_ints = 2 * T + 4 * max_items + 2 * (size_t)st->max_seqs + 1 +
+                  4 * (T + (size_t)st->max_seqs);
+  take(st->r_meta, st->meta_ints * 4);
+  take(st->r_cos, (size_t)c.max_position * (D / 2) * 4);
+  take(st->r_sin, (size_t)c.max_position * (D / 2) * 4);
+  st->ws_bytes = off;
+}
+
+struct StepMeta {
+  int32_t *tok_seq, *tok_pos;
+  DecodeItem* ditems;
+  int32_t *item_start, *tok_rows;
+  PrefillItem* pitems;
+  int n_ditems = 0, n_pitems = 0;
+};
+
+// Lay out the metadata arrays over a base pointer (host staging or device).
+StepMeta meta_view(const stage* st, int32_t* base) {
+  const size_t T = st->max_tokens;
+  const size_t max_items = st->cfg.dtype == STAGE_BF16 ? (size_t)st->max_seqs * kMaxSplits : 0;
+  StepMeta m;
+  m.tok_seq = base;
+  m.tok_pos = base + T;
+  m.ditems = reinterpret_cast<DecodeItem*>(base + 2 * T);
+  m.item_start = base + 2 * T + 4 * max_items;
+  m.tok_rows = m.item_start + st->max_seqs + 1;
+  m.pitems = reinterpret_cast<PrefillItem*>(m.tok_rows + st->max_seqs);
+  return m;
+}
+
+void build_meta(const stage* st, const stage_batch* pf, const stage_batch* dc, StepMeta& m) {
+  const int np = pf ? pf->num_seqs : 0, nd = dc ? dc->num_seqs : 0;
+  int row = 0;
+  const int ppw = prefill_item_positions((DType)st->cfg.dtype,
+                                         st->cfg.n_q_heads / st->cfg.n_kv_heads);
+  m.n_pitems = 0;
+  for (int s = 0; s < np; ++s) {
+    const int q = pf->q_lens[s], ctx = pf->ctx_lens[s];
+    for (int i = 0; i < q; ++i) {
+      m.tok_seq[row + i] = s;
+      m.tok_pos[row + i] = ctx + i;
+    }
+    for (int off = 0; off < q; off += ppw)
+      m.pitems[m.n_pitems++] = PrefillItem{s, row + off, ctx + off, std::min(ppw, q - off)};
+    row += q;
+  }
+  // Longest key ranges first, so the slowest waves start first.
+  std::stable_sort(m.pitems, m.pitems + m.n_pitems, [](const PrefillItem& a, const PrefillItem& b) {
+    return a.p0 + a.npos > b.p0 + b.npos;
+  });
+  m.n_ditems = 0;
+  for (int j = 0; j < nd; ++j) {
+    const int ctx = dc->ctx_lens[j];
+    const int g = np + j;
+    m.tok_seq[row] = g;
+    m.tok_pos[row] = ctx;
+    m.tok_rows[j] = row;
+    m.item_start[j] = m.n_ditems;
+    ++row;
+    if (st->cfg.dtype != STAGE_BF16) continue;  // fp32 attention needs no split plan
+    const int keys = ctx + 1;
+    const int nb = (keys + kBlock - 1) / kBlock;
+    int splits = std::min(kMaxSplits, std::max(1, nb / kSplitMinBlocks));
+    const int bps = (nb + splits - 1) / splits;
+    splits = (nb + bps - 1) / bps;
+    for (int sp = 0; sp < splits; ++sp) {
+      const int k0 = sp * bps * kBlock;
+      const int k1 = std::min(keys, (sp + 1) * bps * kBlock);
+      m.ditems[m.n_ditems++] = DecodeItem{row - 1, g, k0, k1};
+    }
+  }
+  m.item_start[nd] = m.n_ditems;
+}
+
+// Split so that the skinny GEMM launches about `waves` waves.
+int skinny_split(int N, int K, int M, int waves) {
+  const int nt = ((M + 15) / 16) <= 4 ? 4 : 2;
+  const int n_waves = std::max(1, N / (nt * 16));
+  int splits = std::max(1, (waves + n_waves - 1) / n_waves);
+  splits = std::min(splits, K / 64);
+  int ks = (K + splits - 1) / splits;
+  ks = (ks + 63) / 64 * 64;
+  return ks;
+}
+
+hipEvent_t take_event(stage* st) {
+  if (!st->free_events.empty()) {
+    hipEvent_t e = st->free_events.back();
+    st->free_events.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Launch helper: brackets a launch with timing events when enabled.
+struct Launcher {
+  stage* st;
+  hipStream_t s;
+  hipError_t err = hipSuccess;
+  template <typename F>
+  void operator()(int op, F&& f) {
+    if (err != hipSuccess) return;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (st->timing) {
+      e0 = take_event(st);
+      e1 = take_event(st);
+      if (!e0 || !e1) {
+        err = hipErrorOutOfMemory;
+        return;
+      }
+      if ((err = hipEventRecord(e0, s)) != hipSuccess) return;
+    }
+    err = f();
+    if (err == hipSuccess && st->timing) {
+      err = hipEventRecord(e1, s);
+      st->pending.push_back(PendingTiming{op, e0, e1});
+    }
+  }
+};
+
+stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, const void* hin,
+                      void* hout, void* stream_v) {
+  const auto& c = st->cfg;
+  if (!st->ws) return fail(STAGE_ERR_INVALID_ARG, "no workspace bound (stage_bind_workspace)");
+  long long T64 = 0;
+  stage_status vs = check_step(c, st->max_tokens, st->max_seqs, pf, dc, &T64);
+  if (vs != STAGE_OK) return vs;
+  const int T = (int)T64;
+  if (T == 0) return STAGE_OK;
+  if (!hin || !hout) return fail(STAGE_ERR_INVALID_ARG, "hidden_in/hidden_out is NULL");
+  hipStream_t s = (hipStream_t)stream_v;
+  hipError_t e = hipSetDevice(st->device);
+  if (e != hipSuccess) return hip_fail("hipSetDevice", e);
+
+  // metadata: host build in a pinned staging slot, one async upload
+  const int slot = st->ring;
+  st->ring = (st->ring + 1) % kRing;
+  if (st->staging_used[slot]) {
+    e = hipEventSynchronize(st->staging_ev[slot]);
+    if (e != hipSuccess) return hip_fail("staging event", e);
+  }
+  StepMeta hm = meta_view(st, st->staging[slot]);
+  build_meta(st, pf, dc, hm);
+  e = hipMemcpyAsync(st->ws + st->r_meta.off, st->staging[slot], st->meta_ints * 4,
+                     hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) return hip_fail("metadata upload", e);
+  e = hipEventRecord(st->staging_ev[slot], s);
+  if (e != hipSuccess) return hip_fail("metadata event", e);
+  st->staging_used[slot] = true;
+  StepMeta dm = meta_view(st, st->at<int32_t>(st->r_meta));
+
+  const DType dt = (DType)c.dtype;
+  const int H = c.hidden, D = c.head_dim, nq = c.n_q_heads, nkv = c.n_kv_heads, F = c.ffn;
+  const int qw = nq * D, qkvw = (nq + 2 * nkv) * D;
+  const int np = pf ? pf->num_seqs : 0, nd = dc ? dc->num_seqs : 0;
+  const int Tp = T - nd;
+  const bool skinny = dt == DT_BF16 && T <= st->skinny_rows;
+  SegTables tabs{pf && np ? pf->block_tables : nullptr, pf && np ? pf->max_blocks_per_seq : 0, np,
+                 dc && nd ? dc->block_tables : nullptr, dc && nd ? dc->max_blocks_per_seq : 0};
+
+  float* x = st->at<float>(st->r_x);
+  void* h = st->ws + st->r_h.off;
+  float* qkv = st->at<float>(st->r_qkv);
+  void* q = st->ws + st->r_q.off;
+  void* attn = st->ws + st->r_attn.off;
+  void* m = st->ws + st->r_m.off;
+  float* gu = st->at<float>(st->r_gu);
+  const float* cos_t = st->at<float>(st->r_cos);
+  const float* sin_t = st->at<float>(st->r_sin);
+
+  Launcher L{st, s};
+  if (skinny && !st->acc_zero) {
+    L(STAGE_OP_NORM, [&] { return fill_zero_f32(qkv, (size_t)st->skinny_rows * qkvw, s); });
+    L(STAGE_OP_NORM, [&] { return fill_zero_f32(gu, (size_t)st->skinny_rows * 2 * F, s); });
+  }
+  if (!skinny) st->acc_zero = false;
+
+  for (int li = 0; li < st->n_layers; ++li) {
+    const stage_layer_weights& w = st->layers[li];
+    KVLayer kvl{st->kv_pool + (size_t)li * st->kv_layer_bytes, nkv, D};
+    if (li == 0)
+      L(STAGE_OP_NORM, [&] { return embed_norm(dt, hin, x, h, w.attn_norm, T, H, c.rms_eps, s); });
+    else
+      L(STAGE_OP_NORM, [&] { return rmsnorm(dt, x, h, w.attn_norm, T, H, c.rms_eps, s); });
+
+    if (skinny)
+      L(STAGE_OP_QKV, [&] {
+        return gemm_skinny(dt, h, w.w_qkv, T, qkvw, H, qkv, skinny_split(qkvw, H, T, st->skinny_waves), s);
+      });
+    else
+      L(STAGE_OP_QKV, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_qkv, T, qkvw, H, qkv, s); });
+
+    L(STAGE_OP_ROPE_KV, [&] {
+      return rope_kv_write(dt, qkv, skinny ? 1 : 0, q, kvl, dm.tok_seq, dm.tok_pos, tabs, cos_t,
+                           sin_t, c.qk_norm ? w.q_norm : nullptr, c.qk_norm ? w.k_norm : nullptr,
+                           c.qk_rms_eps, T, nq, s);
+    });
+
+    if (dt == DT_F32) {
+      L(STAGE_OP_ATTN, [&] {
+        return attn_f32((const float*)q, kvl, tabs, dm.tok_seq, dm.tok_pos, 0, T, nq,
+                        (float*)attn, s);
+      });
+    } else {
+      if (Tp > 0)
+        L(STAGE_OP_ATTN, [&] {
+          return attn_prefill(dt, q, kvl, tabs, dm.pitems, hm.n_pitems, nq, attn, s);
+        });
+      if (nd > 0) {
+        L(STAGE_OP_ATTN, [&] {
+          return attn_decode(dt, q, kvl, tabs, dm.ditems, hm.n_ditems, nq,
+                             st->at<float>(st->r_part_o), st->at<float>(st->r_part_ml), s);
+        });
+        L(STAGE_OP_ATTN, [&] {
+          return attn_merge(dt, st->at<float>(st->r_part_o), st->at<float>(st->r_part_ml),
+                            dm.item_start, dm.tok_rows, nd, nq, D, attn, s);
+        });
+      }
+    }
+
+    if (skinny)
+      L(STAGE_OP_O, [&] {
+        return gemm_skinny(dt, attn, w.w_o, T, H, qw, x, skinny_split(H, qw, T, st->skinny_waves), s);
+      });
+    else
+      L(STAGE_OP_O, [&] { return gemm(dt, EPI_RESID_ADD, attn, w.w_o, T, H, qw, x, s); });
+
+    L(STAGE_OP_NORM, [&] { return rmsnorm(dt, x, h, w.ffn_norm, T, H, c.rms_eps, s); });
+
+    if (skinny) {
+      L(STAGE_OP_GATE_UP, [&] {
+        return gemm_skinny(dt, h, w.w_gate_up, T, 2 * F, H, gu,
+                           skinny_split(2 * F, H, T, st->skinny_waves), s);
+      });
+      L(STAGE_OP_NORM, [&] { return swiglu(dt, gu, m, T, F, 1, s); });
+    } else if (dt == DT_BF16) {
+      L(STAGE_OP_GATE_UP, [&] { return gemm(dt, EPI_SWIGLU, h, w.w_gate_up, T, 2 * F, H, m, s); });
+    } else {
+      L(STAGE_OP_GATE_UP, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_gate_up, T, 2 * F, H, gu, s); });
+      L(STAGE_OP_NORM, [&] { return swiglu(dt, gu, m, T, F, 0, s); });
+    }
+
+    if (skinny)
+      L(STAGE_OP_DOWN, [&] {
+        return gemm_skinny(dt, m, w.w_down, T, H, F, x, skinny_split(H, F, T, st->skinny_waves), s);
+      });
+    else
+      L(STAGE_OP_DOWN, [&] { return gemm(dt, EPI_RESID_ADD, m, w.w_down, T, H, F, x, s); });
+  }
+  L(STAGE_OP_NORM, [&] { return output_cast(dt, x, hout, (size_t)T * H, s); });
+
+  if (L.err != hipSuccess) {
+    st->acc_zero = false;
+    return hip_fail("kernel launch", L.err);
+  }
+  if (skinny) st->acc_zero = true;
+  return STAGE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+stage_status stage_create(const stage_model_config* cfg, int32_t layer_begin, int32_t layer_end,
+                          const stage_layer_weights* layers, void* kv_pool, int32_t num_blocks,
+                          int32_t max_tokens, int32_t max_seqs, stage_t** out) {
+  if (!out) return fail(STAGE_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  stage_status s = check_config(cfg);
+  if (s != STAGE_OK) return s;
+  if (layer_begin < 0 || layer_end <= layer_begin)
+    return fail(STAGE_ERR_INVALID_ARG, "layer range [%d, %d) is empty or negative", layer_begin,
+                layer_end);
+  if (!layers) return fail(STAGE_ERR_INVALID_ARG, "layers is NULL");
+  if (!kv_pool) return fail(STAGE_ERR_INVALID_ARG, "kv_pool is NULL");
+  if (num_blocks <= 0 || max_tokens <= 0 || max_seqs <= 0)
+    return fail(STAGE_ERR_INVALID_ARG, "num_blocks, max_tokens and max_seqs must be positive");
+  const int n = layer_end - layer_begin;
+  for (int i = 0; i < n; ++i) {
+    const stage_layer_weights& w = layers[i];
+    if (!w.attn_norm || !w.w_qkv || !w.w_o || !w.ffn_norm || !w.w_gate_up || !w.w_down)
+      return fail(STAGE_ERR_INVALID_ARG, "layer %d: a weight pointer is NULL", layer_begin + i);
+    if (cfg->qk_norm && (!w.q_norm || !w.k_norm))
+      return fail(STAGE_ERR_INVALID_ARG, "layer %d: q_norm/k_norm NULL with qk_norm set",
+                  layer_begin + i);
+  }
+  int ndev = 0;
+  hipError_t e = hipGetDeviceCount(&ndev);
+  if (e != hipSuccess || ndev <= 0)
+    return fail(STAGE_ERR_DEVICE, "no HIP device available (%s)",
+                e != hipSuccess ? hipGetErrorString(e) : "0 devices");
+  stage* st = new (std::nothrow) stage();
+  if (!st) return fail(STAGE_ERR_OUT_OF_MEMORY, "host allocation failed");
+  st->cfg = *cfg;
+  st->layer_begin = layer_begin;
+  st->n_layers = n;
+  st->layers.assign(layers, layers + n);
+  st->kv_pool = (char*)kv_pool;
+  st->num_blocks = num_blocks;
+  st->max_tokens = max_tokens;
+  st->max_seqs = max_seqs;
+  st->esize = cfg->dtype == STAGE_BF16 ? 2 : 4;
+  st->kv_layer_bytes = (size_t)num_blocks * cfg->n_kv_heads * 2 * kBlock * cfg->head_dim * st->esize;
+  st->skinny_rows = cfg->dtype == STAGE_BF16 ? std::min(kSkinnyMaxRows, max_tokens) : 0;
+  st->skinny_waves = std::max(64, env_int("STAGE_SKINNY_WAVES", 2048));
+  if ((e = hipGetDevice(&st->device)) != hipSuccess) {
+    delete st;
+    return hip_fail("hipGetDevice", e);
+  }
+  plan_workspace(st);
+  for (int i = 0; i < kRing; ++i) {
+    void* p = nullptr;
+    if ((e = hipHostMalloc(&p, st->meta_ints * 4, hipHostMallocDefault)) != hipSuccess ||
+        (e = hipEventCreateWithFlags(&st->staging_ev[i], hipEventDisableTiming)) != hipSuccess) {
+      if (p) (void)hipHostFree(p);
+      stage_destroy(st);
+      return hip_fail("pinned staging", e);
+    }
+    st->staging[i] = (int32_t*)p;
+  }
+  *out = st;
+  return STAGE_OK;
+}
+
+size_t stage_workspace_bytes(const stage_t* st) { return st ? st->ws_bytes : 0; }
+
+stage_status stage_bind_workspace(stage_t* st, void* dev, size_t bytes) {
+  if (!st || !dev) return fail(STAGE_ERR_INVALID_ARG, "stage or workspace is NULL");
+  if (bytes < st->ws_bytes)
+    return fail(STAGE_ERR_CAPACITY, "workspace of %zu bytes < required %zu", bytes, st->ws_bytes);
+  if (((uintptr_t)dev) % 256 != 0) return fail(STAGE_ERR_INVALID_ARG, "workspace not 256-byte aligned");
+  hipError_t e = hipSetDevice(st->device);
+  if (e != hipSuccess) return hip_fail("hipSetDevice", e);
+  st->ws = (char*)dev;
+  // rotary table: angle p * theta^(-2j/d) in double, rounded once to float
+  const auto& c = st->cfg;
+  const int half = c.head_dim / 2;
+  std::vector<float> cs((size_t)c.max_position * half), sn((size_t)c.max_position * half);
+  for (int j = 0; j < half; ++j) {
+    const double w = std::pow(c.rope_theta, -2.0 * j / c.head_dim);
+    for (int p = 0; p < c.max_position; ++p) {
+      const double a = (double)p * w;
+      cs[(size_t)p * half + j] = (float)std::cos(a);
+      sn[(size_t)p * half + j] = (float)std::sin(a);
+    }
+  }
+  if ((e = hipMemcpy(st->ws + st->r_cos.off, cs.data(), cs.size() * 4, hipMemcpyHostToDevice)) !=
+          hipSuccess ||
+      (e = hipMemcpy(st->ws + st->r_sin.off, sn.data(), sn.size() * 4, hipMemcpyHostToDevice)) !=
+          hipSuccess ||
+      (e = hipMemset(st->ws + st->r_qkv.off, 0, st->r_qkv.bytes)) != hipSuccess ||
+      (e = hipMemset(st->ws + st->r_gu.off, 0, st->r_gu.bytes)) != hipSuccess) {
+    st->ws = nullptr;
+    return hip_fail("workspace init", e);
+  }
+  st->acc_zero = true;
+  return STAGE_OK;
+}
+
+stage_status stage_prefill(stage_t* st, const stage_batch* batch, const void* hidden_in,
+                           void* hidden_out, void* stream) {
+  if (!st) return fail(STAGE_ERR_INVALID_ARG, "stage is NULL");
+  if (!batch) return fail(STAGE_ERR_INVALID_ARG, "batch is NULL");
+  return run_step(st, batch, nullptr, hidden_in, hidden_out, stream);
+}
+
+stage_status stage_decode(stage_t* st, const stage_batch* batch, const void* hidden_in,
+                          void* hidden_out, void* stream) {
+  if (!st) return fail(STAGE_ERR_INVALID_ARG, "stage is NULL");
+  if (!batch) return fail(STAGE_ERR_INVALID_ARG, "batch is NULL");
+  return run_step(st, nullptr, batch, hidden_in, hidden_out, stream);
+}
+
+stage_status stage_step_mixed(stage_t* st, const stage_batch* prefill, const stage_batch* decode,
+                              const void* hidden_in, void* hidden_out, void* stream) {
+  if (!st) return fail(STAGE_ERR_INVALID_ARG, "stage is NULL");
+  return run_step(st, prefill, decode, hidden_in, hidden_out, stream);
+}
+
+stage_status stage_destroy(stage_t* st) {
+  if (!st) return STAGE_OK;
+  for (int i = 0; i < kRing; ++i) {
+    if (st->staging_ev[i]) {
+      if (st->staging_used[i]) (void)hipEventSynchronize(st->staging_ev[i]);
+      (void)hipEventDestroy(st->staging_ev[i]);
+    }
+    if (st->staging[i]) (void)hipHostFree(st->staging[i]);
+  }
+  for (auto& p : st->pending) {
+    (void)hipEventSynchronize(p.e1);
+    (void)hipEventDestroy(p.e0);
+    (void)hipEventDestroy(p.e1);
+  }
+  for (auto e : st->free_events) (void)hipEventDestroy(e);
+  delete st;
+  return STAGE_OK;
+}
+
+const char* stage_last_error(void) { return g_err.c_str(); }
+
+stage_status stage_validate_step(const stage_model_config* cfg, int32_t max_tokens,
+                                 int32_t max_seqs, const stage_batch* prefill,
+                                 const stage_batch* decode) {
+  stage_status s = check_config(cfg);
+  if (s != STAGE_OK) return s;
+  long long T = 0;
+  return check_step(*cfg, max_tokens, max_seqs, prefill, decode, &T);
+}
+
+stage_status stage_set_op_timing(stage_t* st, int32_t enable) {
+  if (!st) return fail(STAGE_ERR_INVALID_ARG, "stage is NULL");
+  st->timing = enable != 0;
+  return STAGE_OK;
+}
+
+stage_status stage_read_op_times(stage_t* st, double* ms, int64_t* launches) {
+  if (!st || !ms || !launches) return fail(STAGE_ERR_INVALID_ARG, "NULL argument");
+  for (auto& p : st->pending) {
+    hipError_t e = hipEventSynchronize(p.e1);
+    if (e != hipSuccess) return hip_fail("timing event", e);
+    float t = 0.f;
+    if (hipEventElapsedTime(&t, p.e0, p.e1) == hipSuccess) {
+      st->op_ms[p.op] += t;
+      st->op_launches[p.op] += 1;
+    }
+    st->free_events.push_back(p.e0);
+    st->free_events.push_back(p.e1);
+  }
+  st->pending.clear();
+  for (int i = 0; i < STAGE_OP_COUNT; ++i) {
+    ms[i] = st->op_ms[i];
+    launches[i] = st->op_launches[i];
+    st->op_ms[i] = 0.0;
+    st->op_launches[i] = 0;
+  }
+  return STAGE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,155 @@
+"""Device-memory plumbing around the stage ABI (PyTorch for memory and
+streams only; every step of the forward pass runs in the HIP library).
+
+``DeviceStage`` owns the caller side of the ABI contract: it allocates the
+weights' device copies, the KV pool, block tables and the workspace as torch
+tensors, creates the stage over them and forwards calls.
+"""
+
+from __future__ import annotations
+
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import stage as S
+from .synth import GAIN_NAMES, ModelShape, _TENSOR_IDS
+
+WEIGHT_FIELDS = ("attn_norm", "w_qkv", "q_norm", "k_norm", "w_o", "ffn_norm", "w_gate_up",
+                 "w_down")
+
+
+def torch_dtype(dtype: str) -> torch.dtype:
+    return {"bf16": torch.bfloat16, "f32": torch.float32}[dtype]
+
+
+def model_config(shape: ModelShape, dtype: str, max_position: int = 8192) -> S.stage_model_config:
+    return S.stage_model_config(
+        hidden=shape.hidden, n_q_heads=shape.n_q_heads, n_kv_heads=shape.n_kv_heads,
+        head_dim=shape.head_dim, ffn=shape.ffn, qk_norm=1 if shape.qk_norm else 0,
+        block_size=shape.block_size, rms_eps=shape.rms_eps, qk_rms_eps=shape.qk_rms_eps,
+        rope_theta=shape.rope_theta, max_position=max_position,
+        dtype=S.STAGE_BF16 if dtype == "bf16" else S.STAGE_F32)
+
+
+def upload_weights(host: Dict[str, np.ndarray], dtype: str, device="cuda") -> Dict[str, torch.Tensor]:
+    """Copy host weights to the device in the mode dtype (fp32 -> bf16 is
+    round-to-nearest-even)."""
+    td = torch_dtype(dtype)
+    return {k: torch.from_numpy(np.ascontiguousarray(v, np.float32)).to(device=device, dtype=td)
+            for k, v in host.items()}
+
+
+def device_layer_weights(shape: ModelShape, seed: int, global_layer: int, dtype: str,
+                         std: float = 0.02, gain_std: float = 0.02,
+                         device="cuda") -> Dict[str, torch.Tensor]:
+    """Random weights generated on the device (for model-sized stages where a
+    host draw would take too long): N(0, std^2) projections, 1 + N(0,
+    gain_std^2) gains, each tensor from its own seeded device generator."""
+    td = torch_dtype(dtype)
+    out = {}
+    for name, shp in shape.weight_shapes().items():
+        g = torch.Generator(device=device)
+        g.manual_seed((seed * 1_000_003 + global_layer * 1009 + _TENSOR_IDS[name]) & 0x7FFFFFFF)
+        if name in GAIN_NAMES:
+            t = torch.empty(shp, dtype=torch.float32, device=device).normal_(1.0, gain_std,
+                                                                            generator=g)
+            out[name] = t.to(td)
+        else:
+            out[name] = torch.empty(shp, dtype=td, device=device).normal_(0.0, std, generator=g)
+    return out
+
+
+def to_host64(weights: Dict[str, torch.Tensor]) -> Dict[str, np.ndarray]:
+    """The stored values, as float64 host arrays."""
+    return {k: v.detach().to(torch.float64).cpu().numpy() for k, v in weights.items()}
+
+
+class DeviceStage:
+    def __init__(self, shape: ModelShape, dtype: str, layer_begin: int,
+                 weights: Sequence[Dict[str, torch.Tensor]], num_blocks: int, max_tokens: int,
+                 max_seqs: int, max_position: int = 8192, device="cuda",
+                 kv_pool: Optional[torch.Tensor] = None):
+        self.shape, self.dtype = shape, dtype
+        self.n_layers = len(weights)
+        self.num_blocks = num_blocks
+        self.cfg = model_config(shape, dtype, max_position)
+        td = torch_dtype(dtype)
+        numel = self.n_layers * num_blocks * shape.n_kv_heads * 2 * shape.block_size * shape.head_dim
+        if kv_pool is None:
+            kv_pool = torch.zeros(numel, dtype=td, device=device)
+        assert kv_pool.numel() >= numel and kv_pool.dtype == td
+        self.kv_pool = kv_pool
+        self.weights = list(weights)
+        layers = []
+        for w in self.weights:
+            for k, v in w.items():
+                assert v.is_contiguous() and v.dtype == td, k
+            layers.append(S.stage_layer_weights(
+                *[w[f].data_ptr() if f in w else None for f in WEIGHT_FIELDS]))
+        self.handle = S.stage_create(self.cfg, layer_begin, layer_begin + self.n_layers, layers,
+                                     kv_pool.data_ptr(), num_blocks, max_tokens, max_seqs)
+        nbytes = S.stage_workspace_bytes(self.handle)
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        S.stage_bind_workspace(self.handle, self.workspace.data_ptr(), nbytes)
+
+    # --- calls -------------------------------------------------------------
+    @staticmethod
+    def batch(q_lens, ctx_lens, block_tables: torch.Tensor) -> S.stage_batch:
+        assert block_tables.dtype == torch.int32 and block_tables.is_contiguous()
+        return S.make_batch(q_lens, ctx_lens, block_tables.data_ptr(), block_tables.shape[1])
+
+    def _out(self, hidden_in, hidden_out):
+        return torch.empty_like(hidden_in) if hidden_out is None else hidden_out
+
+    def prefill(self, q_lens, ctx_lens, bt, hidden_in, hidden_out=None, stream=0):
+        out = self._out(hidden_in, hidden_out)
+        S.stage_prefill(self.handle, self.batch(q_lens, ctx_lens, bt), hidden_in.data_ptr(),
+                        out.data_ptr(), stream)
+        return out
+
+    def decode(self, ctx_lens, bt, hidden_in, hidden_out=None, stream=0):
+        out = self._out(hidden_in, hidden_out)
+        S.stage_decode(self.handle, self.batch(np.ones(len(ctx_lens), np.int32), ctx_lens, bt),
+                       hidden_in.data_ptr(), out.data_ptr(), stream)
+        return out
+
+    def mixed(self, p_q_lens, p_ctx_lens, p_bt, d_ctx_lens, d_bt, hidden_in, hidden_out=None,
+              stream=0):
+        out = self._out(hidden_in, hidden_out)
+        pb = self.batch(p_q_lens, p_ctx_lens, p_bt) if len(p_q_lens) else None
+        db = self.batch(np.ones(len(d_ctx_lens), np.int32), d_ctx_lens, d_bt) \
+            if len(d_ctx_lens) else None
+        S.stage_step_mixed(self.handle, pb, db, hidden_in.data_ptr(), out.data_ptr(), stream)
+        return out
+
+    def kv_view(self) -> torch.Tensor:
+        s = self.shape
+        n = self.n_layers * self.num_blocks * s.n_kv_heads * 2 * s.block_size * s.head_dim
+        return self.kv_pool[:n].view(self.n_layers, self.num_blocks, s.n_kv_heads, 2,
+                                     s.block_size, s.head_dim)
+
+    def close(self):
+        if self.handle:
+            S.stage_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def gpu_kv_to_oracle_layout(kv6: torch.Tensor) -> List[Dict[str, np.ndarray]]:
+    """Convert the GPU pool [L][nb][nkv][2][16][d] (V stored [d][16]) into a
+    list of per-layer {'k','v'} arrays [nb][16][nkv][d] in float64."""
+    a = kv6.detach().to(torch.float64).cpu().numpy()
+    out = []
+    for l in range(a.shape[0]):
+        k = a[l, :, :, 0].transpose(0, 2, 1, 3)                   # [nb][16][nkv][d]
+        v = a[l, :, :, 1].reshape(a.shape[1], a.shape[2], a.shape[5], a.shape[4])  # [nb][nkv][d][16]
+        v = v.transpose(0, 3, 1, 2)                               # [nb][16][nkv][d]
+        out.append({"k": np.ascontiguousarray(k), "v": np.ascontiguousarray(v)})
+    return out

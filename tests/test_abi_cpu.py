@@ -1,0 +1,142 @@
+"""The C-ABI library on a host without a GPU: it loads, exports every symbol
+include/stage.h declares, validates arguments with the documented codes, and
+reports a missing device instead of crashing (CPU only)."""
+
+from __future__ import annotations
+
+import os
+import re
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_18600_amd import stage as S
+from paper_2606_18600_amd import synth
+from paper_2606_18600_amd.harness import model_config
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _lib():
+    if not os.path.exists(S.LIB_PATH):
+        from paper_2606_18600_amd import build
+        build.build(verbose=False)
+    return S.load_library()
+
+
+def header_functions():
+    names = set()
+    for f in os.listdir(os.path.join(ROOT, "include")):
+        if f.endswith(".h"):
+            src = open(os.path.join(ROOT, "include", f)).read()
+            src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+            names |= set(re.findall(r"\b(stage_[a-z_]+)\s*\(", src))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = _lib()
+    declared = header_functions()
+    assert {"stage_create", "stage_prefill", "stage_decode", "stage_step_mixed"} <= declared
+    for name in sorted(declared):
+        assert hasattr(lib, name), f"{name} declared in include/ but not exported"
+    assert declared == set(S.EXPORTED)
+
+
+CFG = model_config(synth.TINY, "bf16", max_position=4096)
+FAKE_TABLE = 0x1000  # never dereferenced by host-side validation
+
+
+def _b(q, c, mb=8, bt=FAKE_TABLE):
+    return S.make_batch(q, c, bt, mb)
+
+
+@pytest.mark.parametrize("case,code", [
+    ("ok_prefill", S.STAGE_OK),
+    ("ok_mixed", S.STAGE_OK),
+    ("q_len_zero", S.STAGE_ERR_INVALID_ARG),
+    ("decode_q_len_two", S.STAGE_ERR_INVALID_ARG),
+    ("negative_ctx", S.STAGE_ERR_INVALID_ARG),
+    ("null_table", S.STAGE_ERR_INVALID_ARG),
+    ("table_too_small", S.STAGE_ERR_CAPACITY),
+    ("too_many_tokens", S.STAGE_ERR_CAPACITY),
+    ("too_many_seqs", S.STAGE_ERR_CAPACITY),
+    ("past_max_position", S.STAGE_ERR_CAPACITY),
+    ("empty", S.STAGE_OK),
+])
+def test_validate_step_codes(case, code):
+    _lib()
+    pf = dc = None
+    mt, ms = 256, 8
+    if case == "ok_prefill":
+        pf = _b([17, 64], [0, 40])
+    elif case == "ok_mixed":
+        pf, dc = _b([16], [0]), _b([1, 1, 1], [0, 5, 127])
+    elif case == "q_len_zero":
+        pf = _b([3, 0], [0, 0])
+    elif case == "decode_q_len_two":
+        dc = S.make_batch([1, 2], [4, 4], FAKE_TABLE, 8)
+    elif case == "negative_ctx":
+        pf = _b([3], [-1])
+    elif case == "null_table":
+        pf = _b([3], [0], bt=0)
+    elif case == "table_too_small":
+        pf = _b([20], [100], mb=7)          # 120 tokens > 7 * 16
+    elif case == "too_many_tokens":
+        pf = _b([200, 57], [0, 0], mb=16)
+    elif case == "too_many_seqs":
+        dc = _b([1] * 9, [3] * 9)
+    elif case == "past_max_position":
+        pf = _b([2], [4095], mb=1024)
+    elif case == "empty":
+        pass
+    got = S.stage_validate_step(CFG, mt, ms, pf, dc)
+    assert got == code, S.stage_last_error()
+    if code != S.STAGE_OK:
+        assert S.stage_last_error()
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("head_dim", 96, S.STAGE_ERR_UNSUPPORTED),
+    ("block_size", 32, S.STAGE_ERR_UNSUPPORTED),
+    ("n_kv_heads", 3, S.STAGE_ERR_UNSUPPORTED),
+    ("hidden", 200, S.STAGE_ERR_UNSUPPORTED),
+    ("ffn", 0, S.STAGE_ERR_INVALID_ARG),
+    ("dtype", 7, S.STAGE_ERR_UNSUPPORTED),
+    ("rope_theta", -1.0, S.STAGE_ERR_INVALID_ARG),
+])
+def test_validate_config_codes(field, value, code):
+    _lib()
+    cfg = model_config(synth.TINY, "bf16")
+    setattr(cfg, field, value)
+    assert S.stage_validate_step(cfg, 16, 4, None, None) == code
+
+
+@pytest.mark.skipif(torch.cuda.is_available(), reason="checks the no-device path")
+def test_create_without_device_reports_device_error():
+    _lib()
+    ws = S.stage_layer_weights(*([0x1000] * 8))
+    with pytest.raises(S.StageError) as e:
+        S.stage_create(CFG, 0, 1, [ws], 0x2000, 16, 64, 4)
+    assert e.value.code == S.STAGE_ERR_DEVICE
+
+
+def test_create_rejects_bad_arguments_before_touching_a_device():
+    _lib()
+    ws = S.stage_layer_weights(*([0x1000] * 8))
+    with pytest.raises(S.StageError) as e:
+        S.stage_create(CFG, 3, 3, [ws], 0x2000, 16, 64, 4)       # empty layer range
+    assert e.value.code == S.STAGE_ERR_INVALID_ARG
+    bad = S.stage_layer_weights(*([0x1000] * 8))
+    bad.w_down = None
+    with pytest.raises(S.StageError) as e:
+        S.stage_create(CFG, 0, 1, [bad], 0x2000, 16, 64, 4)
+    assert e.value.code == S.STAGE_ERR_INVALID_ARG
+
+
+def test_null_stage_calls_fail_cleanly():
+    lib = _lib()
+    assert lib.stage_prefill(None, None, None, None, None) == S.STAGE_ERR_INVALID_ARG
+    assert lib.stage_destroy(None) == S.STAGE_OK
+    assert lib.stage_workspace_bytes(None) == 0

@@ -1,0 +1,257 @@
+"""Parity of the HIP stage with the CPU oracle (GPU).
+
+Every call is compared element by element with the oracle run on the same
+stored weights, inputs and block tables, and the KV entries the calls wrote
+are compared as well. Tolerances: relative L2 <= 1e-4 in the fp32 mode,
+<= 2e-2 in the bf16 mode, and max-abs <= 5e-3 per layer on the tiny config in
+the fp32 mode.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_18600_amd import stage as S
+from paper_2606_18600_amd import synth
+from tests.gpu_pair import Pair, log
+from tests.helpers import rel_l2
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+QWEN_SMALL = synth.ModelShape("qwen-small", hidden=512, n_q_heads=8, n_kv_heads=1, head_dim=128,
+                              ffn=768, rms_eps=1e-6, rope_theta=1e6, qk_norm=True,
+                              qk_rms_eps=1e-6)
+
+
+def _check(tag, y, yr, x, tol):
+    e = rel_l2(y, yr)
+    ed = rel_l2(y - x, yr - x)
+    log(f"  {tag}: rel_l2={e:.3e} delta_rel_l2={ed:.3e} max_abs={np.abs(y - yr).max():.3e}")
+    assert np.isfinite(y).all()
+    assert e <= tol, f"{tag}: rel_l2 {e:.3e} > {tol}"
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_tiny_prefill_then_16_decodes(dtype):
+    """The tiny config end to end: 4 prompts of 16-64 tokens, prefill, then 16
+    decode steps with fresh N(0,1) inputs, shuffled block tables."""
+    seed = 2606
+    shape = synth.TINY
+    log(f"tiny C1 flow dtype={dtype} seed={seed}")
+    lens = synth.uniform_lengths(seed, 0, 4, 16, 64)
+    alloc = synth.BlockAllocator(64, seed)
+    bt = synth.make_block_tables(lens + 16, 8, alloc)
+    pair = Pair(shape, dtype, 2, 64, 256, 8, seed)
+    try:
+        y, yr, x = pair.prefill(lens, np.zeros(4, np.int32), bt,
+                                synth.hidden_states(seed, 1, int(lens.sum()), shape.hidden))
+        _check("prefill", y, yr, x, TOL[dtype])
+        ctx = lens.copy()
+        for step in range(16):
+            y, yr, x = pair.decode(ctx, bt, synth.hidden_states(seed, 100 + step, 4, shape.hidden))
+            _check(f"decode {step}", y, yr, x, TOL[dtype])
+            ctx += 1
+        kv = pair.kv_errors()
+        log(f"  kv rel_l2={kv:.3e}")
+        assert kv <= TOL[dtype]
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("layer", [0, 1])
+def test_tiny_per_layer_max_abs_fp32(layer):
+    seed = 2606
+    shape = synth.TINY
+    log(f"tiny per-layer max-abs layer={layer}")
+    w = [synth.host_layer_weights(shape, seed, layer)]
+    lens = synth.uniform_lengths(seed, 0, 4, 16, 64)
+    bt = synth.make_block_tables(lens + 4, 8, synth.BlockAllocator(64, seed))
+    pair = Pair(shape, "f32", 1, 64, 256, 8, seed, layer_begin=layer, host_weights=w)
+    try:
+        y, yr, _ = pair.prefill(lens, np.zeros(4, np.int32), bt,
+                                synth.hidden_states(seed, 1, int(lens.sum()), shape.hidden))
+        worst = np.abs(y - yr).max()
+        ctx = lens.copy()
+        for step in range(4):
+            y, yr, _ = pair.decode(ctx, bt, synth.hidden_states(seed, 100 + step, 4, shape.hidden))
+            worst = max(worst, np.abs(y - yr).max())
+            ctx += 1
+        log(f"  max_abs={worst:.3e}")
+        assert worst <= 5e-3
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("T", [100, 128, 129, 300])
+def test_prefill_token_counts_cover_both_gemm_paths(dtype, T):
+    """T <= 128 runs the split-K GEMMs, T > 128 the LDS-tiled GEMMs."""
+    seed = 7 + T
+    shape = synth.TINY
+    log(f"prefill T={T} dtype={dtype}")
+    r = np.random.default_rng(seed)
+    cuts = np.sort(r.choice(np.arange(1, T), size=2, replace=False))
+    lens = np.diff(np.concatenate([[0], cuts, [T]])).astype(np.int32)
+    bt = synth.make_block_tables(lens, 32, synth.BlockAllocator(96, seed))
+    pair = Pair(shape, dtype, 2, 96, 512, 8, seed)
+    try:
+        y, yr, x = pair.prefill(lens, np.zeros(3, np.int32), bt,
+                                synth.hidden_states(seed, 1, T, shape.hidden))
+        _check("prefill", y, yr, x, TOL[dtype])
+        assert pair.kv_errors() <= TOL[dtype]
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_ragged_lengths_and_block_boundaries(dtype):
+    seed = 31
+    shape = synth.TINY
+    log(f"ragged dtype={dtype}")
+    lens = np.array([1, 15, 16, 17, 33], np.int32)
+    bt = synth.make_block_tables(lens + 20, 8, synth.BlockAllocator(64, seed))
+    pair = Pair(shape, dtype, 2, 64, 256, 8, seed)
+    try:
+        y, yr, x = pair.prefill(lens, np.zeros(5, np.int32), bt,
+                                synth.hidden_states(seed, 1, int(lens.sum()), shape.hidden))
+        _check("prefill", y, yr, x, TOL[dtype])
+        # continuation chunks that start mid-block
+        q2 = np.array([3, 1, 16, 15, 2], np.int32)
+        y, yr, x = pair.prefill(q2, lens, bt, synth.hidden_states(seed, 2, int(q2.sum()),
+                                                                  shape.hidden))
+        _check("chunk", y, yr, x, TOL[dtype])
+        ctx = lens + q2
+        for step in range(3):
+            y, yr, x = pair.decode(ctx, bt, synth.hidden_states(seed, 10 + step, 5, shape.hidden))
+            _check(f"decode {step}", y, yr, x, TOL[dtype])
+            ctx += 1
+        assert pair.kv_errors() <= TOL[dtype]
+    finally:
+        pair.close()
+
+
+def test_decode_of_a_first_token():
+    """A decode token with no context (position 0) attends only to itself."""
+    seed = 41
+    shape = synth.TINY
+    bt = synth.make_block_tables([5, 5], 2, synth.BlockAllocator(8, seed))
+    pair = Pair(shape, "bf16", 2, 8, 16, 4, seed)
+    try:
+        y, yr, x = pair.decode(np.array([0, 0], np.int32), bt,
+                               synth.hidden_states(seed, 1, 2, shape.hidden))
+        _check("decode@0", y, yr, x, TOL["bf16"])
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("shape", [synth.TINY, QWEN_SMALL], ids=["tiny", "qwen-small"])
+def test_mixed_step(dtype, shape):
+    """Prefill chunks (fresh and continuation) and decodes in one call."""
+    seed = 53
+    log(f"mixed {shape.name} dtype={dtype}")
+    d_ctx0 = np.array([40, 3, 100, 17], np.int32)
+    p_total = np.array([70, 48], np.int32)
+    alloc = synth.BlockAllocator(128, seed)
+    dbt = synth.make_block_tables(d_ctx0 + 4, 16, alloc)
+    pbt = synth.make_block_tables(p_total, 16, alloc)
+    pair = Pair(shape, dtype, 2, 128, 256, 8, seed)
+    try:
+        y, yr, x = pair.prefill(d_ctx0, np.zeros(4, np.int32), dbt,
+                                synth.hidden_states(seed, 1, int(d_ctx0.sum()), shape.hidden))
+        _check("context prefill", y, yr, x, TOL[dtype])
+        # step 1: first chunks of two prompts + 4 decodes
+        pq, pc = np.array([30, 48], np.int32), np.array([0, 0], np.int32)
+        y, yr, x = pair.mixed(pq, pc, pbt, d_ctx0, dbt,
+                              synth.hidden_states(seed, 2, int(pq.sum()) + 4, shape.hidden))
+        _check("mixed 1", y, yr, x, TOL[dtype])
+        # step 2: continuation chunk of prompt 0 + decodes
+        pq2, pc2 = np.array([40], np.int32), np.array([30], np.int32)
+        y, yr, x = pair.mixed(pq2, pc2, pbt[:1], d_ctx0 + 1, dbt,
+                              synth.hidden_states(seed, 3, 44, shape.hidden))
+        _check("mixed 2", y, yr, x, TOL[dtype])
+        assert pair.kv_errors() <= TOL[dtype]
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_qwen_small_long_context_decode(dtype):
+    """head_dim 128, GQA group 8, q/k-norm, contexts long enough for many
+    decode key splits (uneven last split)."""
+    seed = 67
+    shape = QWEN_SMALL
+    log(f"qwen-small long-context dtype={dtype}")
+    ctx = np.array([2500, 700, 129], np.int32)
+    alloc = synth.BlockAllocator(300, seed)
+    bt = synth.make_block_tables(ctx + 3, 160, alloc)
+    pair = Pair(shape, dtype, 1, 300, 1024, 4, seed)
+    try:
+        done = np.zeros(3, np.int32)
+        i = 0
+        while (done < ctx).any():
+            q = np.minimum(ctx - done, 400).astype(np.int32)
+            live = q > 0
+            y, yr, x = pair.prefill(q[live], done[live], bt[live],
+                                    synth.hidden_states(seed, 10 + i, int(q.sum()), shape.hidden))
+            _check(f"chunk {i}", y, yr, x, TOL[dtype])
+            done += q
+            i += 1
+        for step in range(3):
+            y, yr, x = pair.decode(ctx + step, bt,
+                                   synth.hidden_states(seed, 100 + step, 3, shape.hidden))
+            _check(f"decode {step}", y, yr, x, TOL[dtype])
+        assert pair.kv_errors() <= TOL[dtype]
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("lens", [[20, 9], [150, 61]], ids=["split-k", "tiled"])
+def test_hidden_out_may_alias_hidden_in(lens):
+    """Writing the output over the input gives the same result. The tiled
+    GEMMs are deterministic (bitwise equal); the split-K GEMMs sum partial
+    products with atomics, whose order varies from run to run."""
+    seed = 71
+    shape = synth.TINY
+    lens = np.array(lens, np.int32)
+    T = int(lens.sum())
+    bt = synth.make_block_tables(lens, 16, synth.BlockAllocator(32, seed))
+    pair = Pair(shape, "bf16", 2, 32, 256, 4, seed)
+    try:
+        x = synth.hidden_states(seed, 1, T, shape.hidden)
+        xin = torch.from_numpy(x).to("cuda", torch.bfloat16)
+        ref = pair.gpu.prefill(lens, [0, 0], torch.from_numpy(bt).cuda(), xin.clone())
+        # the same slots are rewritten with the same values, so the call repeats exactly
+        out = pair.gpu.prefill(lens, [0, 0], torch.from_numpy(bt).cuda(), xin, hidden_out=xin)
+        torch.cuda.synchronize()
+        assert out.data_ptr() == xin.data_ptr()
+        if T > 128:
+            assert torch.equal(out, ref)
+        else:
+            assert rel_l2(out.double().cpu().numpy(), ref.double().cpu().numpy()) < 1e-2
+    finally:
+        pair.close()
+
+
+def test_forward_calls_return_validation_codes():
+    shape = synth.TINY
+    bt = torch.zeros((2, 4), dtype=torch.int32, device="cuda")
+    pair = Pair(shape, "bf16", 1, 16, 64, 2, 5)
+    try:
+        x = torch.zeros((70, shape.hidden), dtype=torch.bfloat16, device="cuda")
+        with pytest.raises(S.StageError) as e:
+            pair.gpu.prefill([3, 0], [0, 0], bt, x)
+        assert e.value.code == S.STAGE_ERR_INVALID_ARG
+        with pytest.raises(S.StageError) as e:
+            pair.gpu.prefill([70], [0], bt[:1], x)             # 70 tokens > 4 blocks
+        assert e.value.code == S.STAGE_ERR_CAPACITY
+        with pytest.raises(S.StageError) as e:
+            pair.gpu.decode([1, 2, 3], torch.zeros((3, 4), dtype=torch.int32, device="cuda"),
+                            x[:3])                              # 3 seqs > max_seqs 2
+        assert e.value.code == S.STAGE_ERR_CAPACITY
+    finally:
+        pair.close()
