@@ -57,8 +57,9 @@ def prefill_flops(shape, n_layers, chunks):
     lin = 2 * (shape.params_per_layer() - 2 * shape.hidden)
     f = 0
     for ctx, q in chunks:
+        ctx, q = float(ctx), float(q)
         pairs = q * ctx + q * (q + 1) / 2
-        f += q * lin + 4 * shape.head_dim * shape.n_q_heads * pairs
+        f += q * lin + 4.0 * shape.head_dim * shape.n_q_heads * pairs
     return n_layers * f
 
 
