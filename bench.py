@@ -115,7 +115,8 @@ def main():
     import torch
     from paper_2606_18600_amd import stage as S
     from paper_2606_18600_amd import synth
-    from paper_2606_18600_amd.harness import DeviceStage, device_layer_weights
+    from paper_2606_18600_amd.harness import (DeviceStage, device_layer_weights, model_config,
+                                              pack_layer)
 
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
@@ -127,7 +128,9 @@ def main():
     B, K, W = 64, args.steps, args.warmup
 
     log(f"[bench] generating {nL} layers of {shape.name} weights on the device")
-    weights = [device_layer_weights(shape, seed, l, "bf16") for l in range(L0, L1)]
+    cfg = model_config(shape, "bf16")
+    weights = [pack_layer(cfg, device_layer_weights(shape, seed, l, "bf16"), free_source=True)
+               for l in range(L0, L1)]
     ctx0 = synth.uniform_lengths(seed, 1, B, 512, 2048)
     steps_total = W + 2 * K
     dec_final = ctx0 + steps_total + 1
@@ -139,7 +142,8 @@ def main():
     dec_bt_np = synth.make_block_tables(dec_final, int(((dec_final + 15) // 16).max()), alloc)
     pf_bt_np = synth.make_block_tables(p_lens, int(((p_lens + 15) // 16).max()), alloc)
 
-    st = DeviceStage(shape, "bf16", L0, weights, num_blocks, max_tokens=2048, max_seqs=B)
+    st = DeviceStage(shape, "bf16", L0, weights, num_blocks, max_tokens=2048, max_seqs=B,
+                     packed=True)
     # Context KV: random N(0,1) values (decode cost does not depend on them).
     g = torch.Generator(device=dev)
     g.manual_seed(seed)

@@ -22,10 +22,14 @@
  * residual.
  *
  * Conventions shared by every entry point:
- *  - Weights are row-major [N, K] and applied as y = x W^T. w_qkv stacks the
- *    n_q*d query rows, then n_kv*d key rows, then n_kv*d value rows;
- *    w_gate_up stacks ffn gate rows then ffn up rows. Norm gains are [hidden];
- *    q/k-norm gains are [head_dim]. All weights are stored in the mode dtype.
+ *  - Weights are applied as y = x W^T for W [N, K]. In row-major form w_qkv
+ *    stacks the n_q*d query rows, then n_kv*d key rows, then n_kv*d value
+ *    rows; w_gate_up stacks ffn gate rows then ffn up rows. The stage reads
+ *    the four projection matrices in the layout stage_pack_weight() produces
+ *    from that row-major form (bf16: MFMA-fragment-packed; f32: row-major
+ *    unchanged); a weight store packs them once, when it loads them. Norm
+ *    gains are [hidden]; q/k-norm gains are [head_dim]. All weights are stored
+ *    in the mode dtype.
  *  - KV pool (one allocation for the stage's layers):
  *      [n_layers][num_blocks][n_kv][2][block_size][head_dim]
  *    in the mode dtype. Plane 0 holds K as [token][d]; plane 1 holds V
@@ -91,7 +95,8 @@ typedef struct {
 } stage_model_config;
 
 /* Device pointers to one layer's weights (q_norm/k_norm may be NULL unless
- * qk_norm is set). */
+ * qk_norm is set). The four projections must be in the stage_pack_weight()
+ * layout. */
 typedef struct {
   const void* attn_norm; /* [hidden] */
   const void* w_qkv;     /* [(n_q + 2 n_kv) * head_dim, hidden] */
@@ -115,6 +120,25 @@ typedef struct {
   const int32_t* block_tables;  /* device [num_seqs][max_blocks_per_seq] */
   int32_t max_blocks_per_seq;
 } stage_batch;
+
+/* The four projection matrices of a layer. */
+typedef enum {
+  STAGE_W_QKV = 0,     /* [(n_q + 2 n_kv) * head_dim, hidden] */
+  STAGE_W_O = 1,       /* [hidden, n_q * head_dim] */
+  STAGE_W_GATE_UP = 2, /* [2 * ffn, hidden] */
+  STAGE_W_DOWN = 3     /* [hidden, ffn] */
+} stage_weight_kind;
+
+/* Convert one row-major projection matrix (device memory, mode dtype) into
+ * the layout the stage reads, writing dst (device memory of the same size;
+ * must not overlap src). bf16: whole 16 x 32 MFMA operand fragments (1 KB,
+ * lane-major) stored contiguously, rows grouped by 64 so that one group's
+ * fragments for successive k are adjacent; for the gate-up weight each
+ * 64-row group holds 32 gate rows followed by the 32 matching up rows. f32:
+ * a plain copy. Enqueued on `stream`; the caller owns both buffers. Meant
+ * for load time (a weight store), not the forward path. */
+stage_status stage_pack_weight(const stage_model_config* cfg, stage_weight_kind kind,
+                               const void* src, void* dst, void* stream);
 
 /* Create a stage over layers [layer_begin, layer_end) of a model.
  *  layers:   host array of layer_end - layer_begin weight sets (device

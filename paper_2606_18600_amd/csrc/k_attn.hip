@@ -22,6 +22,7 @@
 //   for the fp32 mode.
 #include "common.hpp"
 #include "kernels.hpp"
+#include "packed.hpp"
 
 namespace stage_k {
 
@@ -195,9 +196,16 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const float* __restrict
     if (D > 64) o1 += w * part_o[b * D + lane + 64];
   }
   const float inv = 1.0f / L;
-  OutT* op = out + ((size_t)tok_rows[t] * n_q + h) * D;
-  elem<OutT>::store(op, lane, o0 * inv);
-  if (D > 64) elem<OutT>::store(op, lane + 64, o1 * inv);
+  // bf16: packed activation layout (the O projection's input); fp32: row-major
+  const int row = tok_rows[t], K = n_q * D;
+  if constexpr (sizeof(OutT) == 2) {
+    elem<OutT>::store(out, packed_a_offset(row, h * D + lane, K), o0 * inv);
+    if (D > 64) elem<OutT>::store(out, packed_a_offset(row, h * D + lane + 64, K), o1 * inv);
+  } else {
+    OutT* op = out + (size_t)row * K + h * D;
+    elem<OutT>::store(op, lane, o0 * inv);
+    if (D > 64) elem<OutT>::store(op, lane + 64, o1 * inv);
+  }
 }
 
 // Prefill: one wave per (item, kv head); RT tiles of 16 rows, row r of the
@@ -284,13 +292,16 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(const bf16_t* __restric
     if (!rok[i]) continue;
     const int r = i * 16 + (lane & 15);
     const float inv = 1.0f / st[i].l;
-    bf16_t* op = out + ((size_t)(it.t0 + r / G) * n_q + kvh * G + r % G) * D + (lane >> 4) * 4;
+    // packed activation layout (the O projection's input); 4 consecutive
+    // columns share one 8-byte piece of a fragment lane
+    const int row = it.t0 + r / G;
+    const int col0 = (kvh * G + r % G) * D + (lane >> 4) * 4;
 #pragma unroll
     for (int t = 0; t < D / 16; ++t) {
       u32x2_t w;
       w[0] = pack_bf16x2(oacc[i][t][0] * inv, oacc[i][t][1] * inv);
       w[1] = pack_bf16x2(oacc[i][t][2] * inv, oacc[i][t][3] * inv);
-      *(u32x2_t*)(op + t * 16) = w;
+      *(u32x2_t*)(out + packed_a_offset(row, col0 + t * 16, n_q * D)) = w;
     }
   }
 }

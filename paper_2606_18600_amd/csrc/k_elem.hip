@@ -1,34 +1,81 @@
-// Row-wise and element-wise kernels of a decoder layer: RMSNorm (with the
-// stage-input conversion fused into the first one), per-head q/k RMSNorm +
-// RoPE + paged KV write, SwiGLU, and the stage-output cast.
+// Row-wise and element-wise kernels of a decoder layer: RMSNorm (fused with
+// the stage-input conversion, or with the residual add of split-K partial
+// sums), per-head q/k RMSNorm + RoPE + paged KV write, SwiGLU, and the
+// stage-output cast.
 #include "common.hpp"
 #include "kernels.hpp"
+#include "packed.hpp"
 
 namespace stage_k {
 
 namespace {
 
 constexpr int kNormThreads = 256;
+// One block per row; the row is held in registers (up to kNormVec float4 per
+// thread), so each kernel is one round trip to memory. H is a multiple of 4
+// and at most 4 * kNormThreads * kNormVec.
+constexpr int kNormVec = 16;
+
+template <typename T> struct vec4_io;
+template <> struct vec4_io<float> {
+  __device__ static __forceinline__ float4 load(const float* p, size_t i) {
+    return *(const float4*)(p + i);
+  }
+};
+template <> struct vec4_io<bf16_t> {
+  __device__ static __forceinline__ float4 load(const bf16_t* p, size_t i) {
+    const u32x2_t w = *(const u32x2_t*)(p + i);
+    return make_float4(lo_bf16(w[0]), hi_bf16(w[0]), lo_bf16(w[1]), hi_bf16(w[1]));
+  }
+};
+
+__device__ __forceinline__ void add4(float4& a, const float4 b) {
+  a.x += b.x;
+  a.y += b.y;
+  a.z += b.z;
+  a.w += b.w;
+}
+
+// Store 4 consecutive columns k..k+3 (k % 4 == 0) of row t of an activation:
+// bf16 into the packed layout (8 contiguous bytes), fp32 row-major.
+__device__ __forceinline__ void store_act4(bf16_t* h, int t, int k, int K, float4 v) {
+  u32x2_t w;
+  w[0] = pack_bf16x2(v.x, v.y);
+  w[1] = pack_bf16x2(v.z, v.w);
+  *(u32x2_t*)(h + packed_a_offset(t, k, K)) = w;
+}
+__device__ __forceinline__ void store_act4(float* h, int t, int k, int K, float4 v) {
+  *(float4*)(h + (size_t)t * K + k) = v;
+}
 
 template <typename InT, typename OutT, bool kEmbed>
 __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const InT* __restrict__ in,
                                                                float* __restrict__ x,
+                                                               const float* __restrict__ part,
+                                                               int splits, int T,
                                                                OutT* __restrict__ h,
                                                                const OutT* __restrict__ gain,
                                                                int H, float eps) {
-  // One block per row. H is a multiple of 4 (checked by the runtime).
-  const size_t row = blockIdx.x;
+  const int t = blockIdx.x;
+  const size_t row = (size_t)t * H;
+  const size_t plane = (size_t)T * H;
+  const int H4 = H >> 2;
   __shared__ float red[kNormThreads / STAGE_WAVE];
+  float4 v[kNormVec];
   float ss = 0.f;
-  for (int i = threadIdx.x; i < H; i += kNormThreads) {
-    float v;
-    if constexpr (kEmbed) {
-      v = elem<InT>::load(in, row * H + i);
-      x[row * H + i] = v;
-    } else {
-      v = x[row * H + i];
+#pragma unroll
+  for (int j = 0; j < kNormVec; ++j) {
+    const int i4 = threadIdx.x + j * kNormThreads;
+    if (i4 < H4) {
+      const size_t e = row + 4 * (size_t)i4;
+      if constexpr (kEmbed)
+        v[j] = vec4_io<InT>::load(in, e);
+      else
+        v[j] = *(const float4*)(x + e);
+      for (int sp = 0; sp < splits; ++sp) add4(v[j], *(const float4*)(part + sp * plane + e));
+      if (kEmbed || splits > 0) *(float4*)(x + e) = v[j];
+      ss += v[j].x * v[j].x + v[j].y * v[j].y + v[j].z * v[j].z + v[j].w * v[j].w;
     }
-    ss += v * v;
   }
   ss = wave_sum(ss);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
@@ -37,24 +84,34 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const InT* __rest
 #pragma unroll
   for (int w = 0; w < kNormThreads / STAGE_WAVE; ++w) tot += red[w];
   const float r = 1.0f / sqrtf(tot / (float)H + eps);
-  for (int i = threadIdx.x; i < H; i += kNormThreads) {
-    // embed variant: reread the value just written by this same thread
-    const float v = x[row * H + i];
-    elem<OutT>::store(h, row * H + i, v * r * elem<OutT>::load(gain, i));
+#pragma unroll
+  for (int j = 0; j < kNormVec; ++j) {
+    const int i4 = threadIdx.x + j * kNormThreads;
+    if (i4 < H4) {
+      const float4 g = vec4_io<OutT>::load(gain, 4 * (size_t)i4);
+      store_act4(h, t, 4 * i4, H,
+                 make_float4(v[j].x * r * g.x, v[j].y * r * g.y, v[j].z * r * g.z,
+                             v[j].w * r * g.w));
+    }
   }
 }
 
 template <typename OutT>
-__global__ void output_cast_kernel(const float* __restrict__ x, OutT* __restrict__ out, size_t n) {
-  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n;
-       i += (size_t)gridDim.x * blockDim.x)
-    elem<OutT>::store(out, i, x[i]);
-}
-
-__global__ void fill_zero_kernel(float* __restrict__ p, size_t n) {
-  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n;
-       i += (size_t)gridDim.x * blockDim.x)
-    p[i] = 0.f;
+__global__ __launch_bounds__(256) void output_cast_kernel(const float* __restrict__ x,
+                                                          const float* __restrict__ part,
+                                                          int splits, int T, int H,
+                                                          OutT* __restrict__ out) {
+  const size_t plane = (size_t)T * H;
+  const size_t n4 = plane / 4;
+  for (size_t i4 = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i4 < n4;
+       i4 += (size_t)gridDim.x * blockDim.x) {
+    float4 v = *(const float4*)(x + 4 * i4);
+    for (int sp = 0; sp < splits; ++sp) add4(v, *(const float4*)(part + sp * plane + 4 * i4));
+    elem<OutT>::store(out, 4 * i4 + 0, v.x);
+    elem<OutT>::store(out, 4 * i4 + 1, v.y);
+    elem<OutT>::store(out, 4 * i4 + 2, v.z);
+    elem<OutT>::store(out, 4 * i4 + 3, v.w);
+  }
 }
 
 __device__ __forceinline__ const int32_t* seq_table(const SegTables& t, int seq) {
@@ -63,11 +120,13 @@ __device__ __forceinline__ const int32_t* seq_table(const SegTables& t, int seq)
 }
 
 // One wave per (token, head); heads [0, n_q) are query heads, [n_q, n_q+n_kv)
-// key/value heads. Lane j < d/2 owns the rotate-half pair (j, j + d/2).
+// key/value heads. Lane j < d/2 owns the rotate-half pair (j, j + d/2). The
+// projection is the sum of `splits` partial planes.
 template <typename T>
-__global__ __launch_bounds__(256) void rope_kv_kernel(float* __restrict__ qkv, int zero_after,
-                                                      T* __restrict__ q_out, T* __restrict__ kv,
-                                                      int n_kv, int d, const int32_t* tok_seq,
+__global__ __launch_bounds__(256) void rope_kv_kernel(const float* __restrict__ qkv, int splits,
+                                                      int n_tok, T* __restrict__ q_out,
+                                                      T* __restrict__ kv, int n_kv, int d,
+                                                      const int32_t* tok_seq,
                                                       const int32_t* tok_pos, SegTables tabs,
                                                       const float* __restrict__ cos_tab,
                                                       const float* __restrict__ sin_tab,
@@ -81,14 +140,20 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(float* __restrict__ qkv, i
   const int half = d >> 1;
   const bool act = lane < half;
   const int pos = tok_pos[t];
-  float* row = qkv + (size_t)t * (n_q + 2 * n_kv) * d;
+  const int width = (n_q + 2 * n_kv) * d;
+  const size_t plane = (size_t)n_tok * width;
+  const float* row = qkv + (size_t)t * width;
   const bool is_q = hh < n_q;
   const int kh = hh - n_q;
-  float* src = is_q ? row + (size_t)hh * d : row + (size_t)(n_q + kh) * d;
+  const int col = is_q ? hh * d : (n_q + kh) * d;
   const T* gain = is_q ? q_gain : k_gain;
 
-  float a = act ? src[lane] : 0.f;
-  float b = act ? src[lane + half] : 0.f;
+  float a = 0.f, b = 0.f;
+  if (act)
+    for (int sp = 0; sp < splits; ++sp) {
+      a += row[sp * plane + col + lane];
+      b += row[sp * plane + col + lane + half];
+    }
   if (gain != nullptr) {
     const float ss = wave_sum(a * a + b * b);
     const float r = 1.0f / sqrtf(ss / (float)d + qk_eps);
@@ -102,10 +167,6 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(float* __restrict__ qkv, i
   const float s = sin_tab[(size_t)pos * half + lane];
   const float ra = a * c - b * s;
   const float rb = a * s + b * c;
-  if (zero_after) {
-    src[lane] = 0.f;
-    src[lane + half] = 0.f;
-  }
   if (is_q) {
     T* qo = q_out + ((size_t)t * n_q + hh) * d;
     elem<T>::store(qo, lane, ra);
@@ -119,29 +180,48 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(float* __restrict__ qkv, i
   T* vplane = kplane + (int64_t)kBlock * d;
   elem<T>::store(kplane, (size_t)off * d + lane, ra);
   elem<T>::store(kplane, (size_t)off * d + lane + half, rb);
-  float* vsrc = row + (size_t)(n_q + n_kv + kh) * d;
-  const float va = vsrc[lane], vb = vsrc[lane + half];
-  if (zero_after) {
-    vsrc[lane] = 0.f;
-    vsrc[lane + half] = 0.f;
+  const int vcol = (n_q + n_kv + kh) * d;
+  float va = 0.f, vb = 0.f;
+  for (int sp = 0; sp < splits; ++sp) {
+    va += row[sp * plane + vcol + lane];
+    vb += row[sp * plane + vcol + lane + half];
   }
   elem<T>::store(vplane, (size_t)lane * kBlock + off, va);
   elem<T>::store(vplane, (size_t)(lane + half) * kBlock + off, vb);
 }
 
-template <typename T>
-__global__ void swiglu_kernel(float* __restrict__ gu, T* __restrict__ m, int F, size_t n,
-                              int zero_after) {
+__device__ __forceinline__ float silu_f(float z) { return z / (1.0f + expf(-z)); }
+
+__global__ void swiglu_f32_kernel(const float* __restrict__ gu, float* __restrict__ m, int F,
+                                  size_t n) {
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n;
        i += (size_t)gridDim.x * blockDim.x) {
     const size_t t = i / F, j = i % F;
-    float* g = gu + t * 2 * F + j;
-    const float gv = g[0], uv = g[F];
-    if (zero_after) {
-      g[0] = 0.f;
-      g[F] = 0.f;
+    const float* g = gu + t * 2 * F + j;
+    m[i] = silu_f(g[0]) * g[F];
+  }
+}
+
+// Thread per 4 consecutive output columns c..c+3 of one row; the gate
+// columns of the packed gate-up product are (c/32)*64 + c%32, the up
+// columns 32 further.
+__global__ void swiglu_reduce_kernel(const float* __restrict__ gu, int splits, int T, int F,
+                                     bf16_t* __restrict__ m) {
+  const size_t plane = (size_t)T * 2 * F;
+  const size_t n4 = (size_t)T * F / 4;
+  for (size_t i4 = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i4 < n4;
+       i4 += (size_t)gridDim.x * blockDim.x) {
+    const int t = (int)(i4 / (F / 4));
+    const int c = (int)(i4 % (F / 4)) * 4;
+    const size_t gcol = (size_t)t * 2 * F + (c / 32) * 64 + (c % 32);
+    float4 g = make_float4(0.f, 0.f, 0.f, 0.f), u = g;
+    for (int sp = 0; sp < splits; ++sp) {
+      add4(g, *(const float4*)(gu + sp * plane + gcol));
+      add4(u, *(const float4*)(gu + sp * plane + gcol + 32));
     }
-    elem<T>::store(m, i, gv / (1.0f + expf(-gv)) * uv);
+    store_act4(m, t, c, F,
+               make_float4(silu_f(g.x) * u.x, silu_f(g.y) * u.y, silu_f(g.z) * u.z,
+                           silu_f(g.w) * u.w));
   }
 }
 
@@ -157,66 +237,68 @@ hipError_t embed_norm(DType dt, const void* hidden_in, float* x, void* h, const 
   if (T == 0) return hipSuccess;
   if (dt == DT_BF16)
     rmsnorm_kernel<bf16_t, bf16_t, true><<<T, kNormThreads, 0, s>>>(
-        (const bf16_t*)hidden_in, x, (bf16_t*)h, (const bf16_t*)gain, H, eps);
+        (const bf16_t*)hidden_in, x, nullptr, 0, T, (bf16_t*)h, (const bf16_t*)gain, H, eps);
   else
     rmsnorm_kernel<float, float, true><<<T, kNormThreads, 0, s>>>(
-        (const float*)hidden_in, x, (float*)h, (const float*)gain, H, eps);
+        (const float*)hidden_in, x, nullptr, 0, T, (float*)h, (const float*)gain, H, eps);
   return hipGetLastError();
 }
 
-hipError_t rmsnorm(DType dt, const float* x, void* h, const void* gain, int T, int H, float eps,
-                   hipStream_t s) {
+hipError_t rmsnorm(DType dt, float* x, Partials add, void* h, const void* gain, int T, int H,
+                   float eps, hipStream_t s) {
   if (T == 0) return hipSuccess;
   if (dt == DT_BF16)
     rmsnorm_kernel<float, bf16_t, false><<<T, kNormThreads, 0, s>>>(
-        nullptr, const_cast<float*>(x), (bf16_t*)h, (const bf16_t*)gain, H, eps);
+        nullptr, x, add.p, add.splits, T, (bf16_t*)h, (const bf16_t*)gain, H, eps);
   else
     rmsnorm_kernel<float, float, false><<<T, kNormThreads, 0, s>>>(
-        nullptr, const_cast<float*>(x), (float*)h, (const float*)gain, H, eps);
+        nullptr, x, add.p, add.splits, T, (float*)h, (const float*)gain, H, eps);
   return hipGetLastError();
 }
 
-hipError_t output_cast(DType dt, const float* x, void* out, size_t n, hipStream_t s) {
-  if (n == 0) return hipSuccess;
+hipError_t output_cast(DType dt, const float* x, Partials add, void* out, int T, int H,
+                       hipStream_t s) {
+  const size_t n4 = (size_t)T * H / 4;
+  if (n4 == 0) return hipSuccess;
   if (dt == DT_BF16)
-    output_cast_kernel<bf16_t><<<grid_for(n, 256), 256, 0, s>>>(x, (bf16_t*)out, n);
+    output_cast_kernel<bf16_t><<<grid_for(n4, 256), 256, 0, s>>>(x, add.p, add.splits, T, H,
+                                                                 (bf16_t*)out);
   else
-    output_cast_kernel<float><<<grid_for(n, 256), 256, 0, s>>>(x, (float*)out, n);
+    output_cast_kernel<float><<<grid_for(n4, 256), 256, 0, s>>>(x, add.p, add.splits, T, H,
+                                                                (float*)out);
   return hipGetLastError();
 }
 
-hipError_t fill_zero_f32(float* p, size_t n, hipStream_t s) {
-  if (n == 0) return hipSuccess;
-  fill_zero_kernel<<<grid_for(n, 256), 256, 0, s>>>(p, n);
-  return hipGetLastError();
-}
-
-hipError_t rope_kv_write(DType dt, float* qkv, int zero_after, void* q_out, KVLayer kv,
+hipError_t rope_kv_write(DType dt, const float* qkv, int splits, void* q_out, KVLayer kv,
                          const int32_t* tok_seq, const int32_t* tok_pos, SegTables tabs,
                          const float* cos_tab, const float* sin_tab, const void* q_gain,
                          const void* k_gain, float qk_eps, int T, int n_q, hipStream_t s) {
   if (T == 0) return hipSuccess;
   dim3 grid(T, (n_q + kv.n_kv + 3) / 4);
   if (dt == DT_BF16)
-    rope_kv_kernel<bf16_t><<<grid, 256, 0, s>>>(qkv, zero_after, (bf16_t*)q_out, (bf16_t*)kv.base,
+    rope_kv_kernel<bf16_t><<<grid, 256, 0, s>>>(qkv, splits, T, (bf16_t*)q_out, (bf16_t*)kv.base,
                                                 kv.n_kv, kv.head_dim, tok_seq, tok_pos, tabs,
                                                 cos_tab, sin_tab, (const bf16_t*)q_gain,
                                                 (const bf16_t*)k_gain, qk_eps, n_q);
   else
-    rope_kv_kernel<float><<<grid, 256, 0, s>>>(qkv, zero_after, (float*)q_out, (float*)kv.base,
+    rope_kv_kernel<float><<<grid, 256, 0, s>>>(qkv, splits, T, (float*)q_out, (float*)kv.base,
                                                kv.n_kv, kv.head_dim, tok_seq, tok_pos, tabs,
                                                cos_tab, sin_tab, (const float*)q_gain,
                                                (const float*)k_gain, qk_eps, n_q);
   return hipGetLastError();
 }
 
-hipError_t swiglu(DType dt, float* gu, void* m, int T, int F, int zero_after, hipStream_t s) {
+hipError_t swiglu_f32(const float* gu, float* m, int T, int F, hipStream_t s) {
   const size_t n = (size_t)T * F;
   if (n == 0) return hipSuccess;
-  if (dt == DT_BF16)
-    swiglu_kernel<bf16_t><<<grid_for(n, 256), 256, 0, s>>>(gu, (bf16_t*)m, F, n, zero_after);
-  else
-    swiglu_kernel<float><<<grid_for(n, 256), 256, 0, s>>>(gu, (float*)m, F, n, zero_after);
+  swiglu_f32_kernel<<<grid_for(n, 256), 256, 0, s>>>(gu, m, F, n);
+  return hipGetLastError();
+}
+
+hipError_t swiglu_reduce_bf16(Partials gu, uint16_t* m, int T, int F, hipStream_t s) {
+  const size_t n4 = (size_t)T * F / 4;
+  if (n4 == 0) return hipSuccess;
+  swiglu_reduce_kernel<<<grid_for(n4, 256), 256, 0, s>>>(gu.p, gu.splits, T, F, m);
   return hipGetLastError();
 }
 

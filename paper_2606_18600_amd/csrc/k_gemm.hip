@@ -1,151 +1,263 @@
 // Linear layers of a decoder layer (QKV, O, gate-up, down):
-//   acc[m][n] = sum_k A[m][k] * W[n][k],  A [M,K] row-major, W [N,K] row-major.
+//   acc[m][n] = sum_k A[m][k] * W[n][k]
+// with bf16 operands in the fragment-packed layouts of packed.hpp and fp32
+// accumulation on v_mfma_f32_16x16x32_bf16.
 //
-// * gemm_tiled_bf16: LDS-staged bf16 MFMA tiles (v_mfma_f32_32x32x16_bf16,
-//   fp32 accumulate) for steps with many tokens (prefill, mixed), where the
-//   products are compute-bound. Fused epilogues: fp32 store, residual add,
-//   SwiGLU.
-// * gemm_skinny_bf16: split-K weight streaming for decode-sized M, where the
-//   product is bound by reading W once from HBM. Each wave streams a 64-row
-//   slab of W over one K range and adds its fp32 partial sums atomically.
-// * gemm_tiled_f32: plain fp32 SIMT tiles for the fp32 mode.
+// * gemm_skinny_bf16: decode-sized M (<= 128). The product is bound by
+//   reading W once from HBM. Block = 4 waves on 4 adjacent 64-row groups of W
+//   over one K range (the A fragments they share come through L1). Each wave
+//   streams its group's fragments (contiguous in the packed layout) with
+//   non-temporal loads, two 64-wide k steps in flight, and writes an fp32
+//   partial tile per K split; the consumer kernel sums the splits. With one
+//   split the gate-up GEMM applies SwiGLU in its epilogue.
+// * gemm_tiled_bf16: many rows (prefill, mixed steps), compute-bound.
+//   128 x 128 block tiles, 64-wide k steps double-buffered in LDS, 4 waves of
+//   64 x 64; epilogues: fp32 store, residual add, SwiGLU.
+// * gemm_tiled_f32: plain fp32 SIMT tiles for the fp32 mode (row-major).
 #include "common.hpp"
 #include "kernels.hpp"
+#include "packed.hpp"
 
 namespace stage_k {
 
 namespace {
 
-// ---------------------------------------------------------------------------
-// bf16 MFMA tiled GEMM
-// ---------------------------------------------------------------------------
-constexpr int TB_M = 128, TB_N = 128, TB_K = 64;  // block tile
-constexpr int TB_THREADS = 256;                    // 4 waves, 2 x 2, 64 x 64 each
-constexpr int TB_CHUNKS = TB_K / 8;                // 16-byte chunks per LDS row
-
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + expf(-z)); }
+
+// ---------------------------------------------------------------------------
+// weight packing
+// ---------------------------------------------------------------------------
+__global__ void pack_weight_kernel(const bf16_t* __restrict__ src, bf16_t* __restrict__ dst, int N,
+                                   int K, int gate_up_ffn) {
+  const size_t chunks = (size_t)N * K / 8;
+  const int KT = K / 32;
+  for (size_t c = blockIdx.x * (size_t)blockDim.x + threadIdx.x; c < chunks;
+       c += (size_t)gridDim.x * blockDim.x) {
+    const size_t frag = c / 64;
+    const int lane = (int)(c % 64);
+    const int j = (int)(frag % 4);
+    const size_t rest = frag / 4;
+    const int g = (int)(rest / KT), kt = (int)(rest % KT);
+    const int n = g * 64 + j * 16 + (lane & 15);
+    const int k = kt * 32 + (lane >> 4) * 8;
+    const int row = gate_up_ffn > 0 ? gate_up_source_row(n, gate_up_ffn) : n;
+    *(u32x4_t*)(dst + c * 8) = ldg128(src + (size_t)row * K + k);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 split-K GEMM for decode-sized M
+// ---------------------------------------------------------------------------
+constexpr int SK_WAVES = 4;
+
+enum SkinnyEpi { SK_PARTIAL = 0, SK_SWIGLU = 1 };
+
+template <int MT, int EPI>
+__global__ __launch_bounds__(SK_WAVES * 64) void gemm_skinny_bf16(const bf16_t* __restrict__ A,
+                                                                  const bf16_t* __restrict__ W,
+                                                                  int M, int N, int K, int kb_len,
+                                                                  void* __restrict__ out) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = blockIdx.x * SK_WAVES + wave;
+  if (g * 64 >= N) return;  // no barriers in this kernel
+  const int kbeg = blockIdx.y * kb_len;
+  const int iters = (min(kb_len, K - kbeg)) / 64;  // >= 1: the grid covers K exactly
+  const int r16 = lane & 15;
+  const int KT = K / 32;
+  const bf16_t* wp = W + ((size_t)g * KT + kbeg / 32) * 4 * 512 + lane * 8;
+  const bf16_t* ap = A + (size_t)(kbeg / 32) * 512 + lane * 8;
+
+  f32x4_t acc[MT][4];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  u32x4_t wx[2][4], ax[MT][2], wy[2][4], ay[MT][2];
+  // Loads of k step t (clamped to the last step so that the prefetch past the
+  // end stays in bounds; its data is never used).
+  auto load = [&](u32x4_t (&w)[2][4], u32x4_t (&a)[MT][2], int t) {
+    t = t < iters ? t : iters - 1;
+    const bf16_t* q = wp + (size_t)t * 8 * 512;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        w[h][j] = __builtin_nontemporal_load((const u32x4_t*)(q + (h * 4 + j) * 512));
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) a[i][h] = ldg128(ap + ((size_t)i * KT + 2 * t + h) * 512);
+  };
+  auto compute = [&](const u32x4_t (&w)[2][4], const u32x4_t (&a)[MT][2]) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mfma16x16x32(a[i][h], w[h][j], acc[i][j]);
+  };
+  // Ping-pong over two register sets; the scheduling barriers keep each
+  // step's loads issued ahead of the previous step's MFMAs, so the waits only
+  // cover the older loads.
+  load(wx, ax, 0);
+  int t = 0;
+  for (; t + 1 < iters; t += 2) {
+    load(wy, ay, t + 1);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(wx, ax);
+    __builtin_amdgcn_sched_barrier(0);
+    load(wx, ax, t + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(wy, ay);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if (t < iters) compute(wx, ax);
+
+  // C layout of a 16x16 tile: lane l holds column l%16, rows (l/16)*4 + r.
+  if (EPI == SK_PARTIAL) {
+    float* part = (float*)out + (size_t)blockIdx.y * M * N;
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = i * 16 + (lane >> 4) * 4 + r;
+        if (m >= M) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) part[(size_t)m * N + g * 64 + j * 16 + r16] = acc[i][j][r];
+      }
+  } else {
+    // tiles 0,1: gate columns 32g..32g+31; tiles 2,3: the matching up columns
+    const int F = N / 2;
+    bf16_t* mo = (bf16_t*)out;
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = i * 16 + (lane >> 4) * 4 + r;
+        if (m >= M) continue;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int c = g * 32 + j * 16 + r16;
+          mo[packed_a_offset(m, c, F)] = f32_to_bf16(silu_f(acc[i][j][r]) * acc[i][j + 2][r]);
+        }
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 tiled GEMM (prefill / mixed)
+// ---------------------------------------------------------------------------
+constexpr int TB_M = 128, TB_N = 128, TB_K = 64;
+constexpr int TB_THREADS = 256;
 
 template <int EPI>
 __global__ __launch_bounds__(TB_THREADS) void gemm_tiled_bf16(const bf16_t* __restrict__ A,
                                                               const bf16_t* __restrict__ W, int M,
                                                               int N, int K, void* __restrict__ out) {
-  // LDS rows are TB_K bf16 = 128 B = 8 chunks of 16 B; chunk c of row r is
-  // stored at chunk position c ^ (r & 7) so that MFMA fragment reads of 8
-  // consecutive rows hit 8 different chunk positions.
-  __shared__ u32x4_t As[2][TB_M * TB_CHUNKS];
-  __shared__ u32x4_t Bs[2][TB_N * TB_CHUNKS];
+  // LDS tiles hold whole fragments: A [8 m-tiles][2 k-tiles][64 lanes],
+  // B [2 groups][2 k-tiles][4 n-tiles][64 lanes], 16 bytes per lane.
+  __shared__ u32x4_t As[2][TB_M / 16 * 2 * 64];
+  __shared__ u32x4_t Bs[2][2 * 2 * 4 * 64];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const int m0 = blockIdx.x * TB_M;
-  const int nb = blockIdx.y;
-  const int half_n = N / 2;  // SwiGLU: gate rows [0, N/2), up rows [N/2, N)
+  const int mt0 = blockIdx.x * (TB_M / 16);  // first m-tile of the block
+  const int g0 = blockIdx.y * 2;             // first 64-row group of W
+  const int KT = K / 32;
 
-  // Global rows this thread stages (4 chunks of A, 4 of B per K tile).
+  // Staging map: 4 chunks of A and 4 of B per thread per K tile. A chunk q
+  // (0..1023) is (m-tile q/128, k-tile (q/64)%2, lane q%64); B chunk q is
+  // (group q/512, (k-tile, n-tile, lane) = q%512), each contiguous in memory.
   const bf16_t* a_src[4];
   const bf16_t* b_src[4];
-  int st_off[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int q = tid + i * TB_THREADS;
-    const int r = q >> 3, c = q & 7;
-    int am = m0 + r;
-    am = am < M ? am : M - 1;
-    a_src[i] = A + (size_t)am * K + c * 8;
-    int wrow;
-    if (EPI == EPI_SWIGLU)
-      wrow = (((r >> 5) & 1) ? half_n : 0) + nb * (TB_N / 2) + (r >> 6) * 32 + (r & 31);
-    else
-      wrow = nb * TB_N + r;
-    b_src[i] = W + (size_t)wrow * K + c * 8;
-    st_off[i] = r * TB_CHUNKS + (c ^ (r & 7));
+  for (int p = 0; p < 4; ++p) {
+    const int q = tid + p * TB_THREADS;
+    a_src[p] = A + ((size_t)(mt0 + q / 128) * KT) * 512 + (q % 128) * 8;
+    b_src[p] = W + ((size_t)(g0 + q / 512) * KT * 4) * 512 + (q % 512) * 8;
   }
 
-  f32x16_t acc[2][2];
+  f32x4_t acc[4][4];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{};
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   u32x4_t ra[4], rb[4];
-  const int KT = K / TB_K;
+  const int KTILES = K / TB_K;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    ra[i] = ldg128(a_src[i]);
-    rb[i] = ldg128(b_src[i]);
+  for (int p = 0; p < 4; ++p) {
+    ra[p] = ldg128(a_src[p]);
+    rb[p] = ldg128(b_src[p]);
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    As[0][st_off[i]] = ra[i];
-    Bs[0][st_off[i]] = rb[i];
+  for (int p = 0; p < 4; ++p) {
+    As[0][tid + p * TB_THREADS] = ra[p];
+    Bs[0][tid + p * TB_THREADS] = rb[p];
   }
   __syncthreads();
 
-  const int frow = lane & 31;   // fragment row within a 32-row tile
-  const int fsub = lane >> 5;   // which 8-wide k half of a 16-wide k step
-  for (int kt = 0; kt < KT; ++kt) {
+  for (int kt = 0; kt < KTILES; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < KT) {
-      const size_t koff = (size_t)(kt + 1) * TB_K;
+    const bool more = kt + 1 < KTILES;
+    if (more) {
+      // next K tile: +2 k-tiles of A fragments, +2*4 fragments of W
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        ra[i] = ldg128(a_src[i] + koff);
-        rb[i] = ldg128(b_src[i] + koff);
+      for (int p = 0; p < 4; ++p) {
+        ra[p] = ldg128(a_src[p] + (size_t)(kt + 1) * 2 * 512);
+        rb[p] = ldg128(b_src[p] + (size_t)(kt + 1) * 2 * 4 * 512);
       }
     }
 #pragma unroll
-    for (int kk = 0; kk < TB_K / 16; ++kk) {
-      const int c = kk * 2 + fsub;
-      u32x4_t fa[2], fb[2];
+    for (int h = 0; h < 2; ++h) {
+      u32x4_t fa[4], fb[4];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int r = wm * 64 + i * 32 + frow;
-        fa[i] = As[buf][r * TB_CHUNKS + (c ^ (r & 7))];
-      }
+      for (int i = 0; i < 4; ++i) fa[i] = As[buf][((wm * 4 + i) * 2 + h) * 64 + lane];
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int r = wn * 64 + j * 32 + frow;
-        fb[j] = Bs[buf][r * TB_CHUNKS + (c ^ (r & 7))];
-      }
+      for (int j = 0; j < 4; ++j) fb[j] = Bs[buf][((wn * 2 + h) * 4 + j) * 64 + lane];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mfma32x32x16(fa[i], fb[j], acc[i][j]);
+        for (int j = 0; j < 4; ++j) acc[i][j] = mfma16x16x32(fa[i], fb[j], acc[i][j]);
     }
-    if (kt + 1 < KT) {
+    if (more) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        As[buf ^ 1][st_off[i]] = ra[i];
-        Bs[buf ^ 1][st_off[i]] = rb[i];
+      for (int p = 0; p < 4; ++p) {
+        As[buf ^ 1][tid + p * TB_THREADS] = ra[p];
+        Bs[buf ^ 1][tid + p * TB_THREADS] = rb[p];
       }
     }
     __syncthreads();
   }
 
-  // Epilogue. Accumulator element e of lane l holds row
-  // (e/4)*8 + (l/32)*4 + e%4 and column l%32 of its 32x32 tile.
-  const int col = lane & 31;
+  // Epilogue: lane l holds column (g*64 + j*16 + l%16), rows (l/16)*4 + r of
+  // m-tile (mt0 + wm*4 + i).
+  const int g = g0 + wn;
+  const int r16 = lane & 15;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < 4; ++i) {
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int m = m0 + wm * 64 + i * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
+    for (int r = 0; r < 4; ++r) {
+      const int m = (mt0 + wm * 4 + i) * 16 + (lane >> 4) * 4 + r;
       if (m >= M) continue;
       if (EPI == EPI_SWIGLU) {
-        // tile j=0 holds gate rows, j=1 the matching up rows
-        const int n = nb * (TB_N / 2) + wn * 32 + col;
-        const float g = acc[i][0][e], u = acc[i][1][e];
-        ((bf16_t*)out)[(size_t)m * half_n + n] = f32_to_bf16(silu_f(g) * u);
-      } else {
+        const int F = N / 2;
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-          const int n = nb * TB_N + wn * 64 + j * 32 + col;
-          float* o = (float*)out + (size_t)m * N + n;
+          const int c = g * 32 + j * 16 + r16;
+          ((bf16_t*)out)[packed_a_offset(m, c, F)] =
+              f32_to_bf16(silu_f(acc[i][j][r]) * acc[i][j + 2][r]);
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          float* o = (float*)out + (size_t)m * N + g * 64 + j * 16 + r16;
           if (EPI == EPI_RESID_ADD)
-            *o += acc[i][j][e];
+            *o += acc[i][j][r];
           else
-            *o = acc[i][j][e];
+            *o = acc[i][j][r];
         }
       }
     }
@@ -153,81 +265,7 @@ __global__ __launch_bounds__(TB_THREADS) void gemm_tiled_bf16(const bf16_t* __re
 }
 
 // ---------------------------------------------------------------------------
-// bf16 split-K skinny GEMM (decode)
-// ---------------------------------------------------------------------------
-// Wave tile: all M rows (MT tiles of 16) x SK_NT tiles of 16 columns, one K
-// range. Per 64-wide k step, lane l owns k offsets (l/16)*16 .. +15 of both
-// operands (two 16-byte loads), feeding two v_mfma_f32_16x16x32_bf16; the
-// reduction over k is order-free, so A and W only need the same mapping.
-constexpr int SK_WAVES = 4;
-
-template <int MT, int SK_NT>
-__global__ __launch_bounds__(SK_WAVES * 64) void gemm_skinny_bf16(const bf16_t* __restrict__ A,
-                                                                  const bf16_t* __restrict__ W,
-                                                                  int M, int N, int K, int k_split,
-                                                                  float* __restrict__ out) {
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int n0 = (blockIdx.x * SK_WAVES + wave) * (SK_NT * 16);
-  if (n0 >= N) return;
-  const int kb = blockIdx.y * k_split;
-  const int ke = min(K, kb + k_split);
-  const int r16 = lane & 15;
-  const int koff = (lane >> 4) * 16;
-
-  const bf16_t* wp[SK_NT];
-#pragma unroll
-  for (int j = 0; j < SK_NT; ++j) wp[j] = W + (size_t)(n0 + j * 16 + r16) * K + koff;
-  const bf16_t* ap[MT];
-#pragma unroll
-  for (int i = 0; i < MT; ++i) {
-    int m = i * 16 + r16;
-    m = m < M ? m : M - 1;
-    ap[i] = A + (size_t)m * K + koff;
-  }
-
-  f32x4_t acc[MT][SK_NT];
-#pragma unroll
-  for (int i = 0; i < MT; ++i)
-#pragma unroll
-    for (int j = 0; j < SK_NT; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  for (int k = kb; k < ke; k += 64) {
-    u32x4_t w0[SK_NT], w1[SK_NT], a0[MT], a1[MT];
-#pragma unroll
-    for (int j = 0; j < SK_NT; ++j) {
-      w0[j] = ldg128(wp[j] + k);
-      w1[j] = ldg128(wp[j] + k + 8);
-    }
-#pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      a0[i] = ldg128(ap[i] + k);
-      a1[i] = ldg128(ap[i] + k + 8);
-    }
-#pragma unroll
-    for (int i = 0; i < MT; ++i)
-#pragma unroll
-      for (int j = 0; j < SK_NT; ++j) {
-        acc[i][j] = mfma16x16x32(a0[i], w0[j], acc[i][j]);
-        acc[i][j] = mfma16x16x32(a1[i], w1[j], acc[i][j]);
-      }
-  }
-
-  // C layout of a 16x16 tile: lane l holds column l%16, rows (l/16)*4 + r.
-#pragma unroll
-  for (int i = 0; i < MT; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = i * 16 + (lane >> 4) * 4 + r;
-      if (m >= M) continue;
-#pragma unroll
-      for (int j = 0; j < SK_NT; ++j)
-        unsafeAtomicAdd(out + (size_t)m * N + n0 + j * 16 + r16, acc[i][j][r]);
-    }
-}
-
-// ---------------------------------------------------------------------------
-// fp32 SIMT tiled GEMM (fp32 mode)
+// fp32 SIMT tiled GEMM (fp32 mode, row-major operands)
 // ---------------------------------------------------------------------------
 constexpr int TF = 64, TF_K = 16;
 
@@ -278,7 +316,64 @@ __global__ __launch_bounds__(256) void gemm_tiled_f32(const float* __restrict__ 
   }
 }
 
+template <int MT>
+hipError_t launch_skinny(const bf16_t* a, const bf16_t* w, int M, int N, int K, int kb_len,
+                         bool swiglu, void* out, hipStream_t s) {
+  const int groups = N / 64;
+  dim3 grid((groups + SK_WAVES - 1) / SK_WAVES, (K + kb_len - 1) / kb_len);
+  if (swiglu)
+    gemm_skinny_bf16<MT, SK_SWIGLU><<<grid, SK_WAVES * 64, 0, s>>>(a, w, M, N, K, kb_len, out);
+  else
+    gemm_skinny_bf16<MT, SK_PARTIAL><<<grid, SK_WAVES * 64, 0, s>>>(a, w, M, N, K, kb_len, out);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t pack_weight(const void* src, void* dst, int N, int K, int gate_up_ffn, hipStream_t s) {
+  if (N % 64 != 0 || K % 32 != 0) return hipErrorInvalidValue;
+  const size_t chunks = (size_t)N * K / 8;
+  size_t blocks = (chunks + 255) / 256;
+  if (blocks > 16384) blocks = 16384;
+  pack_weight_kernel<<<(int)blocks, 256, 0, s>>>((const bf16_t*)src, (bf16_t*)dst, N, K,
+                                                 gate_up_ffn);
+  return hipGetLastError();
+}
+
+int skinny_kb_len(int K, int splits) {
+  int kb = (K + splits - 1) / splits;
+  return (kb + 63) / 64 * 64;
+}
+
+int skinny_splits(int N, int K, int target_waves) {
+  const int groups = N / 64;
+  int s = 1;
+  while (s < 8 && groups * s * 2 <= target_waves && K / (s * 2) >= 64) s *= 2;
+  // the number of K ranges actually launched after rounding the range up
+  const int kb = skinny_kb_len(K, s);
+  return (K + kb - 1) / kb;
+}
+
+hipError_t gemm_skinny(const void* A, const void* W, int M, int N, int K, int splits,
+                       bool swiglu, void* out, hipStream_t s) {
+  if (M == 0) return hipSuccess;
+  if (M > 128 || N % 64 != 0 || K % 64 != 0 || splits < 1 || (swiglu && splits != 1))
+    return hipErrorInvalidValue;
+  const int kb = skinny_kb_len(K, splits);
+  if ((K + kb - 1) / kb != splits) return hipErrorInvalidValue;  // every split must be non-empty
+  const bf16_t* a = (const bf16_t*)A;
+  const bf16_t* w = (const bf16_t*)W;
+  switch ((M + 15) / 16) {
+    case 1: return launch_skinny<1>(a, w, M, N, K, kb, swiglu, out, s);
+    case 2: return launch_skinny<2>(a, w, M, N, K, kb, swiglu, out, s);
+    case 3: return launch_skinny<3>(a, w, M, N, K, kb, swiglu, out, s);
+    case 4: return launch_skinny<4>(a, w, M, N, K, kb, swiglu, out, s);
+    case 5: return launch_skinny<5>(a, w, M, N, K, kb, swiglu, out, s);
+    case 6: return launch_skinny<6>(a, w, M, N, K, kb, swiglu, out, s);
+    case 7: return launch_skinny<7>(a, w, M, N, K, kb, swiglu, out, s);
+    default: return launch_skinny<8>(a, w, M, N, K, kb, swiglu, out, s);
+  }
+}
 
 hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int N, int K,
                 void* out, hipStream_t s) {
@@ -311,37 +406,6 @@ hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int
       break;
     default:
       return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
-}
-
-template <int MT, int NT>
-static void launch_skinny(const bf16_t* a, const bf16_t* w, int M, int N, int K, int k_split,
-                          float* out, hipStream_t s) {
-  const int cols_per_block = SK_WAVES * NT * 16;
-  dim3 grid((N + cols_per_block - 1) / cols_per_block, (K + k_split - 1) / k_split);
-  gemm_skinny_bf16<MT, NT><<<grid, SK_WAVES * 64, 0, s>>>(a, w, M, N, K, k_split, out);
-}
-
-hipError_t gemm_skinny(DType dt, const void* A, const void* W, int M, int N, int K, float* out,
-                       int k_split, hipStream_t s) {
-  if (M == 0) return hipSuccess;
-  const int mt = (M + 15) / 16;
-  const int nt = mt <= 4 ? 4 : 2;
-  if (dt != DT_BF16 || M > 128 || N % (nt * 16) != 0 || K % 64 != 0 || k_split % 64 != 0 ||
-      k_split <= 0)
-    return hipErrorInvalidValue;
-  const bf16_t* a = (const bf16_t*)A;
-  const bf16_t* w = (const bf16_t*)W;
-  switch (mt) {
-    case 1: launch_skinny<1, 4>(a, w, M, N, K, k_split, out, s); break;
-    case 2: launch_skinny<2, 4>(a, w, M, N, K, k_split, out, s); break;
-    case 3: launch_skinny<3, 4>(a, w, M, N, K, k_split, out, s); break;
-    case 4: launch_skinny<4, 4>(a, w, M, N, K, k_split, out, s); break;
-    case 5: launch_skinny<5, 2>(a, w, M, N, K, k_split, out, s); break;
-    case 6: launch_skinny<6, 2>(a, w, M, N, K, k_split, out, s); break;
-    case 7: launch_skinny<7, 2>(a, w, M, N, K, k_split, out, s); break;
-    default: launch_skinny<8, 2>(a, w, M, N, K, k_split, out, s); break;
   }
   return hipGetLastError();
 }

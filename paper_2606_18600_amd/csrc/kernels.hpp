@@ -56,26 +56,50 @@ struct PrefillItem {
   int32_t npos;
 };
 
+// Split-K partial sums of an fp32 [M, N] result: `splits` planes of M * N
+// floats (splits == 0: none).
+struct Partials {
+  const float* p;
+  int splits;
+};
+
+// x = fp32(hidden_in); h = RMSNorm(x) * gain. bf16 mode writes h in the packed
+// activation layout, fp32 mode row-major.
 hipError_t embed_norm(DType dt, const void* hidden_in, float* x, void* h, const void* gain,
                       int T, int H, float eps, hipStream_t s);
-hipError_t rmsnorm(DType dt, const float* x, void* h, const void* gain, int T, int H, float eps,
-                   hipStream_t s);
-hipError_t output_cast(DType dt, const float* x, void* out, size_t n, hipStream_t s);
-hipError_t fill_zero_f32(float* p, size_t n, hipStream_t s);
+// x += sum of the partials; h = RMSNorm(x) * gain (layout as above).
+hipError_t rmsnorm(DType dt, float* x, Partials add, void* h, const void* gain, int T, int H,
+                   float eps, hipStream_t s);
+// out = x + sum of the partials, in the mode dtype, row-major.
+hipError_t output_cast(DType dt, const float* x, Partials add, void* out, int T, int H,
+                       hipStream_t s);
 
-hipError_t rope_kv_write(DType dt, float* qkv, int zero_after, void* q_out, KVLayer kv,
+// qkv: fp32 [splits][T][(n_q + 2 n_kv) d] (summed over splits).
+hipError_t rope_kv_write(DType dt, const float* qkv, int splits, void* q_out, KVLayer kv,
                          const int32_t* tok_seq, const int32_t* tok_pos, SegTables tabs,
                          const float* cos_tab, const float* sin_tab, const void* q_gain,
                          const void* k_gain, float qk_eps, int T, int n_q, hipStream_t s);
 
-hipError_t swiglu(DType dt, float* gu, void* m, int T, int F, int zero_after, hipStream_t s);
+// fp32 mode: m = silu(gu[:, :F]) * gu[:, F:] (row-major).
+hipError_t swiglu_f32(const float* gu, float* m, int T, int F, hipStream_t s);
+// bf16 mode: gu = split-K partials [splits][T][2F] in packed gate-up column
+// order; m (packed activation layout [T, F]) = silu(gate) * up.
+hipError_t swiglu_reduce_bf16(Partials gu, uint16_t* m, int T, int F, hipStream_t s);
 
-// GEMMs. `skinny` selects the split-K weight-streaming kernel (EPI_ATOMIC_F32
-// or EPI_RESID_ADD only), else the LDS-tiled kernel.
+// Pack a row-major bf16 [N, K] weight into the packed layout; gate_up_ffn > 0
+// marks the fused gate-up weight (N = 2 * gate_up_ffn).
+hipError_t pack_weight(const void* src, void* dst, int N, int K, int gate_up_ffn, hipStream_t s);
+
+// GEMMs. gemm_skinny (bf16, M <= 128): packed A and W; writes `splits` fp32
+// partial planes [splits][M][N] into out, or with swiglu (splits == 1) the
+// SwiGLU product in the packed activation layout [M, N/2].
+int skinny_splits(int N, int K, int target_waves);
+int skinny_kb_len(int K, int splits);
+hipError_t gemm_skinny(const void* A, const void* W, int M, int N, int K, int splits, bool swiglu,
+                       void* out, hipStream_t s);
+// gemm: bf16 = LDS-tiled MFMA over packed A and W; fp32 = SIMT, row-major.
 hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int N, int K,
                 void* out, hipStream_t s);
-hipError_t gemm_skinny(DType dt, const void* A, const void* W, int M, int N, int K, float* out,
-                       int k_split, hipStream_t s);
 
 hipError_t attn_decode(DType dt, const void* q, KVLayer kv, SegTables tabs,
                        const DecodeItem* items, int n_items, int n_q, float* part_o,

@@ -64,15 +64,16 @@ struct stage {
   size_t esize = 4;
   size_t kv_layer_bytes = 0;
   int device = 0;
-  int skinny_rows = 0;  // rows of the split-K accumulators (0 in fp32 mode)
-  int skinny_waves = 2048;
+  int skinny_rows = 0;  // steps with at most this many tokens use split-K GEMMs
+  // K splits of the four split-K GEMMs (QKV, O, gate-up, down)
+  int s_qkv = 1, s_o = 1, s_gu = 1, s_down = 1;
 
   // workspace
-  Region r_x, r_h, r_qkv, r_q, r_attn, r_m, r_gu, r_part_o, r_part_ml, r_meta, r_cos, r_sin;
+  Region r_x, r_h, r_qkv, r_q, r_attn, r_m, r_gu, r_part_x, r_part_o, r_part_ml, r_meta, r_cos,
+      r_sin;
   size_t ws_bytes = 0;
   char* ws = nullptr;
   size_t meta_ints = 0;
-  bool acc_zero = false;  // split-K accumulators known to be all zero
 
   // pinned staging ring for per-step metadata
   int32_t* staging[kRing] = {};
@@ -112,6 +113,8 @@ stage_status check_config(const stage_model_config* c) {
     return fail(STAGE_ERR_UNSUPPORTED, "head_dim must be 64 or 128 (got %d)", c->head_dim);
   if (c->n_q_heads % c->n_kv_heads != 0 || !is_pow2_le16(c->n_q_heads / c->n_kv_heads))
     return fail(STAGE_ERR_UNSUPPORTED, "n_q_heads/n_kv_heads must be 1, 2, 4, 8 or 16");
+  if (c->hidden > 16384)
+    return fail(STAGE_ERR_UNSUPPORTED, "hidden %d > 16384", c->hidden);
   if (c->hidden % 128 != 0 || (c->n_q_heads * c->head_dim) % 128 != 0 || c->ffn % 64 != 0)
     return fail(STAGE_ERR_UNSUPPORTED,
                 "need hidden %% 128 == 0, n_q*head_dim %% 128 == 0, ffn %% 64 == 0");
@@ -174,6 +177,9 @@ void plan_workspace(stage* st) {
   const size_t T = st->max_tokens, H = c.hidden, D = c.head_dim;
   const size_t qw = (size_t)c.n_q_heads * D, qkvw = (size_t)(c.n_q_heads + 2 * c.n_kv_heads) * D;
   const size_t F = c.ffn, es = st->esize;
+  // GEMM inputs (packed activations) are read in whole 128-row tiles
+  const size_t Tp = (T + 127) / 128 * 128;
+  const size_t R = st->skinny_rows;
   size_t off = 0;
   auto take = [&](Region& r, size_t bytes) {
     r.off = off;
@@ -181,13 +187,14 @@ void plan_workspace(stage* st) {
     off = align_up(off + bytes, 256);
   };
   take(st->r_x, T * H * 4);
-  take(st->r_h, T * H * es);
-  take(st->r_qkv, T * qkvw * 4);
+  take(st->r_h, Tp * H * es);
+  take(st->r_qkv, std::max(T, (size_t)st->s_qkv * R) * qkvw * 4);
   take(st->r_q, T * qw * es);
-  take(st->r_attn, T * qw * es);
-  take(st->r_m, T * F * es);
-  const size_t gu_rows = c.dtype == STAGE_F32 ? T : (size_t)st->skinny_rows;
+  take(st->r_attn, Tp * qw * es);
+  take(st->r_m, Tp * F * es);
+  const size_t gu_rows = c.dtype == STAGE_F32 ? T : (st->s_gu > 1 ? (size_t)st->s_gu * R : 0);
   take(st->r_gu, gu_rows * 2 * F * 4);
+  take(st->r_part_x, (size_t)std::max(st->s_o, st->s_down) * R * H * 4);
   const size_t max_items = c.dtype == STAGE_BF16 ? (size_t)st->max_seqs * kMaxSplits : 0;
   take(st->r_part_o, max_items * qw * 4);
   take(st->r_part_ml, max_items * c.n_q_heads * 2 * 4);
@@ -265,17 +272,6 @@ void build_meta(const stage* st, const stage_batch* pf, const stage_batch* dc, S
     }
   }
   m.item_start[nd] = m.n_ditems;
-}
-
-// Split so that the skinny GEMM launches about `waves` waves.
-int skinny_split(int N, int K, int M, int waves) {
-  const int nt = ((M + 15) / 16) <= 4 ? 4 : 2;
-  const int n_waves = std::max(1, N / (nt * 16));
-  int splits = std::max(1, (waves + n_waves - 1) / n_waves);
-  splits = std::min(splits, K / 64);
-  int ks = (K + splits - 1) / splits;
-  ks = (ks + 63) / 64 * 64;
-  return ks;
 }
 
 hipEvent_t take_event(stage* st) {
@@ -362,33 +358,31 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
   void* attn = st->ws + st->r_attn.off;
   void* m = st->ws + st->r_m.off;
   float* gu = st->at<float>(st->r_gu);
+  float* part_x = st->at<float>(st->r_part_x);
   const float* cos_t = st->at<float>(st->r_cos);
   const float* sin_t = st->at<float>(st->r_sin);
 
+  // Split-K steps leave the O / down projections as partial sums in part_x;
+  // the next RMSNorm (or the output cast) adds them to the residual stream.
+  Partials pending{nullptr, 0};
   Launcher L{st, s};
-  if (skinny && !st->acc_zero) {
-    L(STAGE_OP_NORM, [&] { return fill_zero_f32(qkv, (size_t)st->skinny_rows * qkvw, s); });
-    L(STAGE_OP_NORM, [&] { return fill_zero_f32(gu, (size_t)st->skinny_rows * 2 * F, s); });
-  }
-  if (!skinny) st->acc_zero = false;
-
   for (int li = 0; li < st->n_layers; ++li) {
     const stage_layer_weights& w = st->layers[li];
     KVLayer kvl{st->kv_pool + (size_t)li * st->kv_layer_bytes, nkv, D};
     if (li == 0)
       L(STAGE_OP_NORM, [&] { return embed_norm(dt, hin, x, h, w.attn_norm, T, H, c.rms_eps, s); });
     else
-      L(STAGE_OP_NORM, [&] { return rmsnorm(dt, x, h, w.attn_norm, T, H, c.rms_eps, s); });
+      L(STAGE_OP_NORM, [&] { return rmsnorm(dt, x, pending, h, w.attn_norm, T, H, c.rms_eps, s); });
 
-    if (skinny)
-      L(STAGE_OP_QKV, [&] {
-        return gemm_skinny(dt, h, w.w_qkv, T, qkvw, H, qkv, skinny_split(qkvw, H, T, st->skinny_waves), s);
-      });
-    else
+    int qkv_splits = 1;
+    if (skinny) {
+      qkv_splits = st->s_qkv;
+      L(STAGE_OP_QKV, [&] { return gemm_skinny(h, w.w_qkv, T, qkvw, H, st->s_qkv, false, qkv, s); });
+    } else {
       L(STAGE_OP_QKV, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_qkv, T, qkvw, H, qkv, s); });
-
+    }
     L(STAGE_OP_ROPE_KV, [&] {
-      return rope_kv_write(dt, qkv, skinny ? 1 : 0, q, kvl, dm.tok_seq, dm.tok_pos, tabs, cos_t,
+      return rope_kv_write(dt, qkv, qkv_splits, q, kvl, dm.tok_seq, dm.tok_pos, tabs, cos_t,
                            sin_t, c.qk_norm ? w.q_norm : nullptr, c.qk_norm ? w.k_norm : nullptr,
                            c.qk_rms_eps, T, nq, s);
     });
@@ -415,42 +409,41 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
       }
     }
 
-    if (skinny)
-      L(STAGE_OP_O, [&] {
-        return gemm_skinny(dt, attn, w.w_o, T, H, qw, x, skinny_split(H, qw, T, st->skinny_waves), s);
-      });
-    else
-      L(STAGE_OP_O, [&] { return gemm(dt, EPI_RESID_ADD, attn, w.w_o, T, H, qw, x, s); });
-
-    L(STAGE_OP_NORM, [&] { return rmsnorm(dt, x, h, w.ffn_norm, T, H, c.rms_eps, s); });
-
     if (skinny) {
-      L(STAGE_OP_GATE_UP, [&] {
-        return gemm_skinny(dt, h, w.w_gate_up, T, 2 * F, H, gu,
-                           skinny_split(2 * F, H, T, st->skinny_waves), s);
-      });
-      L(STAGE_OP_NORM, [&] { return swiglu(dt, gu, m, T, F, 1, s); });
-    } else if (dt == DT_BF16) {
-      L(STAGE_OP_GATE_UP, [&] { return gemm(dt, EPI_SWIGLU, h, w.w_gate_up, T, 2 * F, H, m, s); });
+      L(STAGE_OP_O, [&] { return gemm_skinny(attn, w.w_o, T, H, qw, st->s_o, false, part_x, s); });
+      pending = Partials{part_x, st->s_o};
     } else {
-      L(STAGE_OP_GATE_UP, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_gate_up, T, 2 * F, H, gu, s); });
-      L(STAGE_OP_NORM, [&] { return swiglu(dt, gu, m, T, F, 0, s); });
+      L(STAGE_OP_O, [&] { return gemm(dt, EPI_RESID_ADD, attn, w.w_o, T, H, qw, x, s); });
     }
 
-    if (skinny)
-      L(STAGE_OP_DOWN, [&] {
-        return gemm_skinny(dt, m, w.w_down, T, H, F, x, skinny_split(H, F, T, st->skinny_waves), s);
-      });
-    else
-      L(STAGE_OP_DOWN, [&] { return gemm(dt, EPI_RESID_ADD, m, w.w_down, T, H, F, x, s); });
-  }
-  L(STAGE_OP_NORM, [&] { return output_cast(dt, x, hout, (size_t)T * H, s); });
+    L(STAGE_OP_NORM, [&] { return rmsnorm(dt, x, pending, h, w.ffn_norm, T, H, c.rms_eps, s); });
+    pending = Partials{nullptr, 0};
 
-  if (L.err != hipSuccess) {
-    st->acc_zero = false;
-    return hip_fail("kernel launch", L.err);
+    if (skinny) {
+      if (st->s_gu == 1) {
+        L(STAGE_OP_GATE_UP, [&] { return gemm_skinny(h, w.w_gate_up, T, 2 * F, H, 1, true, m, s); });
+      } else {
+        L(STAGE_OP_GATE_UP, [&] {
+          return gemm_skinny(h, w.w_gate_up, T, 2 * F, H, st->s_gu, false, gu, s);
+        });
+        L(STAGE_OP_NORM, [&] {
+          return swiglu_reduce_bf16(Partials{gu, st->s_gu}, (uint16_t*)m, T, F, s);
+        });
+      }
+      L(STAGE_OP_DOWN, [&] { return gemm_skinny(m, w.w_down, T, H, F, st->s_down, false, part_x, s); });
+      pending = Partials{part_x, st->s_down};
+    } else if (dt == DT_BF16) {
+      L(STAGE_OP_GATE_UP, [&] { return gemm(dt, EPI_SWIGLU, h, w.w_gate_up, T, 2 * F, H, m, s); });
+      L(STAGE_OP_DOWN, [&] { return gemm(dt, EPI_RESID_ADD, m, w.w_down, T, H, F, x, s); });
+    } else {
+      L(STAGE_OP_GATE_UP, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_gate_up, T, 2 * F, H, gu, s); });
+      L(STAGE_OP_NORM, [&] { return swiglu_f32(gu, (float*)m, T, F, s); });
+      L(STAGE_OP_DOWN, [&] { return gemm(dt, EPI_RESID_ADD, m, w.w_down, T, H, F, x, s); });
+    }
   }
-  if (skinny) st->acc_zero = true;
+  L(STAGE_OP_NORM, [&] { return output_cast(dt, x, pending, hout, T, H, s); });
+
+  if (L.err != hipSuccess) return hip_fail("kernel launch", L.err);
   return STAGE_OK;
 }
 
@@ -499,7 +492,16 @@ stage_status stage_create(const stage_model_config* cfg, int32_t layer_begin, in
   st->esize = cfg->dtype == STAGE_BF16 ? 2 : 4;
   st->kv_layer_bytes = (size_t)num_blocks * cfg->n_kv_heads * 2 * kBlock * cfg->head_dim * st->esize;
   st->skinny_rows = cfg->dtype == STAGE_BF16 ? std::min(kSkinnyMaxRows, max_tokens) : 0;
-  st->skinny_waves = std::max(64, env_int("STAGE_SKINNY_WAVES", 2048));
+  {
+    // about one wave per SIMD (256 CUs x 4) for each split-K GEMM
+    const int waves = std::max(64, env_int("STAGE_SKINNY_WAVES", 1024));
+    const int H = cfg->hidden, F = cfg->ffn, qw = cfg->n_q_heads * cfg->head_dim;
+    const int qkvw = (cfg->n_q_heads + 2 * cfg->n_kv_heads) * cfg->head_dim;
+    st->s_qkv = skinny_splits(qkvw, H, waves);
+    st->s_o = skinny_splits(H, qw, waves);
+    st->s_gu = skinny_splits(2 * F, H, waves);
+    st->s_down = skinny_splits(H, F, waves);
+  }
   if ((e = hipGetDevice(&st->device)) != hipSuccess) {
     delete st;
     return hip_fail("hipGetDevice", e);
@@ -544,13 +546,10 @@ stage_status stage_bind_workspace(stage_t* st, void* dev, size_t bytes) {
   if ((e = hipMemcpy(st->ws + st->r_cos.off, cs.data(), cs.size() * 4, hipMemcpyHostToDevice)) !=
           hipSuccess ||
       (e = hipMemcpy(st->ws + st->r_sin.off, sn.data(), sn.size() * 4, hipMemcpyHostToDevice)) !=
-          hipSuccess ||
-      (e = hipMemset(st->ws + st->r_qkv.off, 0, st->r_qkv.bytes)) != hipSuccess ||
-      (e = hipMemset(st->ws + st->r_gu.off, 0, st->r_gu.bytes)) != hipSuccess) {
+          hipSuccess) {
     st->ws = nullptr;
     return hip_fail("workspace init", e);
   }
-  st->acc_zero = true;
   return STAGE_OK;
 }
 
@@ -602,6 +601,32 @@ stage_status stage_validate_step(const stage_model_config* cfg, int32_t max_toke
   if (s != STAGE_OK) return s;
   long long T = 0;
   return check_step(*cfg, max_tokens, max_seqs, prefill, decode, &T);
+}
+
+stage_status stage_pack_weight(const stage_model_config* cfg, stage_weight_kind kind,
+                               const void* src, void* dst, void* stream) {
+  stage_status v = check_config(cfg);
+  if (v != STAGE_OK) return v;
+  if (!src || !dst) return fail(STAGE_ERR_INVALID_ARG, "src/dst is NULL");
+  if (src == dst) return fail(STAGE_ERR_INVALID_ARG, "packing cannot run in place");
+  const int H = cfg->hidden, F = cfg->ffn, qw = cfg->n_q_heads * cfg->head_dim;
+  const int qkvw = (cfg->n_q_heads + 2 * cfg->n_kv_heads) * cfg->head_dim;
+  int N = 0, K = 0, ffn = 0;
+  switch (kind) {
+    case STAGE_W_QKV: N = qkvw; K = H; break;
+    case STAGE_W_O: N = H; K = qw; break;
+    case STAGE_W_GATE_UP: N = 2 * F; K = H; ffn = F; break;
+    case STAGE_W_DOWN: N = H; K = F; break;
+    default: return fail(STAGE_ERR_INVALID_ARG, "unknown weight kind %d", (int)kind);
+  }
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e;
+  if (cfg->dtype == STAGE_F32)
+    e = hipMemcpyAsync(dst, src, (size_t)N * K * 4, hipMemcpyDeviceToDevice, s);
+  else
+    e = pack_weight(src, dst, N, K, ffn, s);
+  if (e != hipSuccess) return hip_fail("pack_weight", e);
+  return STAGE_OK;
 }
 
 stage_status stage_set_op_timing(stage_t* st, int32_t enable) {

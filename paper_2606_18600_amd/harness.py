@@ -66,15 +66,42 @@ def to_host64(weights: Dict[str, torch.Tensor]) -> Dict[str, np.ndarray]:
     return {k: v.detach().to(torch.float64).cpu().numpy() for k, v in weights.items()}
 
 
+PACK_KINDS = {"w_qkv": S.STAGE_W_QKV, "w_o": S.STAGE_W_O, "w_gate_up": S.STAGE_W_GATE_UP,
+              "w_down": S.STAGE_W_DOWN}
+
+
+def pack_layer(cfg: S.stage_model_config, w: Dict[str, torch.Tensor],
+               free_source: bool = False) -> Dict[str, torch.Tensor]:
+    """Row-major layer weights -> the layout the stage reads (stage_pack_weight)."""
+    out = {}
+    for k, v in list(w.items()):
+        if k in PACK_KINDS:
+            dst = torch.empty_like(v)
+            S.stage_pack_weight(cfg, PACK_KINDS[k], v.data_ptr(), dst.data_ptr(),
+                                torch.cuda.current_stream().cuda_stream)
+            out[k] = dst
+            if free_source:
+                torch.cuda.current_stream().synchronize()
+                del w[k]
+        else:
+            out[k] = v
+    return out
+
+
 class DeviceStage:
+    """A stage over row-major weights (packed here through the ABI) or over
+    weights already packed (``packed=True``)."""
+
     def __init__(self, shape: ModelShape, dtype: str, layer_begin: int,
                  weights: Sequence[Dict[str, torch.Tensor]], num_blocks: int, max_tokens: int,
                  max_seqs: int, max_position: int = 8192, device="cuda",
-                 kv_pool: Optional[torch.Tensor] = None):
+                 kv_pool: Optional[torch.Tensor] = None, packed: bool = False):
         self.shape, self.dtype = shape, dtype
         self.n_layers = len(weights)
         self.num_blocks = num_blocks
         self.cfg = model_config(shape, dtype, max_position)
+        if not packed:
+            weights = [pack_layer(self.cfg, w) for w in weights]
         td = torch_dtype(dtype)
         numel = self.n_layers * num_blocks * shape.n_kv_heads * 2 * shape.block_size * shape.head_dim
         if kv_pool is None:

@@ -34,7 +34,13 @@ STAGE_OP_COUNT = len(OP_NAMES)
 
 EXPORTED = ("stage_create", "stage_workspace_bytes", "stage_bind_workspace", "stage_prefill",
             "stage_decode", "stage_step_mixed", "stage_destroy", "stage_last_error",
-            "stage_validate_step", "stage_set_op_timing", "stage_read_op_times")
+            "stage_validate_step", "stage_set_op_timing", "stage_read_op_times",
+            "stage_pack_weight")
+
+STAGE_W_QKV = 0
+STAGE_W_O = 1
+STAGE_W_GATE_UP = 2
+STAGE_W_DOWN = 3
 
 
 class StageError(RuntimeError):
@@ -93,12 +99,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.stage_last_error.restype = ctypes.c_char_p
     lib.stage_validate_step.argtypes = [ctypes.POINTER(stage_model_config), i32, i32,
                                         ctypes.POINTER(stage_batch), ctypes.POINTER(stage_batch)]
+    lib.stage_pack_weight.argtypes = [ctypes.POINTER(stage_model_config), i32, P, P, P]
     lib.stage_set_op_timing.argtypes = [P, i32]
     lib.stage_read_op_times.argtypes = [P, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_int64)]
     for name in ("stage_create", "stage_bind_workspace", "stage_prefill", "stage_decode",
                  "stage_step_mixed", "stage_destroy", "stage_validate_step",
-                 "stage_set_op_timing", "stage_read_op_times"):
+                 "stage_set_op_timing", "stage_read_op_times", "stage_pack_weight"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -174,6 +181,11 @@ def stage_validate_step(cfg: stage_model_config, max_tokens: int, max_seqs: int,
     """Returns the status code (does not raise)."""
     return int(load_library().stage_validate_step(ctypes.byref(cfg), max_tokens, max_seqs,
                                                   _bp(prefill), _bp(decode)))
+
+
+def stage_pack_weight(cfg: stage_model_config, kind: int, src: int, dst: int,
+                      stream: int = 0) -> None:
+    _check(load_library().stage_pack_weight(ctypes.byref(cfg), kind, src, dst, stream))
 
 
 def stage_set_op_timing(st: int, enable: bool) -> None:

@@ -255,3 +255,35 @@ def test_forward_calls_return_validation_codes():
         assert e.value.code == S.STAGE_ERR_CAPACITY
     finally:
         pair.close()
+
+
+@pytest.mark.parametrize("kind,shape_fn", [
+    ("w_qkv", lambda s: (s.qkv_width, s.hidden)), ("w_o", lambda s: (s.hidden, s.q_width)),
+    ("w_gate_up", lambda s: (2 * s.ffn, s.hidden)), ("w_down", lambda s: (s.hidden, s.ffn))])
+def test_pack_weight_layout(kind, shape_fn):
+    """stage_pack_weight places element (n, k) of the row-major matrix where
+    the documented layout says: fragment ((n/64)*(K/32) + k/32)*4 + (n/16)%4,
+    lane (n%16) + 16*((k%32)/8), element k%8 (gate-up rows interleaved per 64)."""
+    from paper_2606_18600_amd.harness import PACK_KINDS, model_config
+    shape = QWEN_SMALL
+    N, K = shape_fn(shape)
+    cfg = model_config(shape, "bf16")
+    src = torch.arange(N * K, dtype=torch.float32).remainder_(251).sub_(125).to(
+        torch.bfloat16).reshape(N, K).cuda()
+    dst = torch.empty_like(src)
+    S.stage_pack_weight(cfg, PACK_KINDS[kind], src.data_ptr(), dst.data_ptr(), 0)
+    torch.cuda.synchronize()
+    a, p = src.cpu().float().numpy(), dst.cpu().float().numpy().reshape(-1)
+    n = np.arange(N)[:, None]
+    k = np.arange(K)[None, :]
+    frag = ((n // 64) * (K // 32) + k // 32) * 4 + (n // 16) % 4
+    lane = n % 16 + 16 * ((k % 32) // 8)
+    pos = frag * 512 + lane * 8 + k % 8
+    if kind == "w_gate_up":
+        F = shape.ffn
+        g, r = n // 64, n % 64
+        rows = np.where(r < 32, 32 * g + r, F + 32 * g + r - 32)
+        expect = a[rows[:, 0]]
+    else:
+        expect = a
+    np.testing.assert_array_equal(p[pos], np.broadcast_to(expect, (N, K)))
