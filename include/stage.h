@@ -31,11 +31,14 @@
  *    gains are [hidden]; q/k-norm gains are [head_dim]. All weights are stored
  *    in the mode dtype.
  *  - KV pool (one allocation for the stage's layers):
- *      [n_layers][num_blocks][n_kv][2][block_size][head_dim]
- *    in the mode dtype. Plane 0 holds K as [token][d]; plane 1 holds V
- *    transposed, [d][token]. Token p of a sequence with block table bt lives
- *    in block bt[p / block_size] at offset p % block_size. Block ids index
- *    the same blocks in every layer of the stage.
+ *      [n_layers][num_blocks][n_kv][2][block_size * head_dim]
+ *    in the mode dtype. Token p of a sequence with block table bt lives in
+ *    block bt[p / block_size] at offset o = p % block_size. Plane 0 holds K,
+ *    plane 1 holds V, both as whole MFMA operand fragments so that every
+ *    load of the attention kernels is contiguous:
+ *      K[o][d] at (d / 32) * 512 + (o + 16 * ((d % 32) / 8)) * 8 + d % 8
+ *      V[o][d] at (d / 16) * 256 + (d % 16 + 16 * (o / 4)) * 4 + o % 4
+ *    Block ids index the same blocks in every layer of the stage.
  *  - hidden_in / hidden_out: [T, hidden] in the mode dtype, rows packed
  *    sequence by sequence in batch order (for stage_step_mixed: all prefill
  *    rows first, then the decode rows). hidden_out may alias hidden_in.

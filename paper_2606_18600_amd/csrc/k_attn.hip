@@ -1,8 +1,8 @@
 // Causal grouped-query attention over the paged KV cache.
 //
-// Cache geometry per layer: [num_blocks][n_kv][2][16][d]; plane 0 holds K as
-// [token][d], plane 1 holds V transposed as [d][token]. With that layout every
-// MFMA operand is a contiguous load:
+// Cache geometry per layer: [num_blocks][n_kv][2][16 * d]; plane 0 holds K,
+// plane 1 holds V, each as whole MFMA operand fragments (kv_k_offset and
+// kv_v_offset in packed.hpp), so every operand load is contiguous:
 //   S^T[key][row] = K[key][:] . Q[row][:]        v_mfma_f32_16x16x32_bf16
 //   O^T[d][row]  += V^T[d][key] . P^T[key][row]  v_mfma_f32_16x16x16_bf16
 // The C layout of the first product (lane l: row l%16, keys (l/16)*4 + r) is
@@ -35,29 +35,29 @@ __device__ __forceinline__ const int32_t* seq_table(const SegTables& t, int seq)
                        : t.bt1 + (size_t)(seq - t.nseq0) * t.stride1;
 }
 
-// K fragment of one 16-token block: lane l holds token l%16, d offsets
-// (l/16)*(D/4) .. +D/4 (NJ chunks of 8).
+// K fragments of one 16-token block (kv_k_offset layout): fragment j, lane l
+// = token l%16, d = j*32 + (l/16)*8 .. +7; each load reads 1 KB contiguously.
 template <int D>
 struct KFrag {
   static constexpr int NJ = D / 32;
   u32x4_t v[NJ];
   __device__ __forceinline__ void load(const bf16_t* kplane, int lane) {
-    const bf16_t* p = kplane + (lane & 15) * D + (lane >> 4) * (D / 4);
+    const bf16_t* p = kplane + lane * 8;
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) v[j] = ldg128(p + j * 8);
+    for (int j = 0; j < NJ; ++j) v[j] = ldg128(p + j * 512);
   }
 };
 
-// V^T fragments of one block: for d tile dt, lane l holds d = dt*16 + l%16,
-// tokens (l/16)*4 .. +3.
+// V^T fragments of one block (kv_v_offset layout): for d tile dt, lane l
+// holds d = dt*16 + l%16, tokens (l/16)*4 .. +3; each load reads 512 B.
 template <int D>
 struct VFrag {
   static constexpr int NT = D / 16;
   u32x2_t v[NT];
   __device__ __forceinline__ void load(const bf16_t* vplane, int lane) {
-    const bf16_t* p = vplane + (lane & 15) * kBlock + (lane >> 4) * 4;
+    const bf16_t* p = vplane + lane * 4;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) v[t] = ldg64(p + t * 16 * kBlock);
+    for (int t = 0; t < NT; ++t) v[t] = ldg64(p + t * 256);
   }
 };
 
@@ -117,9 +117,9 @@ __global__ __launch_bounds__(256) void attn_decode_bf16(const bf16_t* __restrict
   u32x4_t qf[NJ];
   {
     const bf16_t* qp = q + ((size_t)it.tok * n_q + kvh * G + (row_ok ? row : 0)) * D +
-                       (lane >> 4) * (D / 4);
+                       (lane >> 4) * 8;
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) qf[j] = row_ok ? ldg128(qp + j * 8) : u32x4_t{0u, 0u, 0u, 0u};
+    for (int j = 0; j < NJ; ++j) qf[j] = row_ok ? ldg128(qp + j * 32) : u32x4_t{0u, 0u, 0u, 0u};
   }
 
   const int32_t* bt = seq_table(tabs, it.seq);
@@ -131,21 +131,18 @@ __global__ __launch_bounds__(256) void attn_decode_bf16(const bf16_t* __restrict
   for (int t = 0; t < D / 16; ++t) oacc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   const int b0 = it.k0 / kBlock, b1 = (it.k1 + kBlock - 1) / kBlock;
-  KFrag<D> kf;
-  VFrag<D> vf;
-  {
-    const bf16_t* kp = kv + ((size_t)bt[b0] * n_kv + kvh) * head_stride;
+  // Two register sets in ping-pong (no copies between them), so a block's
+  // loads stay in flight while the previous block is processed; the
+  // prefetch index is clamped to the last block and its data is unused.
+  KFrag<D> kx, ky;
+  VFrag<D> vx, vy;
+  auto load = [&](KFrag<D>& kf, VFrag<D>& vf, int b) {
+    b = b < b1 ? b : b1 - 1;
+    const bf16_t* kp = kv + ((size_t)bt[b] * n_kv + kvh) * head_stride;
     kf.load(kp, lane);
     vf.load(kp + plane, lane);
-  }
-  for (int b = b0; b < b1; ++b) {
-    KFrag<D> kn;
-    VFrag<D> vn;
-    if (b + 1 < b1) {
-      const bf16_t* kp = kv + ((size_t)bt[b + 1] * n_kv + kvh) * head_stride;
-      kn.load(kp, lane);
-      vn.load(kp + plane, lane);
-    }
+  };
+  auto step = [&](const KFrag<D>& kf, const VFrag<D>& vf, int b) {
     f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int j = 0; j < NJ; ++j) s = mfma16x16x32(kf.v[j], qf[j], s);
@@ -155,11 +152,20 @@ __global__ __launch_bounds__(256) void attn_decode_bf16(const bf16_t* __restrict
       s[r] = key < it.k1 ? s[r] * scale : -INFINITY;
     }
     softmax_pv<D>(s, st, oacc, vf);
-    if (b + 1 < b1) {
-      kf = kn;
-      vf = vn;
-    }
+  };
+  load(kx, vx, b0);
+  int b = b0;
+  for (; b + 1 < b1; b += 2) {
+    load(ky, vy, b + 1);
+    __builtin_amdgcn_sched_barrier(0);
+    step(kx, vx, b);
+    __builtin_amdgcn_sched_barrier(0);
+    load(kx, vx, b + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    step(ky, vy, b + 1);
+    __builtin_amdgcn_sched_barrier(0);
   }
+  if (b < b1) step(kx, vx, b);
 
   if (!row_ok) return;
   const size_t ob = ((size_t)blockIdx.x * n_q + kvh * G + row);
@@ -173,38 +179,55 @@ __global__ __launch_bounds__(256) void attn_decode_bf16(const bf16_t* __restrict
   }
 }
 
-// Combine the key splits of each decode token: one wave per (token, head).
-template <typename OutT>
+// Combine the key splits of each decode token: one wave per (token, kv
+// head). Lane l serves query head row r = l / LPR of the group and DPL
+// consecutive d values (a multiple of 4); the split loop is unrolled so the
+// loads of several splits are in flight together.
+template <int D, int G>
 __global__ __launch_bounds__(256) void attn_merge_kernel(const float* __restrict__ part_o,
                                                          const float* __restrict__ part_ml,
                                                          const int32_t* __restrict__ item_start,
                                                          const int32_t* __restrict__ tok_rows,
-                                                         int n_q, int D, OutT* __restrict__ out) {
+                                                         int n_q, int n_kv,
+                                                         bf16_t* __restrict__ out) {
+  constexpr int LPR = (64 / G) < (D / 4) ? (64 / G) : (D / 4);  // lanes per head row
+  constexpr int DPL = D / LPR;                                    // d values per lane
   const int t = blockIdx.x;
-  const int h = blockIdx.y * 4 + (threadIdx.x >> 6);
-  if (h >= n_q) return;
+  const int kvh = blockIdx.y * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
+  if (kvh >= n_kv || lane >= G * LPR) return;
+  const int h = kvh * G + lane / LPR;
+  const int d0 = (lane % LPR) * DPL;
   const int i0 = item_start[t], i1 = item_start[t + 1];
   float M = -INFINITY;
   for (int i = i0; i < i1; ++i) M = fmaxf(M, part_ml[((size_t)i * n_q + h) * 2]);
-  float L = 0.f, o0 = 0.f, o1 = 0.f;
+  float L = 0.f;
+  float4 o[DPL / 4];
+#pragma unroll
+  for (int c = 0; c < DPL / 4; ++c) o[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 4
   for (int i = i0; i < i1; ++i) {
     const size_t b = (size_t)i * n_q + h;
     const float w = exp2f(part_ml[b * 2] - M);
     L += w * part_ml[b * 2 + 1];
-    o0 += w * part_o[b * D + lane];
-    if (D > 64) o1 += w * part_o[b * D + lane + 64];
+    const float4* po = (const float4*)(part_o + b * D + d0);
+#pragma unroll
+    for (int c = 0; c < DPL / 4; ++c) {
+      const float4 v = po[c];
+      o[c].x += w * v.x;
+      o[c].y += w * v.y;
+      o[c].z += w * v.z;
+      o[c].w += w * v.w;
+    }
   }
   const float inv = 1.0f / L;
-  // bf16: packed activation layout (the O projection's input); fp32: row-major
   const int row = tok_rows[t], K = n_q * D;
-  if constexpr (sizeof(OutT) == 2) {
-    elem<OutT>::store(out, packed_a_offset(row, h * D + lane, K), o0 * inv);
-    if (D > 64) elem<OutT>::store(out, packed_a_offset(row, h * D + lane + 64, K), o1 * inv);
-  } else {
-    OutT* op = out + (size_t)row * K + h * D;
-    elem<OutT>::store(op, lane, o0 * inv);
-    if (D > 64) elem<OutT>::store(op, lane + 64, o1 * inv);
+#pragma unroll
+  for (int c = 0; c < DPL / 4; ++c) {
+    u32x2_t wv;
+    wv[0] = pack_bf16x2(o[c].x * inv, o[c].y * inv);
+    wv[1] = pack_bf16x2(o[c].z * inv, o[c].w * inv);
+    *(u32x2_t*)(out + packed_a_offset(row, h * D + d0 + 4 * c, K)) = wv;
   }
 }
 
@@ -235,9 +258,9 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(const bf16_t* __restric
     const int pc = rok[i] ? pi : it.npos - 1;
     rpos[i] = it.p0 + pc;
     const bf16_t* qp = q + ((size_t)(it.t0 + pc) * n_q + kvh * G + r % G) * D +
-                       (lane >> 4) * (D / 4);
+                       (lane >> 4) * 8;
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) qf[i][j] = ldg128(qp + j * 8);
+    for (int j = 0; j < NJ; ++j) qf[i][j] = ldg128(qp + j * 32);
   }
 
   const int32_t* bt = seq_table(tabs, it.seq);
@@ -254,21 +277,15 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(const bf16_t* __restric
 
   const int kend = it.p0 + it.npos;  // keys [0, kend)
   const int nb = (kend + kBlock - 1) / kBlock;
-  KFrag<D> kf;
-  VFrag<D> vf;
-  {
-    const bf16_t* kp = kv + ((size_t)bt[0] * n_kv + kvh) * head_stride;
+  KFrag<D> kx, ky;
+  VFrag<D> vx, vy;
+  auto load = [&](KFrag<D>& kf, VFrag<D>& vf, int b) {
+    b = b < nb ? b : nb - 1;
+    const bf16_t* kp = kv + ((size_t)bt[b] * n_kv + kvh) * head_stride;
     kf.load(kp, lane);
     vf.load(kp + plane, lane);
-  }
-  for (int b = 0; b < nb; ++b) {
-    KFrag<D> kn;
-    VFrag<D> vn;
-    if (b + 1 < nb) {
-      const bf16_t* kp = kv + ((size_t)bt[b + 1] * n_kv + kvh) * head_stride;
-      kn.load(kp, lane);
-      vn.load(kp + plane, lane);
-    }
+  };
+  auto step = [&](const KFrag<D>& kf, const VFrag<D>& vf, int b) {
 #pragma unroll
     for (int i = 0; i < RT; ++i) {
       f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -281,11 +298,20 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(const bf16_t* __restric
       }
       softmax_pv<D>(s, st[i], oacc[i], vf);
     }
-    if (b + 1 < nb) {
-      kf = kn;
-      vf = vn;
-    }
+  };
+  load(kx, vx, 0);
+  int b = 0;
+  for (; b + 1 < nb; b += 2) {
+    load(ky, vy, b + 1);
+    __builtin_amdgcn_sched_barrier(0);
+    step(kx, vx, b);
+    __builtin_amdgcn_sched_barrier(0);
+    load(kx, vx, b + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    step(ky, vy, b + 1);
+    __builtin_amdgcn_sched_barrier(0);
   }
+  if (b < nb) step(kx, vx, b);
 
 #pragma unroll
   for (int i = 0; i < RT; ++i) {
@@ -329,10 +355,9 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__
     const int key = c0 + lane;
     float s = -INFINITY;
     if (key <= pos) {
-      const float* kp = kv + ((size_t)bt[key / kBlock] * n_kv + kvh) * 2 * plane +
-                        (key % kBlock) * D;
+      const float* kp = kv + ((size_t)bt[key / kBlock] * n_kv + kvh) * 2 * plane;
       float acc = 0.f;
-      for (int e = 0; e < D; ++e) acc = fmaf(qp[e], kp[e], acc);
+      for (int e = 0; e < D; ++e) acc = fmaf(qp[e], kp[kv_k_offset(key % kBlock, e)], acc);
       s = acc * scale;
     }
     const float cm = wave_max(s);
@@ -346,10 +371,9 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__
     for (int j = 0; j < nk; ++j) {
       const float pj = __shfl(p, j, 64);
       const int kj = c0 + j;
-      const float* vp = kv + ((size_t)bt[kj / kBlock] * n_kv + kvh) * 2 * plane + plane +
-                        (kj % kBlock);
-      o0 = fmaf(pj, vp[(size_t)lane * kBlock], o0);
-      if (D > 64) o1 = fmaf(pj, vp[(size_t)(lane + 64) * kBlock], o1);
+      const float* vp = kv + ((size_t)bt[kj / kBlock] * n_kv + kvh) * 2 * plane + plane;
+      o0 = fmaf(pj, vp[kv_v_offset(kj % kBlock, lane)], o0);
+      if (D > 64) o1 = fmaf(pj, vp[kv_v_offset(kj % kBlock, lane + 64)], o1);
     }
     m = mn;
   }
@@ -384,18 +408,34 @@ hipError_t attn_decode(DType dt, const void* q, KVLayer kv, SegTables tabs,
   return hipGetLastError();
 }
 
+template <int D>
+static hipError_t launch_merge(const float* part_o, const float* part_ml, const int32_t* starts,
+                               const int32_t* rows, int n_tok, int n_q, int n_kv, bf16_t* out,
+                               hipStream_t s) {
+  dim3 grid(n_tok, (n_kv + 3) / 4);
+  switch (n_q / n_kv) {
+    case 1: attn_merge_kernel<D, 1><<<grid, 256, 0, s>>>(part_o, part_ml, starts, rows, n_q, n_kv, out); break;
+    case 2: attn_merge_kernel<D, 2><<<grid, 256, 0, s>>>(part_o, part_ml, starts, rows, n_q, n_kv, out); break;
+    case 4: attn_merge_kernel<D, 4><<<grid, 256, 0, s>>>(part_o, part_ml, starts, rows, n_q, n_kv, out); break;
+    case 8: attn_merge_kernel<D, 8><<<grid, 256, 0, s>>>(part_o, part_ml, starts, rows, n_q, n_kv, out); break;
+    case 16: attn_merge_kernel<D, 16><<<grid, 256, 0, s>>>(part_o, part_ml, starts, rows, n_q, n_kv, out); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 hipError_t attn_merge(DType dt, const float* part_o, const float* part_ml,
                       const int32_t* tok_item_start, const int32_t* tok_rows, int n_tok, int n_q,
-                      int head_dim, void* out, hipStream_t s) {
+                      int n_kv, int head_dim, void* out, hipStream_t s) {
   if (n_tok == 0) return hipSuccess;
-  dim3 grid(n_tok, (n_q + 3) / 4);
-  if (dt == DT_BF16)
-    attn_merge_kernel<bf16_t><<<grid, 256, 0, s>>>(part_o, part_ml, tok_item_start, tok_rows, n_q,
-                                                   head_dim, (bf16_t*)out);
-  else
-    attn_merge_kernel<float><<<grid, 256, 0, s>>>(part_o, part_ml, tok_item_start, tok_rows, n_q,
-                                                  head_dim, (float*)out);
-  return hipGetLastError();
+  if (dt != DT_BF16) return hipErrorInvalidValue;
+  if (head_dim == 128)
+    return launch_merge<128>(part_o, part_ml, tok_item_start, tok_rows, n_tok, n_q, n_kv,
+                             (bf16_t*)out, s);
+  if (head_dim == 64)
+    return launch_merge<64>(part_o, part_ml, tok_item_start, tok_rows, n_tok, n_q, n_kv,
+                            (bf16_t*)out, s);
+  return hipErrorInvalidValue;
 }
 
 hipError_t attn_prefill(DType dt, const void* q, KVLayer kv, SegTables tabs,

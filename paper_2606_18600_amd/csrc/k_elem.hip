@@ -10,11 +10,9 @@ namespace stage_k {
 
 namespace {
 
-constexpr int kNormThreads = 256;
-// One block per row; the row is held in registers (up to kNormVec float4 per
-// thread), so each kernel is one round trip to memory. H is a multiple of 4
-// and at most 4 * kNormThreads * kNormVec.
-constexpr int kNormVec = 16;
+// RMSNorm: one block per row; the row is held in registers (16384 / 4 /
+// threads float4 per thread), so each kernel is one round trip to memory.
+// H is a multiple of 4 and at most 16384.
 
 template <typename T> struct vec4_io;
 template <> struct vec4_io<float> {
@@ -48,32 +46,38 @@ __device__ __forceinline__ void store_act4(float* h, int t, int k, int K, float4
   *(float4*)(h + (size_t)t * K + k) = v;
 }
 
-template <typename InT, typename OutT, bool kEmbed>
-__global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const InT* __restrict__ in,
-                                                               float* __restrict__ x,
-                                                               const float* __restrict__ part,
-                                                               int splits, int T,
-                                                               OutT* __restrict__ h,
-                                                               const OutT* __restrict__ gain,
-                                                               int H, float eps) {
+// kS: number of split-K partial planes added to x (compile time, so that all
+// of a thread's loads are issued together).
+template <typename InT, typename OutT, bool kEmbed, int kThreads, int kS>
+__global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const InT* __restrict__ in,
+                                                           float* __restrict__ x,
+                                                           const float* __restrict__ part, int T,
+                                                           OutT* __restrict__ h,
+                                                           const OutT* __restrict__ gain, int H,
+                                                           float eps) {
+  constexpr int kVec = 16384 / 4 / kThreads;
   const int t = blockIdx.x;
   const size_t row = (size_t)t * H;
   const size_t plane = (size_t)T * H;
   const int H4 = H >> 2;
-  __shared__ float red[kNormThreads / STAGE_WAVE];
-  float4 v[kNormVec];
+  __shared__ float red[kThreads / STAGE_WAVE];
+  float4 v[kVec];
   float ss = 0.f;
 #pragma unroll
-  for (int j = 0; j < kNormVec; ++j) {
-    const int i4 = threadIdx.x + j * kNormThreads;
+  for (int j = 0; j < kVec; ++j) {
+    const int i4 = threadIdx.x + j * kThreads;
     if (i4 < H4) {
       const size_t e = row + 4 * (size_t)i4;
       if constexpr (kEmbed)
         v[j] = vec4_io<InT>::load(in, e);
       else
         v[j] = *(const float4*)(x + e);
-      for (int sp = 0; sp < splits; ++sp) add4(v[j], *(const float4*)(part + sp * plane + e));
-      if (kEmbed || splits > 0) *(float4*)(x + e) = v[j];
+      float4 p[kS > 0 ? kS : 1];
+#pragma unroll
+      for (int sp = 0; sp < kS; ++sp) p[sp] = *(const float4*)(part + sp * plane + e);
+#pragma unroll
+      for (int sp = 0; sp < kS; ++sp) add4(v[j], p[sp]);
+      if (kEmbed || kS > 0) *(float4*)(x + e) = v[j];
       ss += v[j].x * v[j].x + v[j].y * v[j].y + v[j].z * v[j].z + v[j].w * v[j].w;
     }
   }
@@ -82,11 +86,11 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const InT* __rest
   __syncthreads();
   float tot = 0.f;
 #pragma unroll
-  for (int w = 0; w < kNormThreads / STAGE_WAVE; ++w) tot += red[w];
+  for (int w = 0; w < kThreads / STAGE_WAVE; ++w) tot += red[w];
   const float r = 1.0f / sqrtf(tot / (float)H + eps);
 #pragma unroll
-  for (int j = 0; j < kNormVec; ++j) {
-    const int i4 = threadIdx.x + j * kNormThreads;
+  for (int j = 0; j < kVec; ++j) {
+    const int i4 = threadIdx.x + j * kThreads;
     if (i4 < H4) {
       const float4 g = vec4_io<OutT>::load(gain, 4 * (size_t)i4);
       store_act4(h, t, 4 * i4, H,
@@ -94,6 +98,39 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const InT* __rest
                              v[j].w * r * g.w));
     }
   }
+}
+
+template <typename InT, typename OutT, bool kEmbed, int kThreads>
+hipError_t launch_norm_t(const InT* in, float* x, Partials add, OutT* h, const OutT* gain, int T,
+                         int H, float eps, hipStream_t s) {
+  switch (add.splits) {
+#define STAGE_NORM_CASE(S)                                                                   \
+  case S:                                                                                    \
+    rmsnorm_kernel<InT, OutT, kEmbed, kThreads, S><<<T, kThreads, 0, s>>>(in, x, add.p, T, h, \
+                                                                         gain, H, eps);      \
+    break;
+    STAGE_NORM_CASE(0)
+    STAGE_NORM_CASE(1)
+    STAGE_NORM_CASE(2)
+    STAGE_NORM_CASE(3)
+    STAGE_NORM_CASE(4)
+    STAGE_NORM_CASE(5)
+    STAGE_NORM_CASE(6)
+    STAGE_NORM_CASE(7)
+    STAGE_NORM_CASE(8)
+#undef STAGE_NORM_CASE
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+// Wide rows get 1024 threads (more loads in flight per row), narrow ones 256.
+template <typename InT, typename OutT, bool kEmbed>
+hipError_t launch_norm(const InT* in, float* x, Partials add, OutT* h, const OutT* gain, int T,
+                       int H, float eps, hipStream_t s) {
+  if (H >= 4096) return launch_norm_t<InT, OutT, kEmbed, 1024>(in, x, add, h, gain, T, H, eps, s);
+  return launch_norm_t<InT, OutT, kEmbed, 256>(in, x, add, h, gain, T, H, eps, s);
 }
 
 template <typename OutT>
@@ -178,16 +215,16 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(const float* __restrict__ 
   const int off = pos % kBlock;
   T* kplane = kv + ((blk * n_kv + kh) * 2 + 0) * (int64_t)kBlock * d;
   T* vplane = kplane + (int64_t)kBlock * d;
-  elem<T>::store(kplane, (size_t)off * d + lane, ra);
-  elem<T>::store(kplane, (size_t)off * d + lane + half, rb);
+  elem<T>::store(kplane, kv_k_offset(off, lane), ra);
+  elem<T>::store(kplane, kv_k_offset(off, lane + half), rb);
   const int vcol = (n_q + n_kv + kh) * d;
   float va = 0.f, vb = 0.f;
   for (int sp = 0; sp < splits; ++sp) {
     va += row[sp * plane + vcol + lane];
     vb += row[sp * plane + vcol + lane + half];
   }
-  elem<T>::store(vplane, (size_t)lane * kBlock + off, va);
-  elem<T>::store(vplane, (size_t)(lane + half) * kBlock + off, vb);
+  elem<T>::store(vplane, kv_v_offset(off, lane), va);
+  elem<T>::store(vplane, kv_v_offset(off, lane + half), vb);
 }
 
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + expf(-z)); }
@@ -235,25 +272,22 @@ inline int grid_for(size_t n, int threads) {
 hipError_t embed_norm(DType dt, const void* hidden_in, float* x, void* h, const void* gain, int T,
                       int H, float eps, hipStream_t s) {
   if (T == 0) return hipSuccess;
+  const Partials none{nullptr, 0};
   if (dt == DT_BF16)
-    rmsnorm_kernel<bf16_t, bf16_t, true><<<T, kNormThreads, 0, s>>>(
-        (const bf16_t*)hidden_in, x, nullptr, 0, T, (bf16_t*)h, (const bf16_t*)gain, H, eps);
-  else
-    rmsnorm_kernel<float, float, true><<<T, kNormThreads, 0, s>>>(
-        (const float*)hidden_in, x, nullptr, 0, T, (float*)h, (const float*)gain, H, eps);
-  return hipGetLastError();
+    return launch_norm<bf16_t, bf16_t, true>((const bf16_t*)hidden_in, x, none, (bf16_t*)h,
+                                             (const bf16_t*)gain, T, H, eps, s);
+  return launch_norm<float, float, true>((const float*)hidden_in, x, none, (float*)h,
+                                         (const float*)gain, T, H, eps, s);
 }
 
 hipError_t rmsnorm(DType dt, float* x, Partials add, void* h, const void* gain, int T, int H,
                    float eps, hipStream_t s) {
   if (T == 0) return hipSuccess;
   if (dt == DT_BF16)
-    rmsnorm_kernel<float, bf16_t, false><<<T, kNormThreads, 0, s>>>(
-        nullptr, x, add.p, add.splits, T, (bf16_t*)h, (const bf16_t*)gain, H, eps);
-  else
-    rmsnorm_kernel<float, float, false><<<T, kNormThreads, 0, s>>>(
-        nullptr, x, add.p, add.splits, T, (float*)h, (const float*)gain, H, eps);
-  return hipGetLastError();
+    return launch_norm<float, bf16_t, false>(nullptr, x, add, (bf16_t*)h, (const bf16_t*)gain, T,
+                                             H, eps, s);
+  return launch_norm<float, float, false>(nullptr, x, add, (float*)h, (const float*)gain, T, H,
+                                          eps, s);
 }
 
 hipError_t output_cast(DType dt, const float* x, Partials add, void* out, int T, int H,

@@ -29,8 +29,8 @@ struct SegTables {
   int32_t stride1;
 };
 
-// KV cache geometry of one layer: [num_blocks][n_kv][2][block][d]; plane 0
-// holds K as [block][d], plane 1 holds V transposed as [d][block].
+// KV cache geometry of one layer: [num_blocks][n_kv][2][block * d]; plane 0
+// holds K, plane 1 holds V, in the fragment layouts of packed.hpp.
 struct KVLayer {
   void* base;
   int32_t n_kv;
@@ -106,7 +106,7 @@ hipError_t attn_decode(DType dt, const void* q, KVLayer kv, SegTables tabs,
                        float* part_ml, hipStream_t s);
 hipError_t attn_merge(DType dt, const float* part_o, const float* part_ml,
                       const int32_t* tok_item_start, const int32_t* tok_rows, int n_tok, int n_q,
-                      int head_dim, void* out, hipStream_t s);
+                      int n_kv, int head_dim, void* out, hipStream_t s);
 hipError_t attn_prefill(DType dt, const void* q, KVLayer kv, SegTables tabs,
                         const PrefillItem* items, int n_items, int n_q, void* out,
                         hipStream_t s);

@@ -40,4 +40,17 @@ __host__ __device__ inline int gate_up_source_row(int n, int F) {
   return r < 32 ? 32 * g + r : F + 32 * g + (r - 32);
 }
 
+// KV cache: per (layer, block, kv head) a K plane and a V plane of
+// block_size (16) tokens x d, each stored as whole MFMA operand fragments.
+// K plane: fragments of 16 tokens x 32 d (the A operand of S^T = K Q^T);
+// lane l holds token l % 16, d offsets (l / 16) * 8 .. + 7 of the fragment.
+__host__ __device__ inline int kv_k_offset(int o, int d) {
+  return (d >> 5) * 512 + (o + 16 * ((d & 31) >> 3)) * 8 + (d & 7);
+}
+// V plane: fragments of 16 d x 16 tokens (the A operand of O^T += V^T P^T);
+// lane l holds d = l % 16 of the fragment and tokens (l / 16) * 4 .. + 3.
+__host__ __device__ inline int kv_v_offset(int o, int d) {
+  return (d >> 4) * 256 + ((d & 15) + 16 * (o >> 2)) * 4 + (o & 3);
+}
+
 }  // namespace stage_k

@@ -33,7 +33,7 @@ stage_status fail(stage_status code, const char* fmt, ...) {
 
 constexpr int kRing = 4;             // pinned staging buffers in flight
 constexpr int kMaxSplits = 32;       // decode key splits per sequence, at most
-constexpr int kSplitMinBlocks = 8;   // at least 8 blocks (128 keys) per split
+constexpr int kSplitMinBlocks = 4;   // at least 4 blocks (64 keys) per split
 constexpr int kSkinnyMaxRows = 128;  // decode-sized steps use split-K GEMMs
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -67,6 +67,7 @@ struct stage {
   int skinny_rows = 0;  // steps with at most this many tokens use split-K GEMMs
   // K splits of the four split-K GEMMs (QKV, O, gate-up, down)
   int s_qkv = 1, s_o = 1, s_gu = 1, s_down = 1;
+  int attn_waves = 3072;  // decode attention waves to aim for (one round)
 
   // workspace
   Region r_x, r_h, r_qkv, r_q, r_attn, r_m, r_gu, r_part_x, r_part_o, r_part_ml, r_meta, r_cos,
@@ -251,6 +252,14 @@ void build_meta(const stage* st, const stage_batch* pf, const stage_batch* dc, S
     return a.p0 + a.npos > b.p0 + b.npos;
   });
   m.n_ditems = 0;
+  // Key blocks per decode split: enough splits that the batch launches about
+  // `attn_waves` waves (one round on the chip), at least kSplitMinBlocks
+  // blocks each, at most kMaxSplits splits per sequence.
+  long long units = 0;
+  for (int j = 0; j < nd; ++j) units += (dc->ctx_lens[j] + kBlock) / kBlock;
+  units *= st->cfg.n_kv_heads;
+  const int bps_target =
+      (int)std::max<long long>(kSplitMinBlocks, (units + st->attn_waves - 1) / st->attn_waves);
   for (int j = 0; j < nd; ++j) {
     const int ctx = dc->ctx_lens[j];
     const int g = np + j;
@@ -262,7 +271,7 @@ void build_meta(const stage* st, const stage_batch* pf, const stage_batch* dc, S
     if (st->cfg.dtype != STAGE_BF16) continue;  // fp32 attention needs no split plan
     const int keys = ctx + 1;
     const int nb = (keys + kBlock - 1) / kBlock;
-    int splits = std::min(kMaxSplits, std::max(1, nb / kSplitMinBlocks));
+    int splits = std::min(kMaxSplits, std::max(1, (nb + bps_target - 1) / bps_target));
     const int bps = (nb + splits - 1) / splits;
     splits = (nb + bps - 1) / bps;
     for (int sp = 0; sp < splits; ++sp) {
@@ -404,7 +413,7 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
         });
         L(STAGE_OP_ATTN, [&] {
           return attn_merge(dt, st->at<float>(st->r_part_o), st->at<float>(st->r_part_ml),
-                            dm.item_start, dm.tok_rows, nd, nq, D, attn, s);
+                            dm.item_start, dm.tok_rows, nd, nq, nkv, D, attn, s);
         });
       }
     }
@@ -501,6 +510,7 @@ stage_status stage_create(const stage_model_config* cfg, int32_t layer_begin, in
     st->s_o = skinny_splits(H, qw, waves);
     st->s_gu = skinny_splits(2 * F, H, waves);
     st->s_down = skinny_splits(H, F, waves);
+    st->attn_waves = std::max(64, env_int("STAGE_ATTN_WAVES", 3072));
   }
   if ((e = hipGetDevice(&st->device)) != hipSuccess) {
     delete st;

@@ -169,14 +169,27 @@ class DeviceStage:
             pass
 
 
+def kv_plane_index(block: int, d: int):
+    """Index arrays (o, dd) -> flat position of K[o][dd] and V[o][dd] inside
+    one (block, kv head) plane (the fragment layouts of the KV pool)."""
+    o = np.arange(block)[:, None]
+    dd = np.arange(d)[None, :]
+    k = (dd // 32) * 512 + (o + 16 * ((dd % 32) // 8)) * 8 + dd % 8
+    v = (dd // 16) * 256 + (dd % 16 + 16 * (o // 4)) * 4 + o % 4
+    return k, v
+
+
 def gpu_kv_to_oracle_layout(kv6: torch.Tensor) -> List[Dict[str, np.ndarray]]:
-    """Convert the GPU pool [L][nb][nkv][2][16][d] (V stored [d][16]) into a
-    list of per-layer {'k','v'} arrays [nb][16][nkv][d] in float64."""
+    """Convert the GPU pool [L][nb][nkv][2][16][d] (planes in fragment order)
+    into per-layer {'k','v'} arrays [nb][16][nkv][d] in float64."""
     a = kv6.detach().to(torch.float64).cpu().numpy()
+    L, nb, nkv, _, blk, d = a.shape
+    ki, vi = kv_plane_index(blk, d)
     out = []
-    for l in range(a.shape[0]):
-        k = a[l, :, :, 0].transpose(0, 2, 1, 3)                   # [nb][16][nkv][d]
-        v = a[l, :, :, 1].reshape(a.shape[1], a.shape[2], a.shape[5], a.shape[4])  # [nb][nkv][d][16]
-        v = v.transpose(0, 3, 1, 2)                               # [nb][16][nkv][d]
-        out.append({"k": np.ascontiguousarray(k), "v": np.ascontiguousarray(v)})
+    for l in range(L):
+        flat = a[l].reshape(nb, nkv, 2, blk * d)
+        k = flat[:, :, 0, :][:, :, ki]          # [nb][nkv][16][d]
+        v = flat[:, :, 1, :][:, :, vi]
+        out.append({"k": np.ascontiguousarray(k.transpose(0, 2, 1, 3)),
+                    "v": np.ascontiguousarray(v.transpose(0, 2, 1, 3))})
     return out
