@@ -43,7 +43,12 @@ design notes of the repository):
   block table ``bt`` lives at ``(bt[p // block_size], p % block_size)``.
 
 Precision: float64 by default; ``dtype=np.float32`` runs the same code in
-float32 (used only to time a CPU baseline).
+float32 (used only to time a CPU baseline). A diagnostic sub-mode
+(``rounding=round_to_bf16``) rounds to bfloat16 at the points where a bf16
+stage stores values (norm outputs, q, k, v, attention probabilities before
+they weight v, the attention output, the SwiGLU output). It is never the
+parity reference; it measures how far bf16 storage alone moves the result
+(the floor any bf16 implementation shares).
 
 Parity status: every function here is pinned by ``tests/test_oracle_*.py``
 (closed forms, invariants, brute force and an independent library
@@ -64,6 +69,7 @@ __all__ = [
     "rms_norm",
     "silu",
     "rope",
+    "round_to_bf16",
     "slot_of",
     "attention_one_sequence",
     "layer_forward",
@@ -148,13 +154,23 @@ def rope(u: np.ndarray, pos: np.ndarray, theta: float) -> np.ndarray:
     return np.concatenate([a * c - b * s, a * s + b * c], axis=-1)
 
 
+def round_to_bf16(a: np.ndarray) -> np.ndarray:
+    """Round to the nearest bfloat16 value (ties to even), returned in the
+    input dtype: keep the top 16 bits of the float32 representation after
+    adding half an ulp of bfloat16 (plus the tie-breaking bit)."""
+    f = np.asarray(a, np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32).astype(np.asarray(a).dtype)
+
+
 def slot_of(block_table: Sequence[int], p: int, block_size: int):
     """(block id, offset) holding position ``p`` of a sequence."""
     return int(block_table[p // block_size]), p % block_size
 
 
 def attention_one_sequence(q: np.ndarray, k_all: np.ndarray, v_all: np.ndarray,
-                           q_pos: np.ndarray) -> np.ndarray:
+                           q_pos: np.ndarray, rounding=None) -> np.ndarray:
     """Causal grouped-query attention for one sequence.
 
     ``q``: ``[n, n_q, d]`` queries at positions ``q_pos``; ``k_all``,
@@ -176,13 +192,17 @@ def attention_one_sequence(q: np.ndarray, k_all: np.ndarray, v_all: np.ndarray,
         s = np.where(visible, s, -np.inf)
         s = s - s.max(axis=1, keepdims=True)
         p = np.exp(s)
-        p = p / p.sum(axis=1, keepdims=True)
+        if rounding is None:
+            p = p / p.sum(axis=1, keepdims=True)
+        else:
+            p = rounding(p) / p.sum(axis=1, keepdims=True)
         out[:, h, :] = p @ v_all[:, kvh, :]
     return out
 
 
 def layer_forward(cfg: OracleConfig, w: Dict[str, np.ndarray], x: np.ndarray,
-                  seqs: Sequence[SeqSpec], kv: Dict[str, np.ndarray]) -> np.ndarray:
+                  seqs: Sequence[SeqSpec], kv: Dict[str, np.ndarray],
+                  rounding=None) -> np.ndarray:
     """One pre-norm decoder layer over a packed batch.
 
     ``x``: ``[T, H]`` rows of all sequences packed in order (``q_len`` rows
@@ -191,12 +211,13 @@ def layer_forward(cfg: OracleConfig, w: Dict[str, np.ndarray], x: np.ndarray,
     the updated residual stream ``[T, H]``.
     """
     dt = x.dtype
+    rnd = rounding if rounding is not None else (lambda a: a)
     H, nq, nkv, d = cfg.hidden, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
     T = x.shape[0]
     assert T == sum(s.q_len for s in seqs)
 
     # attention branch
-    h = rms_norm(x, w["attn_norm"], cfg.rms_eps)
+    h = rnd(rms_norm(x, w["attn_norm"], cfg.rms_eps))
     qkv = h @ w["w_qkv"].T                                 # [T, (nq+2nkv)d]
     q = qkv[:, :nq * d].reshape(T, nq, d)
     k = qkv[:, nq * d:(nq + nkv) * d].reshape(T, nkv, d)
@@ -207,8 +228,9 @@ def layer_forward(cfg: OracleConfig, w: Dict[str, np.ndarray], x: np.ndarray,
 
     pos = np.concatenate([np.arange(s.ctx_len, s.ctx_len + s.q_len) for s in seqs]) \
         if T else np.zeros(0, np.int64)
-    q = rope(q, pos, cfg.rope_theta)
-    k = rope(k, pos, cfg.rope_theta)
+    q = rnd(rope(q, pos, cfg.rope_theta))
+    k = rnd(rope(k, pos, cfg.rope_theta))
+    v = rnd(v)
 
     attn = np.empty((T, nq, d), dt)
     row = 0
@@ -221,22 +243,23 @@ def layer_forward(cfg: OracleConfig, w: Dict[str, np.ndarray], x: np.ndarray,
         C = s.ctx_len + s.q_len
         k_all = np.stack([kv["k"][slot_of(s.block_table, t, cfg.block_size)] for t in range(C)])
         v_all = np.stack([kv["v"][slot_of(s.block_table, t, cfg.block_size)] for t in range(C)])
-        attn[rows] = attention_one_sequence(q[rows], k_all, v_all, pos[rows])
+        attn[rows] = attention_one_sequence(q[rows], k_all, v_all, pos[rows], rounding)
         row += s.q_len
 
-    x = x + attn.reshape(T, nq * d) @ w["w_o"].T
+    x = x + rnd(attn.reshape(T, nq * d)) @ w["w_o"].T
 
     # FFN branch
-    h2 = rms_norm(x, w["ffn_norm"], cfg.rms_eps)
+    h2 = rnd(rms_norm(x, w["ffn_norm"], cfg.rms_eps))
     gu = h2 @ w["w_gate_up"].T                              # [T, 2F]
-    m = silu(gu[:, :cfg.ffn]) * gu[:, cfg.ffn:]
+    m = rnd(silu(gu[:, :cfg.ffn]) * gu[:, cfg.ffn:])
     x = x + m @ w["w_down"].T
     return x
 
 
 def stage_forward(cfg: OracleConfig, layers: Sequence[Dict[str, np.ndarray]],
                   x: np.ndarray, seqs: Sequence[SeqSpec],
-                  kv_cache: Sequence[Dict[str, np.ndarray]], dtype=np.float64) -> np.ndarray:
+                  kv_cache: Sequence[Dict[str, np.ndarray]], dtype=np.float64,
+                  rounding=None) -> np.ndarray:
     """Forward pass of one stage: the layers of ``layers`` applied in order.
 
     ``layers[i]`` and ``kv_cache[i]`` belong to the i-th layer of the stage's
@@ -248,5 +271,5 @@ def stage_forward(cfg: OracleConfig, layers: Sequence[Dict[str, np.ndarray]],
     x = np.asarray(x, dtype)
     for w, kv in zip(layers, kv_cache):
         wd = {name: np.asarray(a, dtype) for name, a in w.items()}
-        x = layer_forward(cfg, wd, x, seqs, kv)
+        x = layer_forward(cfg, wd, x, seqs, kv, rounding)
     return x

@@ -26,21 +26,22 @@ MUTANTS = {
     "causal-exclusive": ("visible = t[None, :] <= q_pos[:, None]",
                          "visible = t[None, :] <= q_pos[:, None] - 1"),
     "scale-1-over-d": ("scale = 1.0 / np.sqrt(d)", "scale = 1.0 / d"),
-    "no-attn-residual": ("x = x + attn.reshape(T, nq * d) @ w[\"w_o\"].T",
-                         "x = attn.reshape(T, nq * d) @ w[\"w_o\"].T"),
-    "wo-transposed": ("attn.reshape(T, nq * d) @ w[\"w_o\"].T", "attn.reshape(T, nq * d) @ w[\"w_o\"]"),
-    "gate-up-swapped": ("m = silu(gu[:, :cfg.ffn]) * gu[:, cfg.ffn:]",
-                        "m = silu(gu[:, cfg.ffn:]) * gu[:, :cfg.ffn]"),
+    "no-attn-residual": ("x = x + rnd(attn.reshape(T, nq * d)) @ w[\"w_o\"].T",
+                         "x = rnd(attn.reshape(T, nq * d)) @ w[\"w_o\"].T"),
+    "wo-transposed": ("rnd(attn.reshape(T, nq * d)) @ w[\"w_o\"].T",
+                      "rnd(attn.reshape(T, nq * d)) @ w[\"w_o\"]"),
+    "gate-up-swapped": ("m = rnd(silu(gu[:, :cfg.ffn]) * gu[:, cfg.ffn:])",
+                        "m = rnd(silu(gu[:, cfg.ffn:]) * gu[:, :cfg.ffn])"),
     "silu-is-sigmoid": ("return z / (1.0 + np.exp(-z))", "return 1.0 / (1.0 + np.exp(-z))"),
     "norm-no-mean": ("ms = np.mean(x * x, axis=-1, keepdims=True)",
                      "ms = np.sum(x * x, axis=-1, keepdims=True)"),
     "norm-no-gain": ("return x / np.sqrt(ms + eps) * g", "return x / np.sqrt(ms + eps)"),
-    "ffn-norm-reuses-attn-gain": ("h2 = rms_norm(x, w[\"ffn_norm\"], cfg.rms_eps)",
-                                  "h2 = rms_norm(x, w[\"attn_norm\"], cfg.rms_eps)"),
+    "ffn-norm-reuses-attn-gain": ("h2 = rnd(rms_norm(x, w[\"ffn_norm\"], cfg.rms_eps))",
+                                  "h2 = rnd(rms_norm(x, w[\"attn_norm\"], cfg.rms_eps))"),
     "k-v-swapped": ("v = qkv[:, (nq + nkv) * d:].reshape(T, nkv, d)",
                     "v = qkv[:, nq * d:(nq + nkv) * d].reshape(T, nkv, d)"),
     "qk-norm-skipped-on-k": ("k = rms_norm(k, w[\"k_norm\"], cfg.qk_rms_eps)", "pass"),
-    "no-rope-on-k": ("k = rope(k, pos, cfg.rope_theta)", "pass"),
+    "no-rope-on-k": ("k = rnd(rope(k, pos, cfg.rope_theta))", "k = rnd(k)"),
     "positions-ignore-context": ("np.arange(s.ctx_len, s.ctx_len + s.q_len)", "np.arange(0, s.q_len)"),
     "slot-wrong-block": ("return int(block_table[p // block_size]), p % block_size",
                          "return int(block_table[p % len(block_table)]), p % block_size"),

@@ -388,3 +388,28 @@ def test_float32_oracle_close_to_float64():
                           O.new_kv_cache(cfg, 2, 12, np.float32), dtype=np.float32)
     assert y32.dtype == np.float32
     assert rel_l2(y32, y64) < 1e-6
+
+
+def test_round_to_bf16_matches_torch_and_the_bf16_grid():
+    r = np.random.default_rng(21)
+    a = np.concatenate([r.standard_normal(5000) * 10.0 ** r.integers(-6, 6, 5000),
+                        [0.0, -0.0, 1.0, 1.00390625, 1.0078125, 3.0e38, -2.5e-39]])
+    ref = torch.tensor(a, dtype=torch.float32).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(O.round_to_bf16(a), ref)
+    # ties go to even: 1 + 2^-8 lies halfway between 1 and 1 + 2^-7
+    assert O.round_to_bf16(np.array([1.0 + 2.0 ** -8]))[0] == 1.0
+    assert O.round_to_bf16(np.array([1.0 + 3 * 2.0 ** -8]))[0] == 1.0 + 2.0 ** -6
+
+
+def test_bf16_emulation_stays_close_and_default_is_exact():
+    shape = SMALL_QK
+    cfg, layers, bt, nb = _setup(shape, 22, [0], [30], n_layers=2)
+    x = synth.hidden_states(22, 1, 30, shape.hidden, np.float64)
+    y = O.stage_forward(cfg, layers, x, seqs_from([0], [30], bt), O.new_kv_cache(cfg, 2, nb))
+    y0 = O.stage_forward(cfg, layers, x, seqs_from([0], [30], bt), O.new_kv_cache(cfg, 2, nb),
+                         rounding=None)
+    np.testing.assert_array_equal(y, y0)
+    ye = O.stage_forward(cfg, layers, x, seqs_from([0], [30], bt), O.new_kv_cache(cfg, 2, nb),
+                         rounding=O.round_to_bf16)
+    e = rel_l2(ye, y)
+    assert 1e-4 < e < 2e-2
