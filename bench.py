@@ -26,8 +26,10 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-HBM_PEAK_GBS = 8000.0
-BF16_PEAK_TFLOPS = 2500.0
+from paper_2606_18600_amd.roofline import (BF16_PEAK_TFLOPS, HBM_PEAK_GBS,  # noqa: E402
+                                           decode_step_bytes, gemm_bytes, prefill_flops,
+                                           step_roofline_ms)
+
 METRIC = "stage decode tok/s + prefill tok/s on 1 GPU; % of HBM / MFMA roofline"
 
 
@@ -35,32 +37,77 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def gemm_bytes(M, N, K, out_bytes):
-    """Algorithmic HBM bytes of one GEMM launch: W and A (bf16) read once,
-    the output written once."""
-    return N * K * 2 + M * K * 2 + M * N * out_bytes
-
-
-def decode_step_bytes(shape, n_layers, ctx_lens):
-    """Algorithmic bytes of one decode step: every weight once, the valid KV
-    of every sequence once per layer, the new KV and the hidden rows in/out."""
-    B = len(ctx_lens)
-    kv_tok = 2 * shape.n_kv_heads * shape.head_dim * 2
-    w = shape.params_per_layer() * 2
-    per_layer = w + int(np.sum(ctx_lens + 1)) * kv_tok
-    return n_layers * per_layer + 2 * B * shape.hidden * 2
-
-
-def prefill_flops(shape, n_layers, chunks):
-    """Algorithmic FLOPs of a chunked prefill: 2 * weights per token for the
-    GEMMs plus causal attention, 4 * d * n_q per (query, visible key)."""
-    lin = 2 * (shape.params_per_layer() - 2 * shape.hidden)
-    f = 0
-    for ctx, q in chunks:
-        ctx, q = float(ctx), float(q)
-        pairs = q * ctx + q * (q + 1) / 2
-        f += q * lin + 4.0 * shape.head_dim * shape.n_q_heads * pairs
-    return n_layers * f
+def bench_q32_mixed(args):
+    """Qwen3-32B-shaped mixed step, 16 layers [24, 40): every step carries 4
+    prefill chunks of 512 tokens (cached prefixes 0/512/1024/1536) and 128
+    decode tokens with contexts uniform 256..4096."""
+    import torch
+    from paper_2606_18600_amd import stage as S
+    from paper_2606_18600_amd import synth
+    from paper_2606_18600_amd.harness import (DeviceStage, device_layer_weights, model_config,
+                                              pack_layer)
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    shape, seed = synth.QWEN32B, args.seed
+    wl = synth.WORKLOADS["q32-mixed"]
+    L0, nL = wl.layer_begin, wl.n_layers
+    K, W = args.steps, args.warmup
+    cfg = model_config(shape, "bf16")
+    log(f"[bench] generating {nL} layers of {shape.name} weights on the device")
+    weights = [pack_layer(cfg, device_layer_weights(shape, seed, l, "bf16"), free_source=True)
+               for l in range(L0, wl.layer_end)]
+    pc = np.array([0, 512, 1024, 1536], np.int32)
+    pq = np.full(4, 512, np.int32)
+    dctx0 = synth.uniform_lengths(seed, 3, 128, 256, 4096)
+    steps_total = W + 2 * K
+    dfinal = dctx0 + steps_total + 1
+    alloc_n = int(((pc + pq + 15) // 16).sum() + ((dfinal + 15) // 16).sum()) + 1
+    alloc = synth.BlockAllocator(alloc_n, seed)
+    pbt = torch.from_numpy(synth.make_block_tables(pc + pq, 128, alloc)).to(dev)
+    dbt = torch.from_numpy(synth.make_block_tables(dfinal, int(((dfinal + 15) // 16).max()),
+                                                   alloc)).to(dev)
+    st = DeviceStage(shape, "bf16", L0, weights, alloc_n, max_tokens=2176, max_seqs=132,
+                     packed=True)
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    st.kv_pool.normal_(0.0, 1.0, generator=g)
+    x = torch.empty((2176, shape.hidden), dtype=torch.bfloat16, device=dev).normal_(generator=g)
+    out = torch.empty_like(x)
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    i = 0
+    for _ in range(W):
+        st.mixed(pq, pc, pbt, dctx0 + i, dbt, x, out, stream=sp)
+        i += 1
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ctx_timed = []
+    e0.record(stream)
+    for _ in range(K):
+        st.mixed(pq, pc, pbt, dctx0 + i, dbt, x, out, stream=sp)
+        ctx_timed.append(dctx0 + i)
+        i += 1
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / K
+    S.stage_set_op_timing(st.handle, True)
+    for _ in range(K):
+        st.mixed(pq, pc, pbt, dctx0 + i, dbt, x, out, stream=sp)
+        i += 1
+    op_ms, op_n = S.stage_read_op_times(st.handle)
+    st.close()
+    chunks = list(zip(pc.tolist(), pq.tolist()))
+    roof = float(np.mean([step_roofline_ms(shape, nL, chunks, c) for c in ctx_timed]))
+    res = {"workload": "q32-mixed: Qwen3-32B-shaped stage, layers [24,40); per step 4 x 512 "
+                       "prefill chunks (prefixes 0/512/1024/1536) + 128 decodes, contexts "
+                       "uniform 256-4096",
+           "ms_per_step": round(ms, 3), "prefill_tok_s": round(2048 / (ms / 1e3), 1),
+           "decode_tok_s": round(128 / (ms / 1e3), 1),
+           "roofline_ms": round(roof, 3), "roofline_frac": round(roof / ms, 4),
+           "ops_ms_per_step": {S.OP_NAMES[j]: round(op_ms[j] / K, 4) for j in range(len(op_ms))}}
+    log(f"[bench] q32-mixed {ms:.3f} ms/step (roofline {roof:.3f} ms, {roof / ms:.1%}); "
+        f"{2048 / (ms / 1e3):.0f} prefill + {128 / (ms / 1e3):.0f} decode tok/s")
+    return res
 
 
 def cpu_baseline(shape, ctx_lens, seed):
@@ -106,11 +153,30 @@ def main():
     ap.add_argument("--seed", type=int, default=2606)
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--requests", type=int, default=512,
+                    help="l70-full: new requests queued behind the 128 running ones")
+    ap.add_argument("--arrival-rate", type=float, default=0.0,
+                    help="l70-full: Poisson arrivals per second (0: all at t=0)")
+    ap.add_argument("--workload", default="l70-decode",
+                    choices=["l70-decode", "q32-mixed", "l70-full"],
+                    help="l70-decode (default: the metric's workload, plus the chunked prefill "
+                         "of the same stage); q32-mixed and l70-full print their own line")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the stage runs on a single MI355X and this build "
               f"has no multi-GPU path (asked for --gpus {args.gpus}).", file=sys.stderr)
         sys.exit(2)
+
+    if args.workload == "q32-mixed":
+        print(json.dumps({"metric": METRIC, "n_gpus": 1, "steps": args.steps,
+                          "warmup": args.warmup, "dtype": "bf16", "data": "synthetic",
+                          **bench_q32_mixed(args)}), flush=True)
+        return
+    if args.workload == "l70-full":
+        from paper_2606_18600_amd.batcher import bench_l70_full
+        print(json.dumps({"metric": METRIC, "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
+                          **bench_l70_full(args, log)}), flush=True)
+        return
 
     import torch
     from paper_2606_18600_amd import stage as S
