@@ -11,8 +11,9 @@
 //   partial tile per K split; the consumer kernel sums the splits. With one
 //   split the gate-up GEMM applies SwiGLU in its epilogue.
 // * gemm_tiled_bf16: many rows (prefill, mixed steps), compute-bound.
-//   128 x 128 block tiles, 64-wide k steps double-buffered in LDS, 4 waves of
-//   64 x 64; epilogues: fp32 store, residual add, SwiGLU.
+//   256 x 256 (8 waves of 128 x 64) or 128 x 128 block tiles; whole fragments
+//   copied HBM -> LDS with direct loads, 64-wide k steps double-buffered;
+//   epilogues: fp32 store, residual add, SwiGLU.
 // * gemm_tiled_f32: plain fp32 SIMT tiles for the fp32 mode (row-major).
 #include "common.hpp"
 #include "kernels.hpp"
@@ -148,116 +149,118 @@ __global__ __launch_bounds__(SK_WAVES * 64) void gemm_skinny_bf16(const bf16_t* 
 // ---------------------------------------------------------------------------
 // bf16 tiled GEMM (prefill / mixed)
 // ---------------------------------------------------------------------------
-constexpr int TB_M = 128, TB_N = 128, TB_K = 64;
-constexpr int TB_THREADS = 256;
+// Block tile: BMT m-tiles (16 rows each) x BNG weight groups (64 columns
+// each); waves WM x WN, each owning (BMT/WM) m-tiles x (BNG/WN) groups. One
+// stage = 64 of K = 2 k-tiles: BMT*2 A fragments and BNG*8 W fragments. The
+// packed layouts make every fragment 1 KB contiguous in HBM, so each wave
+// copies its share straight into LDS with global_load_lds_dwordx4 (lane l
+// lands at base + 16 l, which is the fragment's own lane order); two stages
+// alternate in LDS.
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
-template <int EPI>
-__global__ __launch_bounds__(TB_THREADS) void gemm_tiled_bf16(const bf16_t* __restrict__ A,
-                                                              const bf16_t* __restrict__ W, int M,
-                                                              int N, int K, void* __restrict__ out) {
-  // LDS tiles hold whole fragments: A [8 m-tiles][2 k-tiles][64 lanes],
-  // B [2 groups][2 k-tiles][4 n-tiles][64 lanes], 16 bytes per lane.
-  __shared__ u32x4_t As[2][TB_M / 16 * 2 * 64];
-  __shared__ u32x4_t Bs[2][2 * 2 * 4 * 64];
+template <int BMT, int BNG, int WM, int WN, int EPI>
+__global__ __launch_bounds__(WM * WN * 64) void gemm_tiled_bf16(const bf16_t* __restrict__ A,
+                                                               const bf16_t* __restrict__ W,
+                                                               int M, int N, int K,
+                                                               void* __restrict__ out) {
+  constexpr int NW = WM * WN;
+  constexpr int AF = BMT * 2;
+  constexpr int BF = BNG * 8;
+  constexpr int FR = AF + BF;
+  constexpr int PER_WAVE = FR / NW;
+  constexpr int TM = BMT / WM;
+  constexpr int TG = BNG / WN;
+  static_assert(FR % NW == 0 && BMT % WM == 0 && BNG % WN == 0, "tile split");
+  __shared__ u32x4_t lds[2][FR * 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int mt0 = blockIdx.x * BMT, g0 = blockIdx.y * BNG, KT = K / 32;
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int mt0 = blockIdx.x * (TB_M / 16);  // first m-tile of the block
-  const int g0 = blockIdx.y * 2;             // first 64-row group of W
-  const int KT = K / 32;
-
-  // Staging map: 4 chunks of A and 4 of B per thread per K tile. A chunk q
-  // (0..1023) is (m-tile q/128, k-tile (q/64)%2, lane q%64); B chunk q is
-  // (group q/512, (k-tile, n-tile, lane) = q%512), each contiguous in memory.
-  const bf16_t* a_src[4];
-  const bf16_t* b_src[4];
+  // this wave's fragments of a stage: source (at stage 0) and LDS slot
+  const bf16_t* src[PER_WAVE];
+  size_t stride[PER_WAVE];
 #pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    const int q = tid + p * TB_THREADS;
-    a_src[p] = A + ((size_t)(mt0 + q / 128) * KT) * 512 + (q % 128) * 8;
-    b_src[p] = W + ((size_t)(g0 + q / 512) * KT * 4) * 512 + (q % 512) * 8;
+  for (int p = 0; p < PER_WAVE; ++p) {
+    const int f = wave * PER_WAVE + p;
+    if (f < AF) {
+      src[p] = A + ((size_t)(mt0 + f / 2) * KT + f % 2) * 512 + lane * 8;
+      stride[p] = 2 * 512;
+    } else {
+      const int fb = f - AF;
+      src[p] = W + (((size_t)(g0 + fb / 8) * KT + (fb / 4) % 2) * 4 + fb % 4) * 512 + lane * 8;
+      stride[p] = 2 * 4 * 512;
+    }
   }
+  auto issue = [&](int kt, int buf) {
+#pragma unroll
+    for (int p = 0; p < PER_WAVE; ++p)
+      __builtin_amdgcn_global_load_lds((const void*)(src[p] + (size_t)kt * stride[p]),
+                                       (lds_ptr_t)&lds[buf][(wave * PER_WAVE + p) * 64], 16, 0, 0);
+  };
 
-  f32x4_t acc[4][4];
+  f32x4_t acc[TM][TG * 4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < TG * 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  u32x4_t ra[4], rb[4];
-  const int KTILES = K / TB_K;
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    ra[p] = ldg128(a_src[p]);
-    rb[p] = ldg128(b_src[p]);
-  }
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    As[0][tid + p * TB_THREADS] = ra[p];
-    Bs[0][tid + p * TB_THREADS] = rb[p];
-  }
+  const int KTILES = K / 64;
+  issue(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-
   for (int kt = 0; kt < KTILES; ++kt) {
     const int buf = kt & 1;
-    const bool more = kt + 1 < KTILES;
-    if (more) {
-      // next K tile: +2 k-tiles of A fragments, +2*4 fragments of W
-#pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        ra[p] = ldg128(a_src[p] + (size_t)(kt + 1) * 2 * 512);
-        rb[p] = ldg128(b_src[p] + (size_t)(kt + 1) * 2 * 4 * 512);
-      }
-    }
+    // the other buffer was last read in the previous stage, before its barrier
+    if (kt + 1 < KTILES) issue(kt + 1, buf ^ 1);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      u32x4_t fa[4], fb[4];
+      u32x4_t fb[TG * 4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) fa[i] = As[buf][((wm * 4 + i) * 2 + h) * 64 + lane];
+      for (int gi = 0; gi < TG; ++gi)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) fb[j] = Bs[buf][((wn * 2 + h) * 4 + j) * 64 + lane];
+        for (int j = 0; j < 4; ++j)
+          fb[gi * 4 + j] = lds[buf][(AF + ((wn * TG + gi) * 2 + h) * 4 + j) * 64 + lane];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < TM; ++i) {
+        const u32x4_t fa = lds[buf][((wm * TM + i) * 2 + h) * 64 + lane];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mfma16x16x32(fa[i], fb[j], acc[i][j]);
-    }
-    if (more) {
-#pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        As[buf ^ 1][tid + p * TB_THREADS] = ra[p];
-        Bs[buf ^ 1][tid + p * TB_THREADS] = rb[p];
+        for (int j = 0; j < TG * 4; ++j) acc[i][j] = mfma16x16x32(fa, fb[j], acc[i][j]);
       }
     }
+    __builtin_amdgcn_s_waitcnt(0);  // next stage landed in LDS
     __syncthreads();
   }
 
   // Epilogue: lane l holds column (g*64 + j*16 + l%16), rows (l/16)*4 + r of
-  // m-tile (mt0 + wm*4 + i).
-  const int g = g0 + wn;
+  // m-tile (mt0 + wm*TM + i).
   const int r16 = lane & 15;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < TM; ++i) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int m = (mt0 + wm * 4 + i) * 16 + (lane >> 4) * 4 + r;
+      const int m = (mt0 + wm * TM + i) * 16 + (lane >> 4) * 4 + r;
       if (m >= M) continue;
-      if (EPI == EPI_SWIGLU) {
-        const int F = N / 2;
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int c = g * 32 + j * 16 + r16;
-          ((bf16_t*)out)[packed_a_offset(m, c, F)] =
-              f32_to_bf16(silu_f(acc[i][j][r]) * acc[i][j + 2][r]);
-        }
-      } else {
+      for (int gi = 0; gi < TG; ++gi) {
+        const int g = g0 + wn * TG + gi;
+        if (EPI == EPI_SWIGLU) {
+          // tiles 0,1: gate columns 32g..32g+31; tiles 2,3: the matching up columns
+          const int F = N / 2;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          float* o = (float*)out + (size_t)m * N + g * 64 + j * 16 + r16;
-          if (EPI == EPI_RESID_ADD)
-            *o += acc[i][j][r];
-          else
-            *o = acc[i][j][r];
+          for (int j = 0; j < 2; ++j) {
+            const int c = g * 32 + j * 16 + r16;
+            ((bf16_t*)out)[packed_a_offset(m, c, F)] =
+                f32_to_bf16(silu_f(acc[i][gi * 4 + j][r]) * acc[i][gi * 4 + j + 2][r]);
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            float* o = (float*)out + (size_t)m * N + g * 64 + j * 16 + r16;
+            if (EPI == EPI_RESID_ADD)
+              *o += acc[i][gi * 4 + j][r];
+            else
+              *o = acc[i][gi * 4 + j][r];
+          }
         }
       }
     }
@@ -390,22 +393,35 @@ hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int
       return hipErrorInvalidValue;
     return hipGetLastError();
   }
-  if (N % TB_N != 0 || K % TB_K != 0) return hipErrorInvalidValue;
-  dim3 grid((M + TB_M - 1) / TB_M, N / TB_N);
+  if (N % 128 != 0 || K % 64 != 0) return hipErrorInvalidValue;
+  // Two tilings: 256 x 256 (8 waves, 128 KB LDS, one block per CU) reaches
+  // about 1.1 PFLOP/s on these shapes, 128 x 128 (4 waves, 64 KB, two per CU)
+  // about 0.97; weigh each by how full its last round of blocks is.
+  auto util = [](long blocks, long slots) {
+    const long rounds = (blocks + slots - 1) / slots;
+    return (double)blocks / (double)(rounds * slots);
+  };
+  const long mb256 = (M + 255) / 256, mb128 = (M + 127) / 128;
+  const bool big = N % 256 == 0 &&
+                   1.12 * util(mb256 * (N / 256), 256) >= 0.97 * util(mb128 * (N / 128), 512);
   const bf16_t* a = (const bf16_t*)A;
   const bf16_t* w = (const bf16_t*)W;
-  switch (epi) {
-    case EPI_STORE_F32:
-      gemm_tiled_bf16<EPI_STORE_F32><<<grid, TB_THREADS, 0, s>>>(a, w, M, N, K, out);
-      break;
-    case EPI_RESID_ADD:
-      gemm_tiled_bf16<EPI_RESID_ADD><<<grid, TB_THREADS, 0, s>>>(a, w, M, N, K, out);
-      break;
-    case EPI_SWIGLU:
-      gemm_tiled_bf16<EPI_SWIGLU><<<grid, TB_THREADS, 0, s>>>(a, w, M, N, K, out);
-      break;
-    default:
-      return hipErrorInvalidValue;
+  if (big) {
+    dim3 grid(mb256, N / 256);
+    switch (epi) {
+      case EPI_STORE_F32: gemm_tiled_bf16<16, 4, 2, 4, EPI_STORE_F32><<<grid, 512, 0, s>>>(a, w, M, N, K, out); break;
+      case EPI_RESID_ADD: gemm_tiled_bf16<16, 4, 2, 4, EPI_RESID_ADD><<<grid, 512, 0, s>>>(a, w, M, N, K, out); break;
+      case EPI_SWIGLU: gemm_tiled_bf16<16, 4, 2, 4, EPI_SWIGLU><<<grid, 512, 0, s>>>(a, w, M, N, K, out); break;
+      default: return hipErrorInvalidValue;
+    }
+  } else {
+    dim3 grid(mb128, N / 128);
+    switch (epi) {
+      case EPI_STORE_F32: gemm_tiled_bf16<8, 2, 2, 2, EPI_STORE_F32><<<grid, 256, 0, s>>>(a, w, M, N, K, out); break;
+      case EPI_RESID_ADD: gemm_tiled_bf16<8, 2, 2, 2, EPI_RESID_ADD><<<grid, 256, 0, s>>>(a, w, M, N, K, out); break;
+      case EPI_SWIGLU: gemm_tiled_bf16<8, 2, 2, 2, EPI_SWIGLU><<<grid, 256, 0, s>>>(a, w, M, N, K, out); break;
+      default: return hipErrorInvalidValue;
+    }
   }
   return hipGetLastError();
 }
