@@ -27,7 +27,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 from paper_2606_18600_amd.roofline import (BF16_PEAK_TFLOPS, HBM_PEAK_GBS,  # noqa: E402
-                                           decode_step_bytes, gemm_bytes, prefill_flops,
+                                           decode_step_bytes, gate_up_swiglu_bytes, prefill_flops,
                                            step_roofline_ms)
 
 METRIC = "stage decode tok/s + prefill tok/s on 1 GPU; % of HBM / MFMA roofline"
@@ -110,6 +110,176 @@ def bench_q32_mixed(args):
     return res
 
 
+# The decode gate-up projection is the split-K GEMM instantiated with the
+# fused SwiGLU epilogue (template arguments <m-tiles, 1>).
+GATE_UP_DECODE_KERNEL = r"gemm_skinny_bf16<\d+, 1>"
+KERNEL_SOURCES = ("paper_2606_18600_amd/csrc/k_gemm.hip", "paper_2606_18600_amd/csrc/common.hpp",
+                  "paper_2606_18600_amd/csrc/packed.hpp", "paper_2606_18600_amd/csrc/kernels.hpp")
+TRAFFIC_FILE = "profiles/gate_up_l70_decode_traffic.txt"
+
+
+def kernel_source_sha():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def committed_traffic(kernel_re):
+    """HBM bytes per launch of the kernel, from the committed counter summary
+    (FETCH_SIZE and WRITE_SIZE runs scaled by the copy probe), or None when
+    the summary is missing or the kernel sources changed since it was made."""
+    import re
+    path = os.path.join(ROOT, TRAFFIC_FILE)
+    if not os.path.exists(path):
+        return None, "no counter summary"
+    sha, rows = None, {}
+    for line in open(path):
+        if line.startswith("source_sha256:"):
+            sha = line.split(":", 1)[1].strip()
+        elif line.startswith("TRAFFIC "):
+            kv = dict(t.split("=", 1) for t in line.split()[1:])
+            rows[kv["kernel"]] = kv
+    if sha != kernel_source_sha():
+        return None, "counters predate the current kernel sources"
+    for name, kv in rows.items():
+        if re.fullmatch(kernel_re, name):
+            return (int(float(kv["fetch_bytes"]) + float(kv["write_bytes"])),
+                    f"{TRAFFIC_FILE}: {name} grid {kv['grid']}, fetch {kv['fetch_bytes']} + "
+                    f"write {kv['write_bytes']} bytes per launch")
+    return None, "kernel not in the counter summary"
+
+
+def calibrate(torch, S, stream):
+    """Secondary denominators measured on this GPU: the library's plain
+    streaming copy (read + write bytes) and a large bf16 library GEMM."""
+    nbytes = 4 << 30
+    src = torch.empty(nbytes // 2, dtype=torch.bfloat16, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1.0)
+    sp = stream.cuda_stream
+    ts = []
+    for r in range(6):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        S.stage_copy_probe(src.data_ptr(), dst.data_ptr(), nbytes, sp)
+        b.record(stream)
+        b.synchronize()
+        if r:
+            ts.append(a.elapsed_time(b))
+    copy_gbs = 2 * nbytes / (float(np.median(ts)) / 1e3) / 1e9
+    del src, dst
+    n = 8192
+    x = torch.randn((n, n), dtype=torch.bfloat16, device="cuda")
+    y = torch.randn((n, n), dtype=torch.bfloat16, device="cuda")
+    ts = []
+    for r in range(6):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        torch.mm(x, y)
+        b.record(stream)
+        b.synchronize()
+        if r:
+            ts.append(a.elapsed_time(b))
+    gemm_tfs = 2.0 * n ** 3 / (float(np.median(ts)) / 1e3) / 1e12
+    return {"copy_GBs": round(copy_gbs, 1), "copy_bytes": 2 * nbytes,
+            "gemm_TFLOPs": round(gemm_tfs, 1), "gemm_probe": f"torch.mm bf16 {n}^3"}
+
+
+def _short_kernel(name):
+    for junk in ("void ", "stage_k::(anonymous namespace)::", "(anonymous namespace)::",
+                 "stage_k::"):
+        name = name.replace(junk, "")
+    i = name.find("(")
+    return name[:i] if i > 0 else name
+
+
+def _csv_rows(d, suffix):
+    import csv
+    import glob
+    files = sorted(glob.glob(os.path.join(d, "**", f"*{suffix}"), recursive=True))
+    if not files:
+        raise SystemExit(f"no *{suffix} under {d}")
+    rows = []
+    for f in files:
+        with open(f, newline="") as fh:
+            rows += list(csv.DictReader(fh))
+    return rows
+
+
+def _grid(r):
+    if "Grid_Size_X" in r:
+        wg = max(1, int(r["Workgroup_Size_X"]))
+        return f"{int(r['Grid_Size_X']) // wg},{int(r.get('Grid_Size_Y', 1))}"
+    wg = max(1, int(r.get("Workgroup_Size", 1)))
+    return f"{int(r['Grid_Size']) // wg}"
+
+
+def summarize_trace(d, title, cmd, top=24):
+    """Per (kernel, grid) launch statistics of a rocprofv3 kernel trace."""
+    import collections
+    g = collections.defaultdict(list)
+    for r in _csv_rows(d, "kernel_trace.csv"):
+        g[(_short_kernel(r["Kernel_Name"]), _grid(r))].append(
+            (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    tot = sum(sum(v) for v in g.values())
+    out = [f"# {title}", "", f"command: {cmd}", "",
+           "Per (kernel, grid) launch statistics from the kernel trace (durations in us):", "",
+           f"{'kernel':56s} {'grid':>10s} {'calls':>6s} {'avg_us':>9s} {'min_us':>9s} "
+           f"{'max_us':>9s} {'pct':>6s}"]
+    for (k, grid), v in sorted(g.items(), key=lambda kv: -sum(kv[1]))[:top]:
+        out.append(f"{k[:56]:56s} {grid:>10s} {len(v):6d} {sum(v) / len(v):9.1f} "
+                   f"{min(v):9.1f} {max(v):9.1f} {100 * sum(v) / tot:6.2f}")
+    return "\n".join(out)
+
+
+def summarize_pmc(fetch_dir, write_dir, title, cmds, algorithmic, top=12):
+    """HBM traffic per launch from a FETCH_SIZE run and a WRITE_SIZE run, each
+    scaled by what the counter reads for the copy probe of known size."""
+    import collections
+    per = {}
+    for cname, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        g = collections.defaultdict(list)
+        for r in _csv_rows(d, "counter_collection.csv"):
+            if r["Counter_Name"] != cname:
+                continue
+            g[(_short_kernel(r["Kernel_Name"]), _grid(r))].append(float(r["Counter_Value"]))
+        per[cname] = {k: float(np.mean(v)) for k, v in g.items()}
+    copy_key = [k for k in per["FETCH_SIZE"] if k[0].startswith("copy_probe_kernel")]
+    if not copy_key:
+        raise SystemExit("the copy probe is missing from the counter run")
+    ck = copy_key[0]
+    copy_bytes = 4 << 30
+    f_scale = copy_bytes / (per["FETCH_SIZE"][ck] * 1024)
+    w_scale = copy_bytes / (per["WRITE_SIZE"][ck] * 1024)
+    out = [f"# {title}", ""] + [f"command: {c}" for c in cmds] + [
+        "",
+        f"Copy probe ({ck[0]}, grid {ck[1]}): {copy_bytes} bytes read and written per launch;",
+        f"FETCH_SIZE reads {per['FETCH_SIZE'][ck]:.0f} KiB, WRITE_SIZE "
+        f"{per['WRITE_SIZE'][ck]:.0f} KiB -> scale factors {f_scale:.4f} (fetch), "
+        f"{w_scale:.4f} (write).",
+        "",
+        "Scaled HBM bytes per launch (mean over launches), largest fetchers first:",
+        "",
+        f"{'kernel':44s} {'grid':>10s} {'fetch_KiB':>12s} {'write_KiB':>11s} "
+        f"{'fetch_bytes':>13s} {'write_bytes':>12s}"]
+    keys = sorted(per["FETCH_SIZE"], key=lambda k: -per["FETCH_SIZE"][k])[:top]
+    lines = []
+    for k in keys:
+        fk, wk = per["FETCH_SIZE"][k], per["WRITE_SIZE"].get(k, 0.0)
+        fb, wb = fk * 1024 * f_scale, wk * 1024 * w_scale
+        out.append(f"{k[0][:44]:44s} {k[1]:>10s} {fk:12.0f} {wk:11.0f} {fb:13.0f} {wb:12.0f}")
+        lines.append(f"TRAFFIC kernel={k[0].replace(' ', '')} grid={k[1]} fetch_bytes={fb:.0f} "
+                     f"write_bytes={wb:.0f}")
+    out += ["", f"Algorithmic bytes per launch: {algorithmic}", "",
+            f"source_sha256: {kernel_source_sha()}",
+            "(sha256 over " + ", ".join(KERNEL_SOURCES) + "; bench.py reports the traffic",
+            "only while these sources are unchanged)", ""] + lines
+    return "\n".join(out)
+
+
 def cpu_baseline(shape, ctx_lens, seed):
     """The oracle (float32) on the host: one decode step of one layer for the
     whole batch, scaled by the stage's 20 layers (every layer costs the same)."""
@@ -131,9 +301,12 @@ def cpu_baseline(shape, ctx_lens, seed):
             for i, c in enumerate(ctx_lens)]
     x = synth.hidden_states(seed, 9, B, shape.hidden)
     O.stage_forward(cfg, [w], x[:2], seqs[:2], kv, dtype=np.float32)  # warm caches
-    t0 = time.perf_counter()
-    O.stage_forward(cfg, [w], x, seqs, kv, dtype=np.float32)
-    dt = time.perf_counter() - t0
+    reps, t0 = 0, time.perf_counter()
+    while reps < 40 and (reps == 0 or time.perf_counter() - t0 < 10.0):
+        O.stage_forward(cfg, [w], x, seqs, kv, dtype=np.float32)
+        reps += 1
+    total = time.perf_counter() - t0
+    dt = total / reps
     try:
         from threadpoolctl import threadpool_info
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
@@ -142,7 +315,8 @@ def cpu_baseline(shape, ctx_lens, seed):
     step_s = dt * 20
     return {"value": B / step_s, "unit": "tok/s", "cores": int(cores), "kind": "oracle",
             "sample": f"one decode step of one layer, batch {B} (contexts as the workload), "
-                      f"float32, {dt:.2f} s, scaled x20 layers"}
+                      f"float32, repeated {reps}x ({total:.1f} s, {dt:.2f} s each), "
+                      f"scaled x20 layers"}
 
 
 def main():
@@ -161,7 +335,25 @@ def main():
                     choices=["l70-decode", "q32-mixed", "l70-full"],
                     help="l70-decode (default: the metric's workload, plus the chunked prefill "
                          "of the same stage); q32-mixed and l70-full print their own line")
+    ap.add_argument("--summarize-trace", metavar="DIR",
+                    help="print a summary of a rocprofv3 kernel trace under DIR and exit")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="print HBM traffic per launch from FETCH_SIZE / WRITE_SIZE runs and exit")
+    ap.add_argument("--summary-title", default="")
+    ap.add_argument("--summary-cmd", action="append", default=[])
     args = ap.parse_args()
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace, args.summary_title,
+                              " ; ".join(args.summary_cmd)))
+        return
+    if args.summarize_pmc:
+        from paper_2606_18600_amd import synth
+        sh = synth.LLAMA70B
+        alg = (f"decode gate-up + SwiGLU (M=64, N={2 * sh.ffn}, K={sh.hidden}) "
+               f"{gate_up_swiglu_bytes(sh, 64)} bytes")
+        print(summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.summary_title,
+                            args.summary_cmd, alg))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the stage runs on a single MI355X and this build "
               f"has no multi-GPU path (asked for --gpus {args.gpus}).", file=sys.stderr)
@@ -227,17 +419,18 @@ def main():
         st.decode(ctx0 + i, dec_bt, xs[i], out, stream=sp)
         i += 1
     torch.cuda.synchronize()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
     ctx_timed = []
-    e0.record(stream)
-    for _ in range(K):
+    ev[0].record(stream)
+    for k in range(K):
         st.decode(ctx0 + i, dec_bt, xs[i], out, stream=sp)
+        ev[k + 1].record(stream)
         ctx_timed.append(ctx0 + i)
         i += 1
-    e1.record(stream)
     torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / K
+    ms = ev[0].elapsed_time(ev[K]) / K
+    step_ms = [ev[k].elapsed_time(ev[k + 1]) for k in range(K)]
+    e0, e1 = ev[0], ev[K]
     assert torch.isfinite(out.float()).all(), "non-finite stage output"
     dec_tok_s = B / (ms / 1e3)
     step_bytes = float(np.mean([decode_step_bytes(shape, nL, c) for c in ctx_timed]))
@@ -254,11 +447,12 @@ def main():
     ops = {S.OP_NAMES[j]: {"ms_per_step": op_ms[j] / K, "launches_per_step": op_n[j] / K}
            for j in range(len(op_ms))}
     gu_avg_ms = op_ms[S.OP_NAMES.index("gate_up")] / op_n[S.OP_NAMES.index("gate_up")]
-    gu_bytes = gemm_bytes(B, 2 * shape.ffn, shape.hidden, 4)
+    gu_bytes = gate_up_swiglu_bytes(shape, B)
     gu_gbs = gu_bytes / (gu_avg_ms / 1e3) / 1e9
     log(f"[bench] ops ms/step: " + ", ".join(f"{k}={v['ms_per_step']:.3f}" for k, v in ops.items()))
     log(f"[bench] gate_up split-K GEMM: {gu_avg_ms * 1e3:.1f} us/launch, {gu_gbs:.0f} GB/s")
 
+    gu_traffic, traffic_note = committed_traffic(GATE_UP_DECODE_KERNEL)
     result = {
         "metric": METRIC, "value": round(dec_tok_s, 1), "unit": "tok/s", "n_gpus": 1,
         "steps": K, "warmup": W, "ms_per_step": round(ms, 4), "higher_is_better": True,
@@ -270,14 +464,17 @@ def main():
                    "layers": nL, "batch": B, "hidden": shape.hidden, "block": 16},
         "roofline": {"bound": "hbm", "kernel": "gemm_skinny_bf16 (gate-up, split-K)",
                      "achieved": round(gu_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(gu_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(gu_gbs / HBM_PEAK_GBS, 4), "traffic": gu_traffic,
                      "bytes_per_launch": gu_bytes, "us_per_launch": round(gu_avg_ms * 1e3, 2)},
+        "step_ms_p50": round(float(np.percentile(step_ms, 50)), 4),
+        "step_ms_p90": round(float(np.percentile(step_ms, 90)), 4),
         "step_roofline": {"bound": "hbm", "algorithmic_bytes": step_bytes,
                           "roofline_ms": round(step_bytes / (HBM_PEAK_GBS * 1e9) * 1e3, 4),
                           "measured_ms": round(ms, 4),
                           "frac": round(step_bytes / (HBM_PEAK_GBS * 1e9) / (ms / 1e3), 4)},
         "ops_ms_per_step": {k: round(v["ms_per_step"], 4) for k, v in ops.items()},
     }
+    result["roofline"]["traffic_note"] = traffic_note
 
     if not args.no_prefill:
         pf_bt = torch.from_numpy(pf_bt_np).to(dev)
@@ -329,6 +526,14 @@ def main():
     st.close()
     del weights
     torch.cuda.empty_cache()
+
+    cal = calibrate(torch, S, stream)
+    cal["gate_up_frac_of_copy"] = round(gu_gbs / cal["copy_GBs"], 4)
+    cal["decode_step_frac_of_copy"] = round(step_bytes / (ms / 1e3) / 1e9 / cal["copy_GBs"], 4)
+    if "prefill" in result:
+        cal["prefill_frac_of_gemm_probe"] = round(result["prefill"]["tflops"] / cal["gemm_TFLOPs"], 4)
+    result["calibrated"] = cal
+    log(f"[bench] calibration: {cal}")
 
     if not args.no_cpu:
         log("[bench] timing the CPU oracle on a bounded sample")

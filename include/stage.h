@@ -37,7 +37,7 @@
  *    plane 1 holds V, both as whole MFMA operand fragments so that every
  *    load of the attention kernels is contiguous:
  *      K[o][d] at (d / 32) * 512 + (o + 16 * ((d % 32) / 8)) * 8 + d % 8
- *      V[o][d] at (d / 16) * 256 + (d % 16 + 16 * (o / 4)) * 4 + o % 4
+ *      V[o][d] at (d / 32) * 512 + (d % 16 + 16 * (o / 4)) * 8 + ((d / 16) % 2) * 4 + o % 4
  *    Block ids index the same blocks in every layer of the stage.
  *  - hidden_in / hidden_out: [T, hidden] in the mode dtype, rows packed
  *    sequence by sequence in batch order (for stage_step_mixed: all prefill
@@ -221,6 +221,14 @@ stage_status stage_set_op_timing(stage_t* st, int32_t enable);
  * read; then reset the counters. ms and launches have STAGE_OP_COUNT
  * entries. */
 stage_status stage_read_op_times(stage_t* st, double* ms, int64_t* launches);
+
+/* Enqueue a plain streaming copy of `bytes` from device buffer src to device
+ * buffer dst on `stream`: the known-size reference kernel against which
+ * bandwidth and the hardware traffic counters (FETCH_SIZE, WRITE_SIZE) of
+ * the stage kernels are calibrated. Not part of the forward pass. bytes and
+ * both pointers must be multiples of 16 and the buffers must not overlap
+ * (STAGE_ERR_INVALID_ARG otherwise). */
+stage_status stage_copy_probe(const void* src, void* dst, size_t bytes, void* stream);
 
 #ifdef __cplusplus
 }

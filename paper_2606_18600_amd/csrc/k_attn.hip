@@ -35,6 +35,19 @@ __device__ __forceinline__ const int32_t* seq_table(const SegTables& t, int seq)
                        : t.bt1 + (size_t)(seq - t.nseq0) * t.stride1;
 }
 
+// Block ids of a wave's key range are read 64 at a time into one VGPR (lane
+// i holds entry w + i) and taken back with v_readlane. A scalar load of each
+// entry inside the key loop stalls the loop on every scalar-cache miss before
+// the next block's loads can be issued; a conditional refill inside the loop
+// makes the compiler wait for all outstanding loads at every readlane. So
+// the key loop runs per window: refill, one wait, then the ping-pong over
+// the window's blocks.
+__device__ __forceinline__ int fill_window(const int32_t* bt, int w, int we, int lane) {
+  const int ids = w + lane < we ? bt[w + lane] : 0;
+  __builtin_amdgcn_s_waitcnt(0);
+  return ids;
+}
+
 // K fragments of one 16-token block (kv_k_offset layout): fragment j, lane l
 // = token l%16, d = j*32 + (l/16)*8 .. +7; each load reads 1 KB contiguously.
 template <int D>
@@ -46,20 +59,52 @@ struct KFrag {
 #pragma unroll
     for (int j = 0; j < NJ; ++j) v[j] = ldg128(p + j * 512);
   }
-};
-
-// V^T fragments of one block (kv_v_offset layout): for d tile dt, lane l
-// holds d = dt*16 + l%16, tokens (l/16)*4 .. +3; each load reads 512 B.
-template <int D>
-struct VFrag {
-  static constexpr int NT = D / 16;
-  u32x2_t v[NT];
-  __device__ __forceinline__ void load(const bf16_t* vplane, int lane) {
-    const bf16_t* p = vplane + lane * 4;
+  // streaming (non-temporal) variant for data read once
+  __device__ __forceinline__ void load_nt(const bf16_t* kplane, int lane) {
+    const bf16_t* p = kplane + lane * 8;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) v[t] = ldg64(p + t * 256);
+    for (int j = 0; j < NJ; ++j) v[j] = __builtin_nontemporal_load((const u32x4_t*)(p + j * 512));
   }
 };
+
+// V^T fragments of one block (kv_v_offset layout): 1 KB fragment p, lane l
+// holds d = 32p + l%16 (words 0-1) and d = 32p + 16 + l%16 (words 2-3), each
+// for tokens (l/16)*4 .. +3.
+template <int D>
+struct VFrag {
+  static constexpr int NP = D / 32;
+  u32x4_t v[NP];
+  __device__ __forceinline__ void load(const bf16_t* vplane, int lane) {
+    const bf16_t* p = vplane + lane * 8;
+#pragma unroll
+    for (int j = 0; j < NP; ++j) v[j] = ldg128(p + j * 512);
+  }
+  __device__ __forceinline__ void load_nt(const bf16_t* vplane, int lane) {
+    const bf16_t* p = vplane + lane * 8;
+#pragma unroll
+    for (int j = 0; j < NP; ++j) v[j] = __builtin_nontemporal_load((const u32x4_t*)(p + j * 512));
+  }
+  // A operand of d tile t (16 d values)
+  __device__ __forceinline__ u32x2_t tile(int t) const {
+    const u32x4_t& w = v[t >> 1];
+    return (t & 1) ? u32x2_t{w[2], w[3]} : u32x2_t{w[0], w[1]};
+  }
+};
+
+// Lanes l, l^16, l^32 and l^48 hold the same row of a 16x16 C tile; combine
+// their values with the gfx950 lane swaps (VALU only, no LDS round trip).
+__device__ __forceinline__ float row4_max(float x) {
+  auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float row4_sum(float x) {
+  auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
 
 // Online-softmax state of the row owned by this lane (row l%16 of a tile).
 struct RowState {
@@ -71,9 +116,7 @@ struct RowState {
 template <int D>
 __device__ __forceinline__ void softmax_pv(f32x4_t s, RowState& st, f32x4_t* oacc,
                                            const VFrag<D>& vf) {
-  float bm = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
-  bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
-  bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
+  const float bm = row4_max(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])));
   const float mn = fmaxf(st.m, bm);
   // A row can only be fully masked in a block after an earlier block gave it
   // a finite max, so mn is finite here.
@@ -81,9 +124,7 @@ __device__ __forceinline__ void softmax_pv(f32x4_t s, RowState& st, f32x4_t* oac
   float p[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) p[r] = exp2f(s[r] - mn);
-  float ps = p[0] + p[1] + p[2] + p[3];
-  ps += __shfl_xor(ps, 16, 64);
-  ps += __shfl_xor(ps, 32, 64);
+  const float ps = row4_sum(p[0] + p[1] + p[2] + p[3]);
   st.l = st.l * alpha + ps;
   st.m = mn;
   u32x2_t pb;
@@ -92,7 +133,7 @@ __device__ __forceinline__ void softmax_pv(f32x4_t s, RowState& st, f32x4_t* oac
 #pragma unroll
   for (int t = 0; t < D / 16; ++t) {
     oacc[t] *= alpha;
-    oacc[t] = mfma16x16x16(vf.v[t], pb, oacc[t]);
+    oacc[t] = mfma16x16x16(vf.tile(t), pb, oacc[t]);
   }
 }
 
@@ -133,14 +174,18 @@ __global__ __launch_bounds__(256) void attn_decode_bf16(const bf16_t* __restrict
   const int b0 = it.k0 / kBlock, b1 = (it.k1 + kBlock - 1) / kBlock;
   // Two register sets in ping-pong (no copies between them), so a block's
   // loads stay in flight while the previous block is processed; the
-  // prefetch index is clamped to the last block and its data is unused.
+  // prefetch index is clamped to the window's last block and its data is
+  // unused.
   KFrag<D> kx, ky;
   VFrag<D> vx, vy;
+  int w = 0, we = 0, ids = 0;
   auto load = [&](KFrag<D>& kf, VFrag<D>& vf, int b) {
-    b = b < b1 ? b : b1 - 1;
-    const bf16_t* kp = kv + ((size_t)bt[b] * n_kv + kvh) * head_stride;
-    kf.load(kp, lane);
-    vf.load(kp + plane, lane);
+    b = b < we ? b : we - 1;
+    const bf16_t* kp = kv + ((size_t)__builtin_amdgcn_readlane(ids, b - w) * n_kv + kvh) * head_stride;
+    // each (block, kv head) plane is read by exactly one wave of the step:
+    // stream it (plain loads that allocate in the caches were ~15% slower)
+    kf.load_nt(kp, lane);
+    vf.load_nt(kp + plane, lane);
   };
   auto step = [&](const KFrag<D>& kf, const VFrag<D>& vf, int b) {
     f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -153,19 +198,23 @@ __global__ __launch_bounds__(256) void attn_decode_bf16(const bf16_t* __restrict
     }
     softmax_pv<D>(s, st, oacc, vf);
   };
-  load(kx, vx, b0);
-  int b = b0;
-  for (; b + 1 < b1; b += 2) {
-    load(ky, vy, b + 1);
-    __builtin_amdgcn_sched_barrier(0);
-    step(kx, vx, b);
-    __builtin_amdgcn_sched_barrier(0);
-    load(kx, vx, b + 2);
-    __builtin_amdgcn_sched_barrier(0);
-    step(ky, vy, b + 1);
-    __builtin_amdgcn_sched_barrier(0);
+  for (w = b0; w < b1; w += 64) {
+    we = min(w + 64, b1);
+    ids = fill_window(bt, w, we, lane);
+    load(kx, vx, w);
+    int b = w;
+    for (; b + 1 < we; b += 2) {
+      load(ky, vy, b + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      step(kx, vx, b);
+      __builtin_amdgcn_sched_barrier(0);
+      load(kx, vx, b + 2);
+      __builtin_amdgcn_sched_barrier(0);
+      step(ky, vy, b + 1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (b < we) step(kx, vx, b);
   }
-  if (b < b1) step(kx, vx, b);
 
   if (!row_ok) return;
   const size_t ob = ((size_t)blockIdx.x * n_q + kvh * G + row);
@@ -279,9 +328,10 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(const bf16_t* __restric
   const int nb = (kend + kBlock - 1) / kBlock;
   KFrag<D> kx, ky;
   VFrag<D> vx, vy;
+  int w = 0, we = 0, ids = 0;
   auto load = [&](KFrag<D>& kf, VFrag<D>& vf, int b) {
-    b = b < nb ? b : nb - 1;
-    const bf16_t* kp = kv + ((size_t)bt[b] * n_kv + kvh) * head_stride;
+    b = b < we ? b : we - 1;
+    const bf16_t* kp = kv + ((size_t)__builtin_amdgcn_readlane(ids, b - w) * n_kv + kvh) * head_stride;
     kf.load(kp, lane);
     vf.load(kp + plane, lane);
   };
@@ -299,19 +349,23 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(const bf16_t* __restric
       softmax_pv<D>(s, st[i], oacc[i], vf);
     }
   };
-  load(kx, vx, 0);
-  int b = 0;
-  for (; b + 1 < nb; b += 2) {
-    load(ky, vy, b + 1);
-    __builtin_amdgcn_sched_barrier(0);
-    step(kx, vx, b);
-    __builtin_amdgcn_sched_barrier(0);
-    load(kx, vx, b + 2);
-    __builtin_amdgcn_sched_barrier(0);
-    step(ky, vy, b + 1);
-    __builtin_amdgcn_sched_barrier(0);
+  for (w = 0; w < nb; w += 64) {
+    we = min(w + 64, nb);
+    ids = fill_window(bt, w, we, lane);
+    load(kx, vx, w);
+    int b = w;
+    for (; b + 1 < we; b += 2) {
+      load(ky, vy, b + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      step(kx, vx, b);
+      __builtin_amdgcn_sched_barrier(0);
+      load(kx, vx, b + 2);
+      __builtin_amdgcn_sched_barrier(0);
+      step(ky, vy, b + 1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (b < we) step(kx, vx, b);
   }
-  if (b < nb) step(kx, vx, b);
 
 #pragma unroll
   for (int i = 0; i < RT; ++i) {

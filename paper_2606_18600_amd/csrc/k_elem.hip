@@ -269,6 +269,14 @@ inline int grid_for(size_t n, int threads) {
 
 }  // namespace
 
+// Plain streaming copy of n16 16-byte words (grid-stride, coalesced): the
+// known-size reference for bandwidth and hardware traffic counters.
+__global__ __launch_bounds__(256) void copy_probe_kernel(const u32x4_t* __restrict__ src,
+                                                         u32x4_t* __restrict__ dst, size_t n16) {
+  const size_t stride = (size_t)gridDim.x * 256;
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += stride) dst[i] = src[i];
+}
+
 hipError_t embed_norm(DType dt, const void* hidden_in, float* x, void* h, const void* gain, int T,
                       int H, float eps, hipStream_t s) {
   if (T == 0) return hipSuccess;
@@ -333,6 +341,14 @@ hipError_t swiglu_reduce_bf16(Partials gu, uint16_t* m, int T, int F, hipStream_
   const size_t n4 = (size_t)T * F / 4;
   if (n4 == 0) return hipSuccess;
   swiglu_reduce_kernel<<<grid_for(n4, 256), 256, 0, s>>>(gu.p, gu.splits, T, F, m);
+  return hipGetLastError();
+}
+
+hipError_t copy_probe(const void* src, void* dst, size_t bytes, hipStream_t s) {
+  const size_t n16 = bytes / 16;
+  if (n16 == 0) return hipSuccess;
+  const size_t blocks = std::min<size_t>((n16 + 255) / 256, 8192);
+  copy_probe_kernel<<<(unsigned)blocks, 256, 0, s>>>((const u32x4_t*)src, (u32x4_t*)dst, n16);
   return hipGetLastError();
 }
 

@@ -53,20 +53,50 @@ constexpr int SK_WAVES = 4;
 
 enum SkinnyEpi { SK_PARTIAL = 0, SK_SWIGLU = 1 };
 
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// s_waitcnt immediate that waits until at most n vector-memory operations of
+// this wave are outstanding (vmcnt is split over bits 3:0 and 15:14; expcnt
+// and lgkmcnt are left at their maxima, i.e. not waited for).
+constexpr int vmcnt_at_most(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+// Block = 4 waves on 4 adjacent 64-column weight groups over the same K
+// range. Per 64-wide k step each wave streams its group's 8 W fragments into
+// registers (two register sets in ping-pong), while the step's 2*MT A
+// fragments, which all four waves need, are copied once per block straight
+// into a 3-slot LDS ring (each wave copies a quarter). Streaming the shared
+// A through L2 for every wave costs as many bytes as W itself and was the
+// limit of this kernel. Every wave issues the same number of loads per step,
+// so one vmcnt bound serves all of them.
 template <int MT, int EPI>
 __global__ __launch_bounds__(SK_WAVES * 64) void gemm_skinny_bf16(const bf16_t* __restrict__ A,
                                                                   const bf16_t* __restrict__ W,
                                                                   int M, int N, int K, int kb_len,
                                                                   void* __restrict__ out) {
+  constexpr int NA = (2 * MT + SK_WAVES - 1) / SK_WAVES;  // A copies per wave and step
+  constexpr int SLOT = SK_WAVES * NA;                     // fragments per ring slot
+  constexpr int WAIT = vmcnt_at_most(8 + NA);             // all but the newest step's loads
+  __shared__ u32x4_t As[3][SLOT * 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int g = blockIdx.x * SK_WAVES + wave;
-  if (g * 64 >= N) return;  // no barriers in this kernel
+  const int G = N / 64;
+  const int g_raw = blockIdx.x * SK_WAVES + wave;
+  const bool live = g_raw < G;
+  // a wave past the last group streams the last group again (and stores
+  // nothing) so that it keeps the block's load counts and barriers
+  const int g = live ? g_raw : G - 1;
   const int kbeg = blockIdx.y * kb_len;
   const int iters = (min(kb_len, K - kbeg)) / 64;  // >= 1: the grid covers K exactly
   const int r16 = lane & 15;
   const int KT = K / 32;
   const bf16_t* wp = W + ((size_t)g * KT + kbeg / 32) * 4 * 512 + lane * 8;
-  const bf16_t* ap = A + (size_t)(kbeg / 32) * 512 + lane * 8;
+  // A fragment f = wave + 4u of a step is (m-tile f / 2, k half f % 2); copies
+  // past 2*MT re-read the last fragment into slots nobody reads
+  const bf16_t* asrc[NA];
+#pragma unroll
+  for (int u = 0; u < NA; ++u) {
+    const int f = min(wave + SK_WAVES * u, 2 * MT - 1);
+    asrc[u] = A + ((size_t)(f / 2) * KT + kbeg / 32 + f % 2) * 512 + lane * 8;
+  }
 
   f32x4_t acc[MT][4];
 #pragma unroll
@@ -74,46 +104,63 @@ __global__ __launch_bounds__(SK_WAVES * 64) void gemm_skinny_bf16(const bf16_t* 
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  u32x4_t wx[2][4], ax[MT][2], wy[2][4], ay[MT][2];
-  // Loads of k step t (clamped to the last step so that the prefetch past the
-  // end stays in bounds; its data is never used).
-  auto load = [&](u32x4_t (&w)[2][4], u32x4_t (&a)[MT][2], int t) {
+  u32x4_t wx[2][4], wy[2][4];
+  // Loads of k step t. Past the end the index is clamped to the last step:
+  // the data is never used, and a copy into the last step's slot writes the
+  // bytes that slot already holds.
+  auto load = [&](u32x4_t (&w)[2][4], int t) {
     t = t < iters ? t : iters - 1;
+    const int slot = t % 3;
+#pragma unroll
+    for (int u = 0; u < NA; ++u)
+      __builtin_amdgcn_global_load_lds((const void*)(asrc[u] + (size_t)t * 2 * 512),
+                                       (lds_ptr_t)&As[slot][(wave + SK_WAVES * u) * 64], 16, 0, 0);
     const bf16_t* q = wp + (size_t)t * 8 * 512;
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         w[h][j] = __builtin_nontemporal_load((const u32x4_t*)(q + (h * 4 + j) * 512));
-#pragma unroll
-    for (int i = 0; i < MT; ++i)
-#pragma unroll
-      for (int h = 0; h < 2; ++h) a[i][h] = ldg128(ap + ((size_t)i * KT + 2 * t + h) * 512);
   };
-  auto compute = [&](const u32x4_t (&w)[2][4], const u32x4_t (&a)[MT][2]) {
+  auto compute = [&](const u32x4_t (&w)[2][4], int t) {
+    const int slot = t % 3;
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int i = 0; i < MT; ++i)
+      for (int i = 0; i < MT; ++i) {
+        const u32x4_t a = As[slot][(i * 2 + h) * 64 + lane];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mfma16x16x32(a[i][h], w[h][j], acc[i][j]);
+        for (int j = 0; j < 4; ++j) acc[i][j] = mfma16x16x32(a, w[h][j], acc[i][j]);
+      }
   };
-  // Ping-pong over two register sets; the scheduling barriers keep each
-  // step's loads issued ahead of the previous step's MFMAs, so the waits only
-  // cover the older loads.
-  load(wx, ax, 0);
+  // Step t's loads are complete once only step t+1's are outstanding; the
+  // barrier then publishes every wave's A copies. Slot (t+2) % 3 is refilled
+  // only after the barrier of step t, which every wave reaches after its
+  // reads of step t-1 (the slot's previous contents).
+  load(wx, 0);
   int t = 0;
   for (; t + 1 < iters; t += 2) {
-    load(wy, ay, t + 1);
+    load(wy, t + 1);
     __builtin_amdgcn_sched_barrier(0);
-    compute(wx, ax);
+    __builtin_amdgcn_s_waitcnt(WAIT);
+    __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    load(wx, ax, t + 2);
+    compute(wx, t);
     __builtin_amdgcn_sched_barrier(0);
-    compute(wy, ay);
+    load(wx, t + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(WAIT);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    compute(wy, t + 1);
     __builtin_amdgcn_sched_barrier(0);
   }
-  if (t < iters) compute(wx, ax);
+  if (t < iters) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_s_barrier();
+    compute(wx, t);
+  }
+  if (!live) return;
 
   // C layout of a 16x16 tile: lane l holds column l%16, rows (l/16)*4 + r.
   if (EPI == SK_PARTIAL) {
@@ -156,8 +203,6 @@ __global__ __launch_bounds__(SK_WAVES * 64) void gemm_skinny_bf16(const bf16_t* 
 // copies its share straight into LDS with global_load_lds_dwordx4 (lane l
 // lands at base + 16 l, which is the fragment's own lane order); two stages
 // alternate in LDS.
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
-
 template <int BMT, int BNG, int WM, int WN, int EPI>
 __global__ __launch_bounds__(WM * WN * 64) void gemm_tiled_bf16(const bf16_t* __restrict__ A,
                                                                const bf16_t* __restrict__ W,

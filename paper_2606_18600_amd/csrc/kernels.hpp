@@ -89,6 +89,8 @@ hipError_t swiglu_reduce_bf16(Partials gu, uint16_t* m, int T, int F, hipStream_
 // Pack a row-major bf16 [N, K] weight into the packed layout; gate_up_ffn > 0
 // marks the fused gate-up weight (N = 2 * gate_up_ffn).
 hipError_t pack_weight(const void* src, void* dst, int N, int K, int gate_up_ffn, hipStream_t s);
+// Plain device-to-device copy of `bytes` (a multiple of 16; 16-byte aligned).
+hipError_t copy_probe(const void* src, void* dst, size_t bytes, hipStream_t s);
 
 // GEMMs. gemm_skinny (bf16, M <= 128): packed A and W; writes `splits` fp32
 // partial planes [splits][M][N] into out, or with swiglu (splits == 1) the

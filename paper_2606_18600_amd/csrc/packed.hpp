@@ -47,10 +47,12 @@ __host__ __device__ inline int gate_up_source_row(int n, int F) {
 __host__ __device__ inline int kv_k_offset(int o, int d) {
   return (d >> 5) * 512 + (o + 16 * ((d & 31) >> 3)) * 8 + (d & 7);
 }
-// V plane: fragments of 16 d x 16 tokens (the A operand of O^T += V^T P^T);
-// lane l holds d = l % 16 of the fragment and tokens (l / 16) * 4 .. + 3.
+// V plane: the A operands of O^T += V^T P^T are 16 d x 16 tokens (lane l:
+// d = l % 16, tokens (l / 16) * 4 .. + 3, 8 bytes); two d tiles 2p, 2p + 1
+// are interleaved per lane so that one 16-byte load per lane (a 1 KB
+// fragment) fetches both: lane l holds tile 2p's 4 tokens, then tile 2p+1's.
 __host__ __device__ inline int kv_v_offset(int o, int d) {
-  return (d >> 4) * 256 + ((d & 15) + 16 * (o >> 2)) * 4 + (o & 3);
+  return (d >> 5) * 512 + ((d & 15) + 16 * (o >> 2)) * 8 + ((d >> 4) & 1) * 4 + (o & 3);
 }
 
 }  // namespace stage_k

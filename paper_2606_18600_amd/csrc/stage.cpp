@@ -67,7 +67,10 @@ struct stage {
   int skinny_rows = 0;  // steps with at most this many tokens use split-K GEMMs
   // K splits of the four split-K GEMMs (QKV, O, gate-up, down)
   int s_qkv = 1, s_o = 1, s_gu = 1, s_down = 1;
-  int attn_waves = 3072;  // decode attention waves to aim for (one round)
+  // decode attention waves to aim for: one resident round (the kernel runs
+  // two waves per SIMD, 2048 on the chip) with slack for per-sequence
+  // rounding of the split sizes
+  int attn_waves = 1600;
 
   // workspace
   Region r_x, r_h, r_qkv, r_q, r_attn, r_m, r_gu, r_part_x, r_part_o, r_part_ml, r_meta, r_cos,
@@ -510,7 +513,7 @@ stage_status stage_create(const stage_model_config* cfg, int32_t layer_begin, in
     st->s_o = skinny_splits(H, qw, waves);
     st->s_gu = skinny_splits(2 * F, H, waves);
     st->s_down = skinny_splits(H, F, waves);
-    st->attn_waves = std::max(64, env_int("STAGE_ATTN_WAVES", 3072));
+    st->attn_waves = std::max(64, env_int("STAGE_ATTN_WAVES", 1600));
   }
   if ((e = hipGetDevice(&st->device)) != hipSuccess) {
     delete st;
@@ -636,6 +639,18 @@ stage_status stage_pack_weight(const stage_model_config* cfg, stage_weight_kind 
   else
     e = pack_weight(src, dst, N, K, ffn, s);
   if (e != hipSuccess) return hip_fail("pack_weight", e);
+  return STAGE_OK;
+}
+
+stage_status stage_copy_probe(const void* src, void* dst, size_t bytes, void* stream) {
+  if (!src || !dst) return fail(STAGE_ERR_INVALID_ARG, "src/dst is NULL");
+  if (bytes % 16 != 0 || (uintptr_t)src % 16 != 0 || (uintptr_t)dst % 16 != 0)
+    return fail(STAGE_ERR_INVALID_ARG, "copy probe needs 16-byte aligned pointers and sizes");
+  const char* a = (const char*)src;
+  const char* b = (const char*)dst;
+  if (a < b + bytes && b < a + bytes) return fail(STAGE_ERR_INVALID_ARG, "copy probe buffers overlap");
+  hipError_t e = copy_probe(src, dst, bytes, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail("copy_probe", e);
   return STAGE_OK;
 }
 

@@ -175,7 +175,7 @@ def kv_plane_index(block: int, d: int):
     o = np.arange(block)[:, None]
     dd = np.arange(d)[None, :]
     k = (dd // 32) * 512 + (o + 16 * ((dd % 32) // 8)) * 8 + dd % 8
-    v = (dd // 16) * 256 + (dd % 16 + 16 * (o // 4)) * 4 + o % 4
+    v = (dd // 32) * 512 + (dd % 16 + 16 * (o // 4)) * 8 + ((dd // 16) % 2) * 4 + o % 4
     return k, v
 
 

@@ -25,6 +25,14 @@ def gemm_bytes(M: int, N: int, K: int, out_bytes: int) -> int:
     return N * K * 2 + M * K * 2 + M * N * out_bytes
 
 
+def gate_up_swiglu_bytes(shape, M: int) -> int:
+    """Algorithmic HBM bytes of one fused gate-up + SwiGLU launch over M rows:
+    the [2F, H] bf16 weight and the [M, H] bf16 input read once, the [M, F]
+    bf16 product m written once."""
+    F, H = shape.ffn, shape.hidden
+    return 2 * F * H * 2 + M * H * 2 + M * F * 2
+
+
 def linear_shapes(shape) -> Sequence[Tuple[int, int]]:
     """(N, K) of the four projections of a layer."""
     H, d, F = shape.hidden, shape.head_dim, shape.ffn

@@ -35,7 +35,7 @@ STAGE_OP_COUNT = len(OP_NAMES)
 EXPORTED = ("stage_create", "stage_workspace_bytes", "stage_bind_workspace", "stage_prefill",
             "stage_decode", "stage_step_mixed", "stage_destroy", "stage_last_error",
             "stage_validate_step", "stage_set_op_timing", "stage_read_op_times",
-            "stage_pack_weight")
+            "stage_pack_weight", "stage_copy_probe")
 
 STAGE_W_QKV = 0
 STAGE_W_O = 1
@@ -100,12 +100,14 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.stage_validate_step.argtypes = [ctypes.POINTER(stage_model_config), i32, i32,
                                         ctypes.POINTER(stage_batch), ctypes.POINTER(stage_batch)]
     lib.stage_pack_weight.argtypes = [ctypes.POINTER(stage_model_config), i32, P, P, P]
+    lib.stage_copy_probe.argtypes = [P, P, ctypes.c_size_t, P]
     lib.stage_set_op_timing.argtypes = [P, i32]
     lib.stage_read_op_times.argtypes = [P, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_int64)]
     for name in ("stage_create", "stage_bind_workspace", "stage_prefill", "stage_decode",
                  "stage_step_mixed", "stage_destroy", "stage_validate_step",
-                 "stage_set_op_timing", "stage_read_op_times", "stage_pack_weight"):
+                 "stage_set_op_timing", "stage_read_op_times", "stage_pack_weight",
+                 "stage_copy_probe"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -186,6 +188,10 @@ def stage_validate_step(cfg: stage_model_config, max_tokens: int, max_seqs: int,
 def stage_pack_weight(cfg: stage_model_config, kind: int, src: int, dst: int,
                       stream: int = 0) -> None:
     _check(load_library().stage_pack_weight(ctypes.byref(cfg), kind, src, dst, stream))
+
+
+def stage_copy_probe(src: int, dst: int, nbytes: int, stream: int = 0) -> None:
+    _check(load_library().stage_copy_probe(src, dst, nbytes, stream))
 
 
 def stage_set_op_timing(st: int, enable: bool) -> None:

@@ -140,3 +140,16 @@ def test_null_stage_calls_fail_cleanly():
     assert lib.stage_prefill(None, None, None, None, None) == S.STAGE_ERR_INVALID_ARG
     assert lib.stage_destroy(None) == S.STAGE_OK
     assert lib.stage_workspace_bytes(None) == 0
+
+
+@pytest.mark.parametrize("src,dst,nbytes", [
+    (0, 0x2000, 64),            # NULL source
+    (0x1000, 0, 64),            # NULL destination
+    (0x1000, 0x2000, 40),       # size not a multiple of 16
+    (0x1008, 0x2000, 64),       # misaligned source
+    (0x1000, 0x1020, 64),       # overlapping buffers
+])
+def test_copy_probe_rejects_bad_arguments_on_the_host(src, dst, nbytes):
+    lib = _lib()
+    assert lib.stage_copy_probe(src, dst, nbytes, None) == S.STAGE_ERR_INVALID_ARG
+    assert S.stage_last_error()

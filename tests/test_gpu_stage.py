@@ -287,3 +287,18 @@ def test_pack_weight_layout(kind, shape_fn):
     else:
         expect = a
     np.testing.assert_array_equal(p[pos], np.broadcast_to(expect, (N, K)))
+
+
+@pytest.mark.parametrize("nbytes", [16, 4096, 3 * 1024 * 1024 + 48, 64 << 20])
+def test_copy_probe_copies_exactly(nbytes):
+    """The calibration copy moves every byte (grid-stride tail included)."""
+    log(f"[test] copy probe {nbytes} bytes")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(nbytes)
+    src = torch.randint(0, 1 << 30, (nbytes // 4,), dtype=torch.int32, device="cuda",
+                        generator=g)
+    dst = torch.full((nbytes // 4 + 4,), -7, dtype=torch.int32, device="cuda")
+    S.stage_copy_probe(src.data_ptr(), dst.data_ptr(), nbytes)
+    torch.cuda.synchronize()
+    assert torch.equal(dst[: nbytes // 4], src)
+    assert (dst[nbytes // 4:] == -7).all()      # nothing written past the end

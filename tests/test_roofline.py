@@ -57,3 +57,9 @@ def test_step_roofline_prefill_is_flops_over_peak():
     lin = 2.0 * 2048 * 855_638_016
     attn = 4.0 * 128 * 64 * (2048 * 2049 / 2)
     assert t == pytest.approx(20 * (lin + attn) / 2.5e15 * 1e3, rel=1e-9)
+
+
+def test_gate_up_swiglu_bytes_of_the_llama70b_decode_launch():
+    # [57344, 8192] bf16 weight + [64, 8192] bf16 input + [64, 28672] bf16 product
+    assert R.gate_up_swiglu_bytes(synth.LLAMA70B, 64) == 939524096 + 1048576 + 3670016
+
