@@ -15,6 +15,8 @@
 //   copied HBM -> LDS with direct loads, 64-wide k steps double-buffered;
 //   epilogues: fp32 store, residual add, SwiGLU.
 // * gemm_tiled_f32: plain fp32 SIMT tiles for the fp32 mode (row-major).
+#include <algorithm>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "packed.hpp"
@@ -393,10 +395,10 @@ int skinny_kb_len(int K, int splits) {
   return (kb + 63) / 64 * 64;
 }
 
-int skinny_splits(int N, int K, int target_waves) {
-  const int groups = N / 64;
-  int s = 1;
-  while (s < 8 && groups * s * 2 <= target_waves && K / (s * 2) >= 64) s *= 2;
+int skinny_splits(int N, int K, int target_blocks) {
+  const int col_blocks = (N / 64 + SK_WAVES - 1) / SK_WAVES;
+  int s = std::max(1, target_blocks / col_blocks);
+  s = std::min(s, std::min(kSkinnyMaxSplits, K / 64));
   // the number of K ranges actually launched after rounding the range up
   const int kb = skinny_kb_len(K, s);
   return (K + kb - 1) / kb;

@@ -95,7 +95,11 @@ hipError_t copy_probe(const void* src, void* dst, size_t bytes, hipStream_t s);
 // GEMMs. gemm_skinny (bf16, M <= 128): packed A and W; writes `splits` fp32
 // partial planes [splits][M][N] into out, or with swiglu (splits == 1) the
 // SwiGLU product in the packed activation layout [M, N/2].
-int skinny_splits(int N, int K, int target_waves);
+// Split-K partial planes a consumer (RMSNorm, RoPE, SwiGLU) accepts.
+constexpr int kSkinnyMaxSplits = 8;
+// K splits for an [M <= 128] x [N, K] decode GEMM: as many as keep the launch
+// at <= target_blocks blocks of 4 waves (at most kSkinnyMaxSplits).
+int skinny_splits(int N, int K, int target_blocks);
 int skinny_kb_len(int K, int splits);
 hipError_t gemm_skinny(const void* A, const void* W, int M, int N, int K, int splits, bool swiglu,
                        void* out, hipStream_t s);

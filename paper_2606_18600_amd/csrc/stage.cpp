@@ -504,20 +504,27 @@ stage_status stage_create(const stage_model_config* cfg, int32_t layer_begin, in
   st->esize = cfg->dtype == STAGE_BF16 ? 2 : 4;
   st->kv_layer_bytes = (size_t)num_blocks * cfg->n_kv_heads * 2 * kBlock * cfg->head_dim * st->esize;
   st->skinny_rows = cfg->dtype == STAGE_BF16 ? std::min(kSkinnyMaxRows, max_tokens) : 0;
-  {
-    // about one wave per SIMD (256 CUs x 4) for each split-K GEMM
-    const int waves = std::max(64, env_int("STAGE_SKINNY_WAVES", 1024));
-    const int H = cfg->hidden, F = cfg->ffn, qw = cfg->n_q_heads * cfg->head_dim;
-    const int qkvw = (cfg->n_q_heads + 2 * cfg->n_kv_heads) * cfg->head_dim;
-    st->s_qkv = skinny_splits(qkvw, H, waves);
-    st->s_o = skinny_splits(H, qw, waves);
-    st->s_gu = skinny_splits(2 * F, H, waves);
-    st->s_down = skinny_splits(H, F, waves);
-    st->attn_waves = std::max(64, env_int("STAGE_ATTN_WAVES", 1600));
-  }
   if ((e = hipGetDevice(&st->device)) != hipSuccess) {
     delete st;
     return hip_fail("hipGetDevice", e);
+  }
+  {
+    // Split-K GEMM blocks stream at a roughly fixed rate per CU, so each
+    // GEMM gets as many K splits as fill ~90% of the CUs with one block
+    // each (more blocks than CUs double up on some CUs and stretch the tail).
+    int cus = 256;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, st->device) !=
+            hipSuccess ||
+        cus <= 0)
+      cus = 256;
+    const int blocks = std::max(1, env_int("STAGE_SKINNY_BLOCKS", cus * 9 / 10));
+    const int H = cfg->hidden, F = cfg->ffn, qw = cfg->n_q_heads * cfg->head_dim;
+    const int qkvw = (cfg->n_q_heads + 2 * cfg->n_kv_heads) * cfg->head_dim;
+    st->s_qkv = skinny_splits(qkvw, H, blocks);
+    st->s_o = skinny_splits(H, qw, blocks);
+    st->s_gu = skinny_splits(2 * F, H, blocks);
+    st->s_down = skinny_splits(H, F, blocks);
+    st->attn_waves = std::max(64, env_int("STAGE_ATTN_WAVES", 1600));
   }
   plan_workspace(st);
   for (int i = 0; i < kRing; ++i) {
