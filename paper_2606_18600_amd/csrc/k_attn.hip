@@ -280,41 +280,59 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const float* __restrict
   }
 }
 
-// Prefill: one wave per (item, kv head); RT tiles of 16 rows, row r of the
-// wave is position r / G and head kvh*G + r % G.
+// Prefill: one workgroup of kPfWaves waves per (item, kv head). Row r of
+// the workgroup (r < kPfWaves * RT * 16) is query position r / G of the item
+// and head kvh*G + r % G; wave w owns row tiles w*RT .. w*RT + RT - 1. Keys
+// run in stages of BPS 16-token blocks: each stage's K and V fragments are
+// copied once into LDS (direct loads, two buffers) and read by all waves, so
+// a key is fetched once per workgroup instead of once per 16 rows. Scores
+// of a whole stage are reduced together; the running maximum is only moved
+// (and the accumulators rescaled) when it grows by more than 2^8, so P stays
+// below 256 and the rescale is rare after the first stage.
+constexpr int kPfWaves = 4;
+constexpr int kPfBPS = 4;
+constexpr float kLazyRescale = 8.0f;  // log2 units
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
 template <int D, int RT>
-__global__ __launch_bounds__(256) void attn_prefill_bf16(const bf16_t* __restrict__ q,
-                                                         const bf16_t* __restrict__ kv, int n_kv,
-                                                         SegTables tabs,
-                                                         const PrefillItem* __restrict__ items,
-                                                         int n_q, bf16_t* __restrict__ out) {
-  const int lane = threadIdx.x & 63;
-  const int kvh = blockIdx.y * 4 + (threadIdx.x >> 6);
-  if (kvh >= n_kv) return;
+__global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_bf16(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ kv, int n_kv, SegTables tabs,
+    const PrefillItem* __restrict__ items, int n_q, bf16_t* __restrict__ out) {
+  constexpr int BPS = kPfBPS;
+  constexpr int NJ = D / 32;           // K fragments per block (and V fragments)
+  constexpr int FR = 2 * NJ;           // fragments per block
+  constexpr int SF = BPS * FR;         // fragments per stage
+  constexpr int PER = SF / kPfWaves;   // fragment copies per wave and stage
+  static_assert(SF % kPfWaves == 0, "stage split");
+  __shared__ u32x4_t lds[2][SF * 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int kvh = blockIdx.y;
   const PrefillItem it = items[blockIdx.x];
   const int G = n_q / n_kv;
   const float scale = kLog2e / sqrtf((float)D);
-  constexpr int NJ = D / 32;
 
   int rpos[RT];  // position of this lane's row in each tile
   bool rok[RT];
   u32x4_t qf[RT][NJ];
 #pragma unroll
   for (int i = 0; i < RT; ++i) {
-    const int r = i * 16 + (lane & 15);
+    const int r = (wave * RT + i) * 16 + (lane & 15);
     const int pi = r / G;
     rok[i] = pi < it.npos;
     const int pc = rok[i] ? pi : it.npos - 1;
     rpos[i] = it.p0 + pc;
-    const bf16_t* qp = q + ((size_t)(it.t0 + pc) * n_q + kvh * G + r % G) * D +
-                       (lane >> 4) * 8;
+    const bf16_t* qp = q + ((size_t)(it.t0 + pc) * n_q + kvh * G + r % G) * D + (lane >> 4) * 8;
 #pragma unroll
     for (int j = 0; j < NJ; ++j) qf[i][j] = ldg128(qp + j * 32);
   }
 
   const int32_t* bt = seq_table(tabs, it.seq);
   const size_t plane = (size_t)kBlock * D;
-  const size_t head_stride = 2 * plane;
+  const int kend = it.p0 + it.npos;  // keys [0, kend)
+  const int nb = (kend + kBlock - 1) / kBlock;
+  const int nst = (nb + BPS - 1) / BPS;
+
   RowState st[RT];
   f32x4_t oacc[RT][D / 16];
 #pragma unroll
@@ -324,53 +342,106 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(const bf16_t* __restric
     for (int t = 0; t < D / 16; ++t) oacc[i][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
 
-  const int kend = it.p0 + it.npos;  // keys [0, kend)
-  const int nb = (kend + kBlock - 1) / kBlock;
-  KFrag<D> kx, ky;
-  VFrag<D> vx, vy;
-  int w = 0, we = 0, ids = 0;
-  auto load = [&](KFrag<D>& kf, VFrag<D>& vf, int b) {
-    b = b < we ? b : we - 1;
-    const bf16_t* kp = kv + ((size_t)__builtin_amdgcn_readlane(ids, b - w) * n_kv + kvh) * head_stride;
-    kf.load(kp, lane);
-    vf.load(kp + plane, lane);
+  // Block ids, 64 at a time (a multiple of BPS, so a stage never straddles
+  // two windows).
+  int wbase = 0, ids = 0;
+  auto issue = [&](int stg, int buf) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int f = wave * PER + p;
+      const int c = f % FR;
+      int b = stg * BPS + f / FR;
+      b = b < nb ? b : nb - 1;  // past the end: a valid block, never used
+      const bf16_t* src = kv + ((size_t)__builtin_amdgcn_readlane(ids, b - wbase) * n_kv + kvh) *
+                                   (2 * plane) +
+                          (c < NJ ? c * 512 : plane + (c - NJ) * 512) + lane * 8;
+      __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)&lds[buf][f * 64], 16, 0, 0);
+    }
   };
-  auto step = [&](const KFrag<D>& kf, const VFrag<D>& vf, int b) {
+
+  ids = fill_window(bt, 0, min(64, nb), lane);
+  issue(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  for (int stg = 0; stg < nst; ++stg) {
+    const int buf = stg & 1;
+    if (stg + 1 < nst) {
+      if ((stg + 1) * BPS - wbase >= 64) {
+        wbase = (stg + 1) * BPS;
+        ids = fill_window(bt, wbase, min(wbase + 64, nb), lane);
+      }
+      issue(stg + 1, buf ^ 1);
+    }
+    const u32x4_t* L = lds[buf];
+    // scores of the stage: S^T tiles, lane l: row l%16, keys (l/16)*4 + r
+    f32x4_t sc[RT][BPS];
+#pragma unroll
+    for (int bi = 0; bi < BPS; ++bi) {
+      u32x4_t kf[NJ];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) kf[j] = L[(bi * FR + j) * 64 + lane];
+      const int key0 = (stg * BPS + bi) * kBlock + (lane >> 4) * 4;
+#pragma unroll
+      for (int i = 0; i < RT; ++i) {
+        f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) s = mfma16x16x32(kf[j], qf[i][j], s);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) s[r] = key0 + r <= rpos[i] ? s[r] * scale : -INFINITY;
+        sc[i][bi] = s;
+      }
+    }
+    // softmax statistics of the stage; P as bf16 B operands
+    u32x2_t pb[RT][BPS];
 #pragma unroll
     for (int i = 0; i < RT; ++i) {
-      f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      float bm = -INFINITY;
 #pragma unroll
-      for (int j = 0; j < NJ; ++j) s = mfma16x16x32(kf.v[j], qf[i][j], s);
+      for (int bi = 0; bi < BPS; ++bi)
+        bm = fmaxf(bm, fmaxf(fmaxf(sc[i][bi][0], sc[i][bi][1]), fmaxf(sc[i][bi][2], sc[i][bi][3])));
+      bm = row4_max(bm);
+      const bool grow = bm > st[i].m + kLazyRescale;
+      const float mn = grow ? bm : st[i].m;
+      const float alpha = exp2f(st[i].m - mn);  // 1 unless the maximum moved
+      float ps = 0.f;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = b * kBlock + (lane >> 4) * 4 + r;
-        s[r] = key <= rpos[i] ? s[r] * scale : -INFINITY;
+      for (int bi = 0; bi < BPS; ++bi) {
+        float p[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) p[r] = exp2f(sc[i][bi][r] - mn);
+        ps += (p[0] + p[1]) + (p[2] + p[3]);
+        pb[i][bi] = u32x2_t{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3])};
       }
-      softmax_pv<D>(s, st[i], oacc[i], vf);
+      st[i].l = st[i].l * alpha + row4_sum(ps);
+      st[i].m = mn;
+      if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+#pragma unroll
+        for (int t = 0; t < D / 16; ++t) oacc[i][t] *= alpha;
+      }
     }
-  };
-  for (w = 0; w < nb; w += 64) {
-    we = min(w + 64, nb);
-    ids = fill_window(bt, w, we, lane);
-    load(kx, vx, w);
-    int b = w;
-    for (; b + 1 < we; b += 2) {
-      load(ky, vy, b + 1);
-      __builtin_amdgcn_sched_barrier(0);
-      step(kx, vx, b);
-      __builtin_amdgcn_sched_barrier(0);
-      load(kx, vx, b + 2);
-      __builtin_amdgcn_sched_barrier(0);
-      step(ky, vy, b + 1);
-      __builtin_amdgcn_sched_barrier(0);
+    // O^T += V^T P^T
+#pragma unroll
+    for (int bi = 0; bi < BPS; ++bi) {
+      u32x4_t vf[NJ];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) vf[j] = L[(bi * FR + NJ + j) * 64 + lane];
+#pragma unroll
+      for (int i = 0; i < RT; ++i)
+#pragma unroll
+        for (int t = 0; t < D / 16; ++t) {
+          const u32x4_t& w = vf[t >> 1];
+          const u32x2_t vt = (t & 1) ? u32x2_t{w[2], w[3]} : u32x2_t{w[0], w[1]};
+          oacc[i][t] = mfma16x16x16(vt, pb[i][bi], oacc[i][t]);
+        }
     }
-    if (b < we) step(kx, vx, b);
+    __builtin_amdgcn_s_waitcnt(0);  // the next stage has landed in LDS
+    __syncthreads();
   }
 
 #pragma unroll
   for (int i = 0; i < RT; ++i) {
     if (!rok[i]) continue;
-    const int r = i * 16 + (lane & 15);
+    const int r = (wave * RT + i) * 16 + (lane & 15);
     const float inv = 1.0f / st[i].l;
     // packed activation layout (the O projection's input); 4 consecutive
     // columns share one 8-byte piece of a fragment lane
@@ -436,13 +507,11 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__
   if (D > 64) op[lane + 64] = o1 / l;
 }
 
-constexpr int kPrefillRT = 2;
-
 }  // namespace
 
-int prefill_item_positions(DType dt, int group) {
+int prefill_item_positions(DType dt, int group, int row_tiles) {
   (void)dt;
-  return kPrefillRT * 16 / group;
+  return kPfWaves * row_tiles * 16 / group;
 }
 
 hipError_t attn_decode(DType dt, const void* q, KVLayer kv, SegTables tabs,
@@ -492,20 +561,29 @@ hipError_t attn_merge(DType dt, const float* part_o, const float* part_ml,
   return hipErrorInvalidValue;
 }
 
+template <int D, int RT>
+static void launch_prefill(dim3 grid, hipStream_t s, const void* q, KVLayer kv, SegTables tabs,
+                           const PrefillItem* items, int n_q, void* out) {
+  attn_prefill_bf16<D, RT><<<grid, kPfWaves * 64, 0, s>>>(
+      (const bf16_t*)q, (const bf16_t*)kv.base, kv.n_kv, tabs, items, n_q, (bf16_t*)out);
+}
+
 hipError_t attn_prefill(DType dt, const void* q, KVLayer kv, SegTables tabs,
-                        const PrefillItem* items, int n_items, int n_q, void* out,
+                        const PrefillItem* items, int n_items, int n_q, int row_tiles, void* out,
                         hipStream_t s) {
   if (n_items == 0) return hipSuccess;
-  if (dt != DT_BF16) return hipErrorInvalidValue;
-  dim3 grid(n_items, (kv.n_kv + 3) / 4);
-  if (kv.head_dim == 128)
-    attn_prefill_bf16<128, kPrefillRT><<<grid, 256, 0, s>>>(
-        (const bf16_t*)q, (const bf16_t*)kv.base, kv.n_kv, tabs, items, n_q, (bf16_t*)out);
-  else if (kv.head_dim == 64)
-    attn_prefill_bf16<64, kPrefillRT><<<grid, 256, 0, s>>>(
-        (const bf16_t*)q, (const bf16_t*)kv.base, kv.n_kv, tabs, items, n_q, (bf16_t*)out);
-  else
+  if (dt != DT_BF16 || (row_tiles != 2 && row_tiles != 4)) return hipErrorInvalidValue;
+  if ((kPfWaves * row_tiles * 16) % (n_q / kv.n_kv) != 0) return hipErrorInvalidValue;
+  dim3 grid(n_items, kv.n_kv);
+  if (kv.head_dim == 128) {
+    if (row_tiles == 4) launch_prefill<128, 4>(grid, s, q, kv, tabs, items, n_q, out);
+    else launch_prefill<128, 2>(grid, s, q, kv, tabs, items, n_q, out);
+  } else if (kv.head_dim == 64) {
+    if (row_tiles == 4) launch_prefill<64, 4>(grid, s, q, kv, tabs, items, n_q, out);
+    else launch_prefill<64, 2>(grid, s, q, kv, tabs, items, n_q, out);
+  } else {
     return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
