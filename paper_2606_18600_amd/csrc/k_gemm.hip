@@ -221,7 +221,26 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tiled_bf16(const bf16_t* __
   __shared__ u32x4_t lds[2][FR * 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WN, wn = wave % WN;
-  const int mt0 = blockIdx.x * BMT, g0 = blockIdx.y * BNG, KT = K / 32;
+  // Blocks are dealt round-robin to the 8 XCDs (block b -> XCD b % 8), each
+  // with its own L2. Remap so that each XCD gets whole weight columns (all
+  // m-blocks of a column one after another): a weight tile is then fetched
+  // into one L2 instead of all eight. Columns past the last multiple of 8
+  // are mapped in plain order.
+  int mb, nb;
+  {
+    const int MB = gridDim.x, NB = gridDim.y, NB8 = NB / 8 * 8;
+    const int lin = blockIdx.x + blockIdx.y * MB;
+    if (lin < MB * NB8) {
+      const int xcd = lin % 8, j = lin / 8;
+      nb = (j / MB) * 8 + xcd;
+      mb = j % MB;
+    } else {
+      const int rem = lin - MB * NB8;
+      nb = NB8 + rem / MB;
+      mb = rem % MB;
+    }
+  }
+  const int mt0 = mb * BMT, g0 = nb * BNG, KT = K / 32;
 
   // this wave's fragments of a stage: source (at stage 0) and LDS slot
   const bf16_t* src[PER_WAVE];
