@@ -112,7 +112,7 @@ def bench_q32_mixed(args):
 
 # The decode gate-up projection is the split-K GEMM instantiated with the
 # fused SwiGLU epilogue (template arguments <m-tiles, 1>).
-GATE_UP_DECODE_KERNEL = r"gemm_skinny_bf16<\d+, 1>"
+GATE_UP_DECODE_KERNEL = r"gemm_skinny_bf16<\d+, ?1>"
 KERNEL_SOURCES = ("paper_2606_18600_amd/csrc/k_gemm.hip", "paper_2606_18600_amd/csrc/common.hpp",
                   "paper_2606_18600_amd/csrc/packed.hpp", "paper_2606_18600_amd/csrc/kernels.hpp")
 TRAFFIC_FILE = "profiles/gate_up_l70_decode_traffic.txt"

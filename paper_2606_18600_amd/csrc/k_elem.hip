@@ -269,12 +269,22 @@ inline int grid_for(size_t n, int threads) {
 
 }  // namespace
 
-// Plain streaming copy of n16 16-byte words (grid-stride, coalesced): the
-// known-size reference for bandwidth and hardware traffic counters.
+// Plain streaming copy of n16 16-byte words: each thread moves four words
+// per round (loads issued before stores), grid-stride, non-temporal on both
+// sides. The known-size reference for bandwidth and hardware traffic
+// counters.
 __global__ __launch_bounds__(256) void copy_probe_kernel(const u32x4_t* __restrict__ src,
                                                          u32x4_t* __restrict__ dst, size_t n16) {
-  const size_t stride = (size_t)gridDim.x * 256;
-  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += stride) dst[i] = src[i];
+  const size_t stride = (size_t)gridDim.x * 1024;
+  size_t i = (size_t)blockIdx.x * 1024 + threadIdx.x;
+  for (; i + 768 < n16; i += stride) {
+    u32x4_t v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = __builtin_nontemporal_load(src + i + u * 256);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) __builtin_nontemporal_store(v[u], dst + i + u * 256);
+  }
+  for (; i < n16; i += 256) dst[i] = src[i];
 }
 
 hipError_t embed_norm(DType dt, const void* hidden_in, float* x, void* h, const void* gain, int T,
@@ -347,7 +357,7 @@ hipError_t swiglu_reduce_bf16(Partials gu, uint16_t* m, int T, int F, hipStream_
 hipError_t copy_probe(const void* src, void* dst, size_t bytes, hipStream_t s) {
   const size_t n16 = bytes / 16;
   if (n16 == 0) return hipSuccess;
-  const size_t blocks = std::min<size_t>((n16 + 255) / 256, 8192);
+  const size_t blocks = std::min<size_t>((n16 + 1023) / 1024, 4096);
   copy_probe_kernel<<<(unsigned)blocks, 256, 0, s>>>((const u32x4_t*)src, (u32x4_t*)dst, n16);
   return hipGetLastError();
 }
