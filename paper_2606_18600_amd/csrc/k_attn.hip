@@ -29,6 +29,9 @@ namespace stage_k {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+// Online softmax: move the reference maximum only when a block's maximum
+// exceeds it by more than this (log2 units).
+constexpr float kLazyRescale = 8.0f;
 
 __device__ __forceinline__ const int32_t* seq_table(const SegTables& t, int seq) {
   return seq < t.nseq0 ? t.bt0 + (size_t)seq * t.stride0
@@ -119,7 +122,9 @@ __device__ __forceinline__ void softmax_pv(f32x4_t s, RowState& st, f32x4_t* oac
   const float bm = row4_max(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])));
   const float mn = fmaxf(st.m, bm);
   // A row can only be fully masked in a block after an earlier block gave it
-  // a finite max, so mn is finite here.
+  // a finite max, so mn is finite here. (No data-dependent branch here: a
+  // branch inside the pipelined key loop makes the compiler wait for every
+  // outstanding load at the join.)
   const float alpha = exp2f(st.m - mn);
   float p[4];
 #pragma unroll
@@ -291,7 +296,6 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const float* __restrict
 // below 256 and the rescale is rare after the first stage.
 constexpr int kPfWaves = 4;
 constexpr int kPfBPS = 4;
-constexpr float kLazyRescale = 8.0f;  // log2 units
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
