@@ -235,8 +235,7 @@ __global__ __launch_bounds__(256) void attn_decode_bf16(const bf16_t* __restrict
 
 // Combine the key splits of each decode token: one wave per (token, kv
 // head). Lane l serves query head row r = l / LPR of the group and DPL
-// consecutive d values (a multiple of 4); the split loop is unrolled so the
-// loads of several splits are in flight together.
+// consecutive d values (a multiple of 4).
 template <int D, int G>
 __global__ __launch_bounds__(256) void attn_merge_kernel(const float* __restrict__ part_o,
                                                          const float* __restrict__ part_ml,
@@ -253,26 +252,51 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const float* __restrict
   const int h = kvh * G + lane / LPR;
   const int d0 = (lane % LPR) * DPL;
   const int i0 = item_start[t], i1 = item_start[t + 1];
-  float M = -INFINITY;
-  for (int i = i0; i < i1; ++i) M = fmaxf(M, part_ml[((size_t)i * n_q + h) * 2]);
-  float L = 0.f;
+  // Online merge over chunks of 4 splits: a chunk's loads are all issued
+  // before any is used (indices past the last split are clamped and masked),
+  // so a token with up to 4 splits costs one memory round trip.
+  float M = -INFINITY, L = 0.f;
   float4 o[DPL / 4];
 #pragma unroll
   for (int c = 0; c < DPL / 4; ++c) o[c] = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll 4
-  for (int i = i0; i < i1; ++i) {
-    const size_t b = (size_t)i * n_q + h;
-    const float w = exp2f(part_ml[b * 2] - M);
-    L += w * part_ml[b * 2 + 1];
-    const float4* po = (const float4*)(part_o + b * D + d0);
+  for (int i = i0; i < i1; i += 4) {
+    float mu[4], lu[4];
+    float4 v[4][DPL / 4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const size_t b = (size_t)min(i + u, i1 - 1) * n_q + h;
+      mu[u] = part_ml[b * 2];
+      lu[u] = part_ml[b * 2 + 1];
+      const float4* po = (const float4*)(part_o + b * D + d0);
+#pragma unroll
+      for (int c = 0; c < DPL / 4; ++c) v[u][c] = po[c];
+    }
+    float cm = M;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (i + u < i1) cm = fmaxf(cm, mu[u]);
+    const float sc = exp2f(M - cm);  // 0 for the first chunk (M = -inf)
+    L *= sc;
 #pragma unroll
     for (int c = 0; c < DPL / 4; ++c) {
-      const float4 v = po[c];
-      o[c].x += w * v.x;
-      o[c].y += w * v.y;
-      o[c].z += w * v.z;
-      o[c].w += w * v.w;
+      o[c].x *= sc;
+      o[c].y *= sc;
+      o[c].z *= sc;
+      o[c].w *= sc;
     }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float w = i + u < i1 ? exp2f(mu[u] - cm) : 0.f;
+      L += w * lu[u];
+#pragma unroll
+      for (int c = 0; c < DPL / 4; ++c) {
+        o[c].x += w * v[u][c].x;
+        o[c].y += w * v[u][c].y;
+        o[c].z += w * v[u][c].z;
+        o[c].w += w * v[u][c].w;
+      }
+    }
+    M = cm;
   }
   const float inv = 1.0f / L;
   const int row = tok_rows[t], K = n_q * D;
