@@ -251,3 +251,71 @@ def test_q32_mixed_step_sampled():
         _check_rows_one_layer(shape, st, w64, dbt_np, drow, x64, y64, "decode rows")
     finally:
         st.close()
+
+
+def test_l70_decode_batch128_one_layer_sampled():
+    """The 80-layer workload's decode-only step shape: batch 128 (the split-K
+    GEMMs with 8 m-tiles), contexts U[1024, 4096]."""
+    seed, shape, layer, B = 2608, synth.LLAMA70B, 60, 128
+    log("l70 decode, one layer, batch 128")
+    cfg = model_config(shape, "bf16")
+    w = device_layer_weights(shape, seed, layer, "bf16")
+    w64 = _host64(w)
+    ctx = synth.uniform_lengths(seed, 1, B, 1024, 4096)
+    nblocks = int(((ctx + 16) // 16).sum()) + 8
+    bt_np = synth.make_block_tables(ctx + 1, int((ctx.max() + 16) // 16),
+                                    synth.BlockAllocator(nblocks, seed))
+    st = DeviceStage(shape, "bf16", layer, [pack_layer(cfg, w)], nblocks, 2176, B, packed=True)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    try:
+        st.kv_pool.normal_(0.0, 1.0, generator=g)
+        x = torch.randn((B, shape.hidden), generator=g, device="cuda").to(torch.bfloat16)
+        y = st.decode(ctx, torch.from_numpy(bt_np).cuda(), x)
+        torch.cuda.synchronize()
+        rng = np.random.default_rng(seed)
+        pick = sorted({0, B - 1, int(np.argmax(ctx)), int(np.argmin(ctx))} |
+                      set(rng.choice(B, 4, replace=False).tolist()))
+        rows = [(j, int(ctx[j]), j) for j in pick]
+        _check_rows_one_layer(shape, st, w64, bt_np, rows, x.double().cpu().numpy(),
+                              y.double().cpu().numpy(), "decode rows (batch 128)")
+    finally:
+        st.close()
+
+
+def test_l70_mixed_step_sampled():
+    """The 80-layer workload's mixed step shape: 128 decodes (contexts
+    U[1024, 4096]) plus 2048 prefill tokens, one continuation chunk that
+    starts mid-block and one fresh prompt."""
+    seed, shape, layer = 2609, synth.LLAMA70B, 79
+    log("l70 mixed step, one layer: 1500 + 548 prefill + 128 decodes")
+    cfg = model_config(shape, "bf16")
+    w = device_layer_weights(shape, seed, layer, "bf16")
+    w64 = _host64(w)
+    pc = np.array([1000, 0], np.int32)
+    pq = np.array([1500, 548], np.int32)
+    dctx = synth.uniform_lengths(seed, 3, 128, 1024, 4096)
+    alloc = synth.BlockAllocator(int(((pc + pq + 15) // 16).sum() + ((dctx + 16) // 16).sum()) + 4,
+                                 seed)
+    pbt_np = synth.make_block_tables(pc + pq, int(((pc + pq + 15) // 16).max()), alloc)
+    dbt_np = synth.make_block_tables(dctx + 1, int((dctx.max() + 16) // 16), alloc)
+    nb = int(max(pbt_np.max(), dbt_np.max())) + 1
+    st = DeviceStage(shape, "bf16", layer, [pack_layer(cfg, w)], nb, 2176, 130, packed=True)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    try:
+        st.kv_pool.normal_(0.0, 1.0, generator=g)  # cached prefix and decode contexts
+        x = torch.randn((2176, shape.hidden), generator=g, device="cuda").to(torch.bfloat16)
+        y = st.mixed(pq, pc, torch.from_numpy(pbt_np).cuda(), dctx, torch.from_numpy(dbt_np).cuda(),
+                     x)
+        torch.cuda.synchronize()
+        rng = np.random.default_rng(seed)
+        x64, y64 = x.double().cpu().numpy(), y.double().cpu().numpy()
+        prow = _sample_rows(rng, pq, pc, 8)
+        _check_rows_one_layer(shape, st, w64, pbt_np, prow, x64, y64, "prefill rows")
+        drow = [(int(j), int(dctx[j]), 2048 + int(j))
+                for j in sorted({0, 127, int(np.argmax(dctx)), int(np.argmin(dctx))} |
+                                set(rng.choice(128, 6, replace=False).tolist()))]
+        _check_rows_one_layer(shape, st, w64, dbt_np, drow, x64, y64, "decode rows")
+    finally:
+        st.close()
