@@ -335,8 +335,13 @@ __global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_bf16(
   static_assert(SF % kPfWaves == 0, "stage split");
   __shared__ u32x4_t lds[2][SF * 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int kvh = blockIdx.y;
-  const PrefillItem it = items[blockIdx.x];
+  // Workgroup b runs on XCD b % 8, each XCD with its own L2. Take the kv head
+  // from the linear id modulo n_kv, so every XCD serves a fixed set of kv
+  // heads and a sequence's K/V for one head is pulled into one L2 only (not
+  // into all eight); items stay in their longest-first order.
+  const int lin = blockIdx.x + blockIdx.y * gridDim.x;
+  const int kvh = lin % n_kv;
+  const PrefillItem it = items[lin / n_kv];
   const int G = n_q / n_kv;
   const float scale = kLog2e / sqrtf((float)D);
 
