@@ -209,7 +209,7 @@ template <int BMT, int BNG, int WM, int WN, int EPI>
 __global__ __launch_bounds__(WM * WN * 64) void gemm_tiled_bf16(const bf16_t* __restrict__ A,
                                                                const bf16_t* __restrict__ W,
                                                                int M, int N, int K,
-                                                               void* __restrict__ out) {
+                                                               void* __restrict__ out, int ldo) {
   constexpr int NW = WM * WN;
   constexpr int AF = BMT * 2;
   constexpr int BF = BNG * 8;
@@ -321,7 +321,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tiled_bf16(const bf16_t* __
         } else {
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            float* o = (float*)out + (size_t)m * N + g * 64 + j * 16 + r16;
+            float* o = (float*)out + (size_t)m * ldo + g * 64 + j * 16 + r16;
             if (EPI == EPI_RESID_ADD)
               *o += acc[i][gi * 4 + j][r];
             else
@@ -468,28 +468,48 @@ hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int
     return (double)blocks / (double)(rounds * slots);
   };
   const long mb256 = (M + 255) / 256, mb128 = (M + 127) / 128;
-  const bool big = N % 256 == 0 &&
-                   1.12 * util(mb256 * (N / 256), 256) >= 0.97 * util(mb128 * (N / 128), 512);
   const bf16_t* a = (const bf16_t*)A;
   const bf16_t* w = (const bf16_t*)W;
-  if (big) {
-    dim3 grid(mb256, N / 256);
-    switch (epi) {
-      case EPI_STORE_F32: gemm_tiled_bf16<16, 4, 2, 4, EPI_STORE_F32><<<grid, 512, 0, s>>>(a, w, M, N, K, out); break;
-      case EPI_RESID_ADD: gemm_tiled_bf16<16, 4, 2, 4, EPI_RESID_ADD><<<grid, 512, 0, s>>>(a, w, M, N, K, out); break;
-      case EPI_SWIGLU: gemm_tiled_bf16<16, 4, 2, 4, EPI_SWIGLU><<<grid, 512, 0, s>>>(a, w, M, N, K, out); break;
-      default: return hipErrorInvalidValue;
+  // columns [n0, n0 + Nl) of the product; fp32 outputs keep the row stride N
+  auto launch = [&](bool big, int n0, int Nl) -> hipError_t {
+    const bf16_t* wl = w + (size_t)n0 * K;  // packed groups of 64 rows stay in row order
+    void* ol = epi == EPI_SWIGLU ? out : (void*)((float*)out + n0);
+    if (big) {
+      dim3 grid(mb256, Nl / 256);
+      switch (epi) {
+        case EPI_STORE_F32: gemm_tiled_bf16<16, 4, 2, 4, EPI_STORE_F32><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N); break;
+        case EPI_RESID_ADD: gemm_tiled_bf16<16, 4, 2, 4, EPI_RESID_ADD><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N); break;
+        case EPI_SWIGLU: gemm_tiled_bf16<16, 4, 2, 4, EPI_SWIGLU><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N); break;
+        default: return hipErrorInvalidValue;
+      }
+    } else {
+      dim3 grid(mb128, Nl / 128);
+      switch (epi) {
+        case EPI_STORE_F32: gemm_tiled_bf16<8, 2, 2, 2, EPI_STORE_F32><<<grid, 256, 0, s>>>(a, wl, M, Nl, K, ol, N); break;
+        case EPI_RESID_ADD: gemm_tiled_bf16<8, 2, 2, 2, EPI_RESID_ADD><<<grid, 256, 0, s>>>(a, wl, M, Nl, K, ol, N); break;
+        case EPI_SWIGLU: gemm_tiled_bf16<8, 2, 2, 2, EPI_SWIGLU><<<grid, 256, 0, s>>>(a, wl, M, Nl, K, ol, N); break;
+        default: return hipErrorInvalidValue;
+      }
     }
-  } else {
-    dim3 grid(mb128, N / 128);
-    switch (epi) {
-      case EPI_STORE_F32: gemm_tiled_bf16<8, 2, 2, 2, EPI_STORE_F32><<<grid, 256, 0, s>>>(a, w, M, N, K, out); break;
-      case EPI_RESID_ADD: gemm_tiled_bf16<8, 2, 2, 2, EPI_RESID_ADD><<<grid, 256, 0, s>>>(a, w, M, N, K, out); break;
-      case EPI_SWIGLU: gemm_tiled_bf16<8, 2, 2, 2, EPI_SWIGLU><<<grid, 256, 0, s>>>(a, w, M, N, K, out); break;
-      default: return hipErrorInvalidValue;
+    return hipGetLastError();
+  };
+  const bool big = N % 256 == 0 &&
+                   1.12 * util(mb256 * (N / 256), 256) >= 0.97 * util(mb128 * (N / 128), 512);
+  if (!big && epi != EPI_SWIGLU && N % 256 == 0) {
+    // When 256-tiles would leave a partial last round, run the columns that
+    // fill whole rounds on 256-tiles and only the rest on 128-tiles (e.g.
+    // QKV at 2048 rows: 8192 columns = one round of 256 blocks, 2048 left).
+    long g = mb256, b = 256;
+    while (b) { const long t = g % b; g = b; b = t; }  // gcd(mb256, 256)
+    const long per_round = 256 / g;                     // column blocks per whole round
+    const int n1 = (int)((N / 256) / per_round * per_round * 256);
+    if (n1 >= N / 2 && n1 < N) {
+      const hipError_t e = launch(true, 0, n1);
+      if (e != hipSuccess) return e;
+      return launch(false, n1, N - n1);
     }
   }
-  return hipGetLastError();
+  return launch(big, 0, N);
 }
 
 }  // namespace stage_k
