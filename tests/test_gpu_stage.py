@@ -302,3 +302,46 @@ def test_copy_probe_copies_exactly(nbytes):
     torch.cuda.synchronize()
     assert torch.equal(dst[: nbytes // 4], src)
     assert (dst[nbytes // 4:] == -7).all()      # nothing written past the end
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_stage_composition(dtype):
+    """Pipeline partitioning: stage [0, 1) followed by stage [1, 2) equals
+    stage [0, 2) over a prefill and three decode steps. fp32 mode: bitwise
+    (the fp32 stage output is the residual stream itself and every kernel
+    is deterministic). bf16: within tolerance, since the hidden state that
+    crosses the stage boundary is rounded to bf16 there."""
+    from paper_2606_18600_amd.harness import DeviceStage, torch_dtype, upload_weights
+    seed, shape = 2610, synth.TINY
+    log(f"stage composition dtype={dtype}")
+    td = torch_dtype(dtype)
+    w = [upload_weights(synth.host_layer_weights(shape, seed, l), dtype) for l in range(2)]
+    lens = synth.uniform_lengths(seed, 0, 4, 16, 64)
+    bt = torch.from_numpy(synth.make_block_tables(lens + 4, 8, synth.BlockAllocator(48, seed)))
+    bt = bt.cuda()
+    whole = DeviceStage(shape, dtype, 0, w, 48, 256, 8)
+    first = DeviceStage(shape, dtype, 0, w[:1], 48, 256, 8)
+    second = DeviceStage(shape, dtype, 1, w[1:], 48, 256, 8)
+    try:
+        steps = [(lens, np.zeros(4, np.int32), int(lens.sum()))]
+        steps += [(np.ones(4, np.int32), lens + i, 4) for i in range(3)]
+        for k, (q, c, T) in enumerate(steps):
+            x = torch.from_numpy(synth.hidden_states(seed, 10 + k, T, shape.hidden)).cuda().to(td)
+            if k == 0:
+                y = whole.prefill(q, c, bt, x)
+                y2 = second.prefill(q, c, bt, first.prefill(q, c, bt, x))
+            else:
+                y = whole.decode(c, bt, x)
+                y2 = second.decode(c, bt, first.decode(c, bt, x))
+            torch.cuda.synchronize()
+            a, b = y.double().cpu().numpy(), y2.double().cpu().numpy()
+            e = rel_l2(b, a)
+            log(f"  step {k}: rel_l2 {e:.3e}")
+            if dtype == "f32":
+                assert torch.equal(y, y2), f"step {k}: not bitwise equal ({e:.3e})"
+            else:
+                assert e <= TOL[dtype], (k, e)
+    finally:
+        whole.close()
+        first.close()
+        second.close()
