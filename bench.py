@@ -110,6 +110,85 @@ def bench_q32_mixed(args):
     return res
 
 
+# Context lengths of the migration sweep, and the links a migrated
+# request's KV would otherwise cross: data-centre NICs between instances and,
+# for scale, one xGMI link inside a node.
+MIGRATE_LENGTHS = (1024, 2048, 4096, 8192, 16384, 32768, 65536)
+MIGRATE_LINKS_GBS = {"25GbE": 3.125, "100GbE": 12.5, "400GbE": 50.0, "xGMI_link": 153.0}
+
+
+def bench_migrate(args):
+    """Migration by recomputation on the Llama-3.1-70B-shaped 20-layer stage:
+    for each context length, the time to rebuild one request's KV by chunked
+    prefill (2048-token chunks) over the hidden states of all its tokens,
+    next to the bytes a KV transfer of the same request would move."""
+    import torch
+    from paper_2606_18600_amd import stage as S
+    from paper_2606_18600_amd import synth
+    from paper_2606_18600_amd.harness import (DeviceStage, device_layer_weights, model_config,
+                                              pack_layer)
+    from paper_2606_18600_amd.migrate import migration_points, recompute_kv
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    shape, seed = synth.LLAMA70B, args.seed
+    wl = synth.WORKLOADS["l70-decode"]
+    L0, nL = wl.layer_begin, wl.n_layers
+    Lmax = max(MIGRATE_LENGTHS)
+    nb = Lmax // 16
+    cfg = model_config(shape, "bf16", max_position=Lmax)
+    log(f"[bench] generating {nL} layers of {shape.name} weights on the device")
+    weights = [pack_layer(cfg, device_layer_weights(shape, seed, l, "bf16"), free_source=True)
+               for l in range(L0, wl.layer_end)]
+    bt = torch.from_numpy(synth.make_block_tables([Lmax], nb, synth.BlockAllocator(nb + 1, seed)))
+    bt = bt.to(dev)
+    st = DeviceStage(shape, "bf16", L0, weights, nb + 1, max_tokens=2048, max_seqs=1, packed=True,
+                     max_position=Lmax)
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    hidden = torch.empty((Lmax, shape.hidden), dtype=torch.bfloat16, device=dev)
+    hidden.normal_(0.0, 1.0, generator=g)
+    out = torch.empty_like(hidden)
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    recompute_kv(st, hidden[:4096], bt, 2048, out[:4096], stream=sp)  # warm-up
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ms_list, extra = [], []
+    for L in MIGRATE_LENGTHS:
+        reps = max(1, min(args.steps, 8192 // L))
+        e0.record(stream)
+        for _ in range(reps):
+            recompute_kv(st, hidden[:L], bt, 2048, out[:L], stream=sp)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        S.stage_set_op_timing(st.handle, True)
+        recompute_kv(st, hidden[:L], bt, 2048, out[:L], stream=sp)
+        op_ms, _ = S.stage_read_op_times(st.handle)
+        S.stage_set_op_timing(st.handle, False)
+        assert torch.isfinite(out[:L].float()).all(), "non-finite stage output"
+        chunks = [(c0, min(2048, L - c0)) for c0 in range(0, L, 2048)]
+        fl = prefill_flops(shape, nL, chunks)
+        ms_list.append(ms)
+        extra.append({"tflops": round(fl / (ms / 1e3) / 1e12, 1),
+                      "frac_mfma_peak": round(fl / (ms / 1e3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+                      "attn_share": round(op_ms[S.OP_NAMES.index("attn")] / sum(op_ms), 4)})
+        log(f"[bench] recompute {L} tokens: {ms:.1f} ms ({reps} reps), "
+            f"{fl / (ms / 1e3) / 1e12:.0f} TFLOP/s, attention {extra[-1]['attn_share']:.0%}")
+    st.close()
+    pts = []
+    for (L, b, ms, link_ms), ex in zip(migration_points(shape, nL, MIGRATE_LENGTHS, ms_list,
+                                                        MIGRATE_LINKS_GBS), extra):
+        pts.append({"tokens": L, "recompute_ms": round(ms, 2),
+                    "recompute_ms_per_layer": round(ms / nL, 3),
+                    "kv_transfer_bytes": b, "kv_transfer_ms": {k: round(v, 2)
+                                                               for k, v in link_ms.items()},
+                    "breakeven_link_GBs": round(b / (ms / 1e3) / 1e9, 2), **ex})
+    return {"workload": "migrate: Llama-3.1-70B-shaped stage, layers [20,40); one request's KV "
+                        "rebuilt by chunked prefill (2048-token chunks) at 1K-64K tokens",
+            "points": pts}
+
+
 # The decode gate-up projection is the split-K GEMM instantiated with the
 # fused SwiGLU epilogue (template arguments <m-tiles, 1>).
 GATE_UP_DECODE_KERNEL = r"gemm_skinny_bf16<\d+, ?1>"
@@ -332,9 +411,10 @@ def main():
     ap.add_argument("--arrival-rate", type=float, default=0.0,
                     help="l70-full: Poisson arrivals per second (0: all at t=0)")
     ap.add_argument("--workload", default="l70-decode",
-                    choices=["l70-decode", "q32-mixed", "l70-full"],
+                    choices=["l70-decode", "q32-mixed", "l70-full", "migrate"],
                     help="l70-decode (default: the metric's workload, plus the chunked prefill "
-                         "of the same stage); q32-mixed and l70-full print their own line")
+                         "of the same stage); q32-mixed, l70-full and migrate print their own "
+                         "line")
     ap.add_argument("--summarize-trace", metavar="DIR",
                     help="print a summary of a rocprofv3 kernel trace under DIR and exit")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -363,6 +443,10 @@ def main():
         print(json.dumps({"metric": METRIC, "n_gpus": 1, "steps": args.steps,
                           "warmup": args.warmup, "dtype": "bf16", "data": "synthetic",
                           **bench_q32_mixed(args)}), flush=True)
+        return
+    if args.workload == "migrate":
+        print(json.dumps({"metric": METRIC, "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
+                          **bench_migrate(args)}), flush=True)
         return
     if args.workload == "l70-full":
         from paper_2606_18600_amd.batcher import bench_l70_full

@@ -1,0 +1,154 @@
+"""Migration by recomputation: a request's KV rebuilt by chunked prefill over
+the hidden states of all its tokens (prompt + generated) equals the KV its
+original serving path (prefill, then decode steps) wrote, and the next
+decode step agrees on both instances."""
+
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import stage_oracle as O
+from paper_2606_18600_amd import synth
+from paper_2606_18600_amd.harness import (DeviceStage, device_layer_weights, gpu_kv_to_oracle_layout,
+                                          model_config, pack_layer, to_host64, torch_dtype,
+                                          upload_weights)
+from paper_2606_18600_amd.migrate import recompute_kv
+from tests.gpu_pair import log
+from tests.helpers import ocfg, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def _seq_kv(st, bt_row, n_tok):
+    nb = (n_tok + 15) // 16
+    ids = torch.tensor([int(b) for b in bt_row[:nb]], dtype=torch.long, device="cuda")
+    out = []
+    for c in gpu_kv_to_oracle_layout(st.kv_view()[:, ids]):
+        k = c["k"].reshape(-1, *c["k"].shape[2:])[:n_tok]   # [pos][nkv][d]
+        v = c["v"].reshape(-1, *c["v"].shape[2:])[:n_tok]
+        out.append((k, v))
+    return out
+
+
+def _run(shape, dtype, weights, prompt, n_dec, seed, chunk, max_tokens, layer_begin=0):
+    td = torch_dtype(dtype)
+    H = shape.hidden
+    total = prompt + n_dec + 1
+    nb = (total + 15) // 16
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    xs = torch.randn((total, H), generator=g, device="cuda").to(td)
+    # the original instance and the one that receives the migrated request,
+    # each with its own pool and a different (shuffled) block table
+    a = DeviceStage(shape, dtype, layer_begin, weights, nb + 8, max_tokens, 4, packed=True,
+                    max_position=max(8192, total + 16))
+    b = DeviceStage(shape, dtype, layer_begin, weights, nb + 8, max_tokens, 4, packed=True,
+                    max_position=max(8192, total + 16))
+    try:
+        bta = synth.make_block_tables([total], nb, synth.BlockAllocator(nb + 8, seed))
+        btb = synth.make_block_tables([total], nb, synth.BlockAllocator(nb + 8, seed + 1))
+        ta, tb = torch.from_numpy(bta).cuda(), torch.from_numpy(btb).cuda()
+        # original: chunked prefill of the prompt, then n_dec decode steps
+        ya = torch.empty_like(xs)
+        for c0 in range(0, prompt, chunk):
+            q = min(chunk, prompt - c0)
+            a.prefill([q], [c0], ta, xs[c0:c0 + q], ya[c0:c0 + q])
+        for i in range(n_dec):
+            p = prompt + i
+            a.decode([p], ta, xs[p:p + 1], ya[p:p + 1])
+        # migration: the receiver recomputes from the hidden states of all
+        # prompt_len + n_dec tokens
+        n = prompt + n_dec
+        yb = recompute_kv(b, xs[:n].contiguous(), tb, chunk=chunk)
+        torch.cuda.synchronize()
+        worst = 0.0
+        for l, ((ka, va), (kb, vb)) in enumerate(zip(_seq_kv(a, bta[0], n), _seq_kv(b, btb[0], n))):
+            ek, ev = rel_l2(kb, ka), rel_l2(vb, va)
+            worst = max(worst, ek, ev)
+            assert ek <= TOL[dtype] and ev <= TOL[dtype], (l, ek, ev)
+        eo = rel_l2(yb.double().cpu().numpy(), ya[:n].double().cpu().numpy())
+        assert eo <= TOL[dtype], ("outputs", eo)
+        # both continue with the same next token
+        p = n
+        za = a.decode([p], ta, xs[p:p + 1])
+        zb = b.decode([p], tb, xs[p:p + 1])
+        torch.cuda.synchronize()
+        en = rel_l2(zb.double().cpu().numpy(), za.double().cpu().numpy())
+        assert en <= TOL[dtype], ("next decode", en)
+        log(f"  {shape.name} {dtype}: prompt {prompt} + {n_dec} decodes, chunk {chunk}: KV worst "
+            f"{worst:.3e}, outputs {eo:.3e}, next decode {en:.3e}")
+    finally:
+        a.close()
+        b.close()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_migration_by_recomputation_tiny(dtype):
+    shape, seed = synth.TINY, 2611
+    w = [upload_weights(synth.host_layer_weights(shape, seed, l), dtype) for l in range(2)]
+    cfg = model_config(shape, dtype)
+    w = [pack_layer(cfg, x) for x in w]
+    _run(shape, dtype, w, prompt=70, n_dec=23, seed=seed, chunk=37, max_tokens=64)
+
+
+def test_migration_by_recomputation_l70_layer():
+    shape, seed, layer = synth.LLAMA70B, 2612, 40
+    cfg = model_config(shape, "bf16")
+    w = [pack_layer(cfg, device_layer_weights(shape, seed, layer, "bf16"))]
+    _run(shape, "bf16", w, prompt=3000, n_dec=24, seed=seed, chunk=2048, max_tokens=2048,
+         layer_begin=layer)
+
+
+def test_long_context_chunk_sampled():
+    """The last 2048-token chunk of a 64K-token recomputation, one L70 layer:
+    context 63483 (not block aligned), positions up to 65530 of a 65536-entry
+    RoPE table. The query rows of the QKV weight are scaled by 4 (exact in
+    bf16), so each row's softmax over ~64K random keys concentrates on a few
+    of them and the attention output is O(1) in the layer's output: a wrong
+    block, offset or mask shows in the sampled rows. Each sampled row is
+    checked against the oracle given the stage's keys/values of positions
+    < p."""
+    seed, shape, layer = 2613, synth.LLAMA70B, 39
+    ctx0, q = 65536 - 2048 - 5, 2048
+    n = ctx0 + q
+    nb = (n + 15) // 16
+    log(f"l70 one layer, prefill chunk q={q} at context {ctx0}")
+    cfg = model_config(shape, "bf16", max_position=65536)
+    w = device_layer_weights(shape, seed, layer, "bf16")
+    w["w_qkv"][:shape.n_q_heads * shape.head_dim] *= 4
+    w64 = to_host64(w)
+    bt_np = synth.make_block_tables([n], nb, synth.BlockAllocator(nb + 4, seed))
+    st = DeviceStage(shape, "bf16", layer, [pack_layer(cfg, w)], nb + 4, 2048, 1, packed=True,
+                     max_position=65536)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    try:
+        st.kv_pool.normal_(0.0, 1.0, generator=g)
+        x = torch.randn((q, shape.hidden), generator=g, device="cuda").to(torch.bfloat16)
+        y = st.prefill([q], [ctx0], torch.from_numpy(bt_np).cuda(), x)
+        torch.cuda.synchronize()
+        x64, y64 = x.double().cpu().numpy(), y.double().cpu().numpy()
+        ids = torch.tensor(bt_np[0].tolist(), dtype=torch.long, device="cuda")
+        cache = gpu_kv_to_oracle_layout(st.kv_view()[:, ids])[0]
+        table = list(range(nb))
+        rng = np.random.default_rng(seed)
+        rows = sorted({0, q - 1} | set(rng.choice(q, 8, replace=False).tolist()))
+        oc = ocfg(shape)
+        worst = 0.0
+        for r in rows:
+            p = ctx0 + r
+            b, o = divmod(p, 16)
+            gk, gv = cache["k"][b, o].copy(), cache["v"][b, o].copy()
+            yr = O.layer_forward(oc, w64, x64[r:r + 1], [O.SeqSpec(p, 1, table)], cache)[0]
+            ek, ev = rel_l2(gk, cache["k"][b, o]), rel_l2(gv, cache["v"][b, o])
+            e, ed = rel_l2(y64[r], yr), rel_l2(y64[r] - x64[r], yr - x64[r])
+            worst = max(worst, e, ed, ek, ev)
+            assert max(e, ed, ek, ev) <= TOL["bf16"], (r, p, e, ed, ek, ev)
+            cache["k"][b, o], cache["v"][b, o] = gk, gv  # later rows read the stage's entry
+        log(f"  {len(rows)} sampled rows, worst rel_l2 {worst:.3e} (output, layer delta, K, V)")
+    finally:
+        st.close()
