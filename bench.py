@@ -189,6 +189,102 @@ def bench_migrate(args):
             "points": pts}
 
 
+# The estimator sweep: the 80-layer Llama-3.1-70B cut into PP stages of TP
+# ranks (PP x TP = 8), one rank's stage measured at its own shape; static
+# batches of B requests with the mean prompt/output lengths of the paper's
+# trace (763 / 232).
+EST_CONFIGS = ((8, 1), (4, 2), (2, 4), (1, 8))
+EST_BATCHES = (1, 2, 4, 8, 16, 32)
+EST_S_IN, EST_S_OUT = 763, 232
+
+
+def bench_estimator(args):
+    """Static latency estimator against the measured stage (Sec. 4.1.1 and
+    the accuracy experiment of Sec. 7): one-time calibration, then for each
+    (PP, TP) and batch size the measured prefill + decode latency of one
+    rank's stage next to Eq. 1's prediction; MAPE over all configurations."""
+    import torch
+    from paper_2606_18600_amd import estimator as E
+    from paper_2606_18600_amd import synth
+    from paper_2606_18600_amd.harness import (DeviceStage, device_layer_weights, model_config,
+                                              pack_layer)
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    base, seed = synth.LLAMA70B, args.seed
+    t0 = time.time()
+    cal = E.calibrate(base, seed, log=log)
+    cal_s = time.time() - t0
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    Bmax, nbs = max(EST_BATCHES), (EST_S_IN + EST_S_OUT + 15) // 16
+    rows = []
+    for pp, tp in EST_CONFIGS:
+        shape, nL = E.tp_shard(base, tp), 80 // pp
+        log(f"[bench] PP{pp}/TP{tp}: {nL} layers of {shape.name}")
+        cfg = model_config(shape, "bf16")
+        weights = [pack_layer(cfg, device_layer_weights(shape, seed, l, "bf16"), free_source=True)
+                   for l in range(nL)]
+        bt = torch.from_numpy(synth.make_block_tables(
+            [EST_S_IN + EST_S_OUT] * Bmax, nbs, synth.BlockAllocator(Bmax * nbs + 1, seed))).to(dev)
+        st = DeviceStage(shape, "bf16", 0, weights, Bmax * nbs + 1, max_tokens=2048,
+                         max_seqs=Bmax, packed=True)
+        x = torch.empty((2048, shape.hidden), dtype=torch.bfloat16, device=dev).normal_()
+        out = torch.empty_like(x)
+
+        def run(B):
+            steps = synth.chunk_schedule([EST_S_IN] * B, 2048)
+            tabs = [bt[[i for i, _, _ in stp]].contiguous() for stp in steps]
+            ev[0].record(stream)
+            for stp, tb in zip(steps, tabs):
+                T = sum(q for _, _, q in stp)
+                st.prefill([q for _, _, q in stp], [c for _, c, _ in stp], tb, x[:T], out[:T],
+                           stream=sp)
+            ev[1].record(stream)
+            for t in range(1, EST_S_OUT + 1):
+                st.decode(np.full(B, EST_S_IN + t - 1, np.int32), bt[:B], x[:B], out[:B],
+                          stream=sp)
+            ev[2].record(stream)
+            torch.cuda.synchronize()
+            return ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2])
+
+        run(EST_BATCHES[0])  # warm-up
+        for B in EST_BATCHES:
+            pf, dc = run(B)
+            ppf, pdc = E.static_batch_ms(shape, nL, B, EST_S_IN, EST_S_OUT, cal, prefill_chunk=2048)
+            dpf, ddc = E.static_batch_ms(shape, nL, B, EST_S_IN, EST_S_OUT, E.DATASHEET,
+                                         prefill_chunk=2048)
+            rows.append({"pp": pp, "tp": tp, "layers": nL, "batch": B,
+                         "measured_ms": {"prefill": round(pf, 2), "decode": round(dc, 2)},
+                         "predicted_ms": {"prefill": round(ppf, 2), "decode": round(pdc, 2)},
+                         "datasheet_ms": {"prefill": round(dpf, 2), "decode": round(ddc, 2)}})
+            log(f"[bench]   B={B:2d}: measured {pf:8.1f} + {dc:8.1f} ms, predicted {ppf:8.1f} + "
+                f"{pdc:8.1f} ms ({(ppf + pdc) / (pf + dc) - 1:+.1%})")
+        st.close()
+        del weights, st
+        torch.cuda.empty_cache()
+
+    def err(key, part=None):
+        get = (lambda r, k: r[k]["prefill"] + r[k]["decode"]) if part is None else \
+            (lambda r, k: r[k][part])
+        return round(E.mape([get(r, key) for r in rows], [get(r, "measured_ms") for r in rows]), 2)
+
+    res = {"workload": "estimator: Llama-3.1-70B, PP x TP in {8x1, 4x2, 2x4, 1x8}, one rank's "
+                       "stage at its shard shape; static batches B = 1..32 of 763-token prompts "
+                       "(2048-token prefill steps) and 232 decode steps",
+           "calibration": {"tflops": round(cal.tflops, 1), "gbs": round(cal.gbs, 1),
+                           "gemm_tflops": {k: round(v, 1) for k, v in cal.gemm_samples.items()},
+                           "gemv_gbs": {k: round(v, 1) for k, v in cal.gemv_samples.items()},
+                           "seconds": round(cal_s, 1)},
+           "mape_pct": {"calibrated": err("predicted_ms"), "datasheet": err("datasheet_ms"),
+                        "calibrated_prefill": err("predicted_ms", "prefill"),
+                        "calibrated_decode": err("predicted_ms", "decode")},
+           "points": rows}
+    log(f"[bench] MAPE calibrated {res['mape_pct']['calibrated']}%, "
+        f"datasheet {res['mape_pct']['datasheet']}%")
+    return res
+
+
 # The decode gate-up projection is the split-K GEMM instantiated with the
 # fused SwiGLU epilogue (template arguments <m-tiles, 1>).
 GATE_UP_DECODE_KERNEL = r"gemm_skinny_bf16<\d+, ?1>"
@@ -411,10 +507,10 @@ def main():
     ap.add_argument("--arrival-rate", type=float, default=0.0,
                     help="l70-full: Poisson arrivals per second (0: all at t=0)")
     ap.add_argument("--workload", default="l70-decode",
-                    choices=["l70-decode", "q32-mixed", "l70-full", "migrate"],
+                    choices=["l70-decode", "q32-mixed", "l70-full", "migrate", "estimator"],
                     help="l70-decode (default: the metric's workload, plus the chunked prefill "
-                         "of the same stage); q32-mixed, l70-full and migrate print their own "
-                         "line")
+                         "of the same stage); q32-mixed, l70-full, migrate and estimator print "
+                         "their own line")
     ap.add_argument("--summarize-trace", metavar="DIR",
                     help="print a summary of a rocprofv3 kernel trace under DIR and exit")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -443,6 +539,10 @@ def main():
         print(json.dumps({"metric": METRIC, "n_gpus": 1, "steps": args.steps,
                           "warmup": args.warmup, "dtype": "bf16", "data": "synthetic",
                           **bench_q32_mixed(args)}), flush=True)
+        return
+    if args.workload == "estimator":
+        print(json.dumps({"metric": METRIC, "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
+                          **bench_estimator(args)}), flush=True)
         return
     if args.workload == "migrate":
         print(json.dumps({"metric": METRIC, "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
