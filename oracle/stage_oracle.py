@@ -256,6 +256,14 @@ def layer_forward(cfg: OracleConfig, w: Dict[str, np.ndarray], x: np.ndarray,
     return x
 
 
+def lm_head(cfg: OracleConfig, x: np.ndarray, final_norm: np.ndarray,
+            w_lm: np.ndarray) -> np.ndarray:
+    """Logits of the last pipeline stage (Table 2, "Logits Calculation"):
+    the model's final RMSNorm of each selected output row ``x`` ``[n, H]``,
+    then the vocabulary projection ``w_lm`` ``[V, H]``. Returns ``[n, V]``."""
+    return rms_norm(x, final_norm, cfg.rms_eps) @ w_lm.T
+
+
 def stage_forward(cfg: OracleConfig, layers: Sequence[Dict[str, np.ndarray]],
                   x: np.ndarray, seqs: Sequence[SeqSpec],
                   kv_cache: Sequence[Dict[str, np.ndarray]], dtype=np.float64,

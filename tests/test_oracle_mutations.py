@@ -43,6 +43,10 @@ MUTANTS = {
     "qk-norm-skipped-on-k": ("k = rms_norm(k, w[\"k_norm\"], cfg.qk_rms_eps)", "pass"),
     "no-rope-on-k": ("k = rnd(rope(k, pos, cfg.rope_theta))", "k = rnd(k)"),
     "positions-ignore-context": ("np.arange(s.ctx_len, s.ctx_len + s.q_len)", "np.arange(0, s.q_len)"),
+    "lm-head-no-final-norm": ("return rms_norm(x, final_norm, cfg.rms_eps) @ w_lm.T",
+                              "return x @ w_lm.T"),
+    "lm-head-gain-ignored": ("return rms_norm(x, final_norm, cfg.rms_eps) @ w_lm.T",
+                             "return rms_norm(x, 1.0, cfg.rms_eps) @ w_lm.T"),
     "slot-wrong-block": ("return int(block_table[p // block_size]), p % block_size",
                          "return int(block_table[p % len(block_table)]), p % block_size"),
 }

@@ -413,3 +413,55 @@ def test_bf16_emulation_stays_close_and_default_is_exact():
                          rounding=O.round_to_bf16)
     e = rel_l2(ye, y)
     assert 1e-4 < e < 2e-2
+
+
+# --------------------------------------------------------------------------
+# LM head of the last stage: final RMSNorm + vocabulary projection
+# --------------------------------------------------------------------------
+
+def test_lm_head_hand_example():
+    """H = 2, x = (3, 4): rms = sqrt(12.5); gain (1, 2); three vocabulary
+    rows (1, 0), (0, 1), (1, 1)."""
+    cfg = O.OracleConfig(hidden=2, n_q_heads=1, n_kv_heads=1, head_dim=2, ffn=2, rms_eps=0.0,
+                         rope_theta=1e4)
+    r = np.sqrt(12.5)
+    y = O.lm_head(cfg, np.array([[3.0, 4.0]]), np.array([1.0, 2.0]),
+                  np.array([[1.0, 0.0], [0.0, 1.0], [1.0, 1.0]]))
+    np.testing.assert_allclose(y, [[3 / r, 8 / r, 11 / r]], rtol=1e-15)
+
+
+def test_lm_head_constant_row_gives_row_sums_of_scaled_weight():
+    """A constant row normalises to all ones (eps = 0), so logits = W g,
+    whatever the constant; and the logits do not depend on the row's scale."""
+    rng = np.random.default_rng(5)
+    H, V = 64, 40
+    cfg = O.OracleConfig(hidden=H, n_q_heads=1, n_kv_heads=1, head_dim=64, ffn=64, rms_eps=0.0,
+                         rope_theta=1e4)
+    g = rng.uniform(0.5, 1.5, H)
+    w = rng.standard_normal((V, H))
+    for c in (-3.0, 0.25, 7.0):
+        y = O.lm_head(cfg, np.full((1, H), c), g, w)
+        np.testing.assert_allclose(y[0], np.sign(c) * (w @ g), rtol=1e-12)
+    x = rng.standard_normal((3, H))
+    np.testing.assert_allclose(O.lm_head(cfg, 5.0 * x, g, w), O.lm_head(cfg, x, g, w), rtol=1e-12)
+
+
+def test_lm_head_matches_transformers_norm_and_linear():
+    """transformers' Llama final norm and LM head (random init, float64 weights;
+    its RMSNorm computes in float32 internally, so agreement is ~1e-7 while a
+    wiring error is O(1))."""
+    from transformers.models.llama.modeling_llama import LlamaRMSNorm
+    rng = np.random.default_rng(6)
+    H, V, n = 96, 200, 5
+    cfg = O.OracleConfig(hidden=H, n_q_heads=1, n_kv_heads=1, head_dim=96, ffn=96, rms_eps=1e-5,
+                         rope_theta=1e4)
+    g = rng.uniform(0.5, 1.5, H)
+    w = rng.standard_normal((V, H)) / np.sqrt(H)
+    x = rng.standard_normal((n, H))
+    norm = LlamaRMSNorm(H, eps=1e-5).double()
+    head = torch.nn.Linear(H, V, bias=False).double()
+    with torch.no_grad():
+        norm.weight.copy_(torch.tensor(g))
+        head.weight.copy_(torch.tensor(w))
+        ref = head(norm(torch.tensor(x))).numpy()
+    assert rel_l2(O.lm_head(cfg, x, g, w), ref) < 1e-6
