@@ -212,8 +212,10 @@ def bench_estimator(args):
     dev = torch.device("cuda:0")
     base, seed = synth.LLAMA70B, args.seed
     t0 = time.time()
-    cal = E.calibrate(base, seed, log=log)
+    cal_l = E.calibrate(base, seed, log=log)
     cal_s = time.time() - t0
+    # the paper's Eq. 1 alone, and with the per-launch cost
+    cal = E.Calibration(cal_l.tflops, cal_l.gbs, 0.0, cal_l.gemm_samples, cal_l.gemv_samples)
     stream = torch.cuda.current_stream()
     sp = stream.cuda_stream
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
@@ -254,10 +256,13 @@ def bench_estimator(args):
             ppf, pdc = E.static_batch_ms(shape, nL, B, EST_S_IN, EST_S_OUT, cal, prefill_chunk=2048)
             dpf, ddc = E.static_batch_ms(shape, nL, B, EST_S_IN, EST_S_OUT, E.DATASHEET,
                                          prefill_chunk=2048)
+            lpf, ldc = E.static_batch_ms(shape, nL, B, EST_S_IN, EST_S_OUT, cal_l,
+                                         prefill_chunk=2048)
             rows.append({"pp": pp, "tp": tp, "layers": nL, "batch": B,
                          "measured_ms": {"prefill": round(pf, 2), "decode": round(dc, 2)},
                          "predicted_ms": {"prefill": round(ppf, 2), "decode": round(pdc, 2)},
-                         "datasheet_ms": {"prefill": round(dpf, 2), "decode": round(ddc, 2)}})
+                         "datasheet_ms": {"prefill": round(dpf, 2), "decode": round(ddc, 2)},
+                         "with_launch_ms": {"prefill": round(lpf, 2), "decode": round(ldc, 2)}})
             log(f"[bench]   B={B:2d}: measured {pf:8.1f} + {dc:8.1f} ms, predicted {ppf:8.1f} + "
                 f"{pdc:8.1f} ms ({(ppf + pdc) / (pf + dc) - 1:+.1%})")
         st.close()
@@ -273,15 +278,70 @@ def bench_estimator(args):
                        "stage at its shard shape; static batches B = 1..32 of 763-token prompts "
                        "(2048-token prefill steps) and 232 decode steps",
            "calibration": {"tflops": round(cal.tflops, 1), "gbs": round(cal.gbs, 1),
+                           "launch_us": round(cal_l.launch_us, 2),
                            "gemm_tflops": {k: round(v, 1) for k, v in cal.gemm_samples.items()},
                            "gemv_gbs": {k: round(v, 1) for k, v in cal.gemv_samples.items()},
                            "seconds": round(cal_s, 1)},
            "mape_pct": {"calibrated": err("predicted_ms"), "datasheet": err("datasheet_ms"),
+                        "calibrated_with_launch": err("with_launch_ms"),
                         "calibrated_prefill": err("predicted_ms", "prefill"),
                         "calibrated_decode": err("predicted_ms", "decode")},
            "points": rows}
     log(f"[bench] MAPE calibrated {res['mape_pct']['calibrated']}%, "
+        f"with launch cost {res['mape_pct']['calibrated_with_launch']}%, "
         f"datasheet {res['mape_pct']['datasheet']}%")
+    return res
+
+
+def bench_lm_head(args):
+    """The last stage's LM head on the Llama-3.1-70B shape (vocab 128256):
+    final RMSNorm + logits of 64 decode rows, of the last rows of 8 prompts,
+    and of 256 rows (the tiled GEMM); HBM roofline of the weight read."""
+    import torch
+    from paper_2606_18600_amd import stage as S
+    from paper_2606_18600_amd import synth
+    from paper_2606_18600_amd.harness import (DeviceStage, device_layer_weights, model_config,
+                                              pack_lm_head)
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    shape, seed, V = synth.LLAMA70B, args.seed, 128256
+    cfg = model_config(shape, "bf16")
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    w = torch.empty((V, shape.hidden), dtype=torch.bfloat16, device=dev).normal_(0, 0.02,
+                                                                                generator=g)
+    wp = pack_lm_head(cfg, w)
+    del w
+    gain = torch.empty(shape.hidden, device=dev).normal_(1.0, 0.02, generator=g).to(torch.bfloat16)
+    st = DeviceStage(shape, "bf16", 79, [device_layer_weights(shape, seed, 79, "bf16")], 8, 256, 4)
+    x = torch.empty((256, shape.hidden), dtype=torch.bfloat16, device=dev).normal_(generator=g)
+    logits = torch.empty((256, V), dtype=torch.float32, device=dev)
+    sp = torch.cuda.current_stream().cuda_stream
+    K = max(args.steps, 10)
+    res = {"workload": "lm-head: Llama-3.1-70B final RMSNorm + logits, vocab 128256, hidden 8192",
+           "cases": []}
+    for label, n, rows in (("decode batch 64", 64, None), ("last rows of 8 prompts", 8,
+                                                           list(range(255, 0, -32))),
+                           ("256 rows", 256, None)):
+        call = lambda: st.lm_head(gain, wp, x, rows=rows, n_rows=n, logits=logits[:n], stream=sp)
+        call()
+        torch.cuda.synchronize()
+        S.stage_set_op_timing(st.handle, True)
+        for _ in range(K):
+            call()
+        op_ms, op_n = S.stage_read_op_times(st.handle)
+        S.stage_set_op_timing(st.handle, False)
+        ms = op_ms[S.OP_NAMES.index("lm_head")] / K
+        byts = V * shape.hidden * 2 + n * shape.hidden * 2 + n * V * 4
+        fl = 2.0 * n * V * shape.hidden
+        res["cases"].append({"rows": n, "label": label, "us_per_call": round(ms * 1e3, 1),
+                             "algorithmic_bytes": byts, "GBs": round(byts / (ms / 1e3) / 1e9, 1),
+                             "frac_hbm_peak": round(byts / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+                             "tflops": round(fl / (ms / 1e3) / 1e12, 1)})
+        log(f"[bench] lm-head {label}: {ms * 1e3:.1f} us, {byts / (ms / 1e3) / 1e9:.0f} GB/s, "
+            f"{fl / (ms / 1e3) / 1e12:.0f} TFLOP/s")
+    assert torch.isfinite(logits).all(), "non-finite logits"
+    st.close()
     return res
 
 
@@ -507,10 +567,10 @@ def main():
     ap.add_argument("--arrival-rate", type=float, default=0.0,
                     help="l70-full: Poisson arrivals per second (0: all at t=0)")
     ap.add_argument("--workload", default="l70-decode",
-                    choices=["l70-decode", "q32-mixed", "l70-full", "migrate", "estimator"],
+                    choices=["l70-decode", "q32-mixed", "l70-full", "migrate", "estimator",
+                             "lm-head"],
                     help="l70-decode (default: the metric's workload, plus the chunked prefill "
-                         "of the same stage); q32-mixed, l70-full, migrate and estimator print "
-                         "their own line")
+                         "of the same stage); the others print their own line")
     ap.add_argument("--summarize-trace", metavar="DIR",
                     help="print a summary of a rocprofv3 kernel trace under DIR and exit")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -539,6 +599,10 @@ def main():
         print(json.dumps({"metric": METRIC, "n_gpus": 1, "steps": args.steps,
                           "warmup": args.warmup, "dtype": "bf16", "data": "synthetic",
                           **bench_q32_mixed(args)}), flush=True)
+        return
+    if args.workload == "lm-head":
+        print(json.dumps({"metric": METRIC, "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
+                          **bench_lm_head(args)}), flush=True)
         return
     if args.workload == "estimator":
         print(json.dumps({"metric": METRIC, "n_gpus": 1, "dtype": "bf16", "data": "synthetic",

@@ -197,6 +197,35 @@ stage_status stage_validate_step(const stage_model_config* cfg, int32_t max_toke
                                  int32_t max_seqs, const stage_batch* prefill,
                                  const stage_batch* decode);
 
+/* ---- last stage: LM head ---------------------------------------------- */
+/* Only the last stage of a pipeline turns hidden states into logits: the
+ * model's final RMSNorm (gain final_norm, epsilon cfg.rms_eps) of each
+ * selected row of its output, then the vocabulary projection
+ * logits = norm(x) W_lm^T with W_lm [vocab, hidden] (Table 2, "Logits
+ * Calculation"). A prefill step needs the last row of each sequence, a decode
+ * step every row.
+ *  final_norm: device [hidden] gain (mode dtype).
+ *  w_lm:       device [vocab, hidden] in the stage_pack_lm_head() layout.
+ *  hidden:     device [hidden_rows, hidden] (mode dtype, row-major), e.g. the
+ *              hidden_out of the stage's last forward call.
+ *  rows:       HOST [n_rows] indices into hidden, each in [0, hidden_rows);
+ *              NULL selects rows 0 .. n_rows-1 (then n_rows <= hidden_rows).
+ *  logits:     device float32 [n_rows, vocab], row-major, written.
+ * n_rows <= max_tokens of the stage; bf16 needs vocab % 128 == 0
+ * (STAGE_ERR_UNSUPPORTED otherwise); bad row indices give
+ * STAGE_ERR_INVALID_ARG before anything is enqueued. Uses the stage's
+ * workspace, so it is ordered with the stage's forward calls only on the
+ * same stream. Timed as STAGE_OP_LM_HEAD. */
+stage_status stage_lm_head(stage_t* st, const void* final_norm, const void* w_lm, int32_t vocab,
+                           const void* hidden, int32_t hidden_rows, const int32_t* rows,
+                           int32_t n_rows, float* logits, void* stream);
+
+/* Convert a row-major [vocab, hidden] LM-head matrix (device, mode dtype)
+ * into the layout stage_lm_head reads (the stage_pack_weight fragment
+ * layout; f32: a copy). dst must not overlap src. Meant for load time. */
+stage_status stage_pack_lm_head(const stage_model_config* cfg, int32_t vocab, const void* src,
+                                void* dst, void* stream);
+
 /* ---- measurement hooks ------------------------------------------------ */
 
 /* Operation classes timed by the op-timing hook. */
@@ -208,7 +237,8 @@ typedef enum {
   STAGE_OP_O = 4,         /* output projection + residual */
   STAGE_OP_GATE_UP = 5,   /* gate-up projection (+ SwiGLU when fused) */
   STAGE_OP_DOWN = 6,      /* down projection + residual */
-  STAGE_OP_COUNT = 7
+  STAGE_OP_LM_HEAD = 7,   /* final norm + logits projection (stage_lm_head) */
+  STAGE_OP_COUNT = 8
 } stage_op;
 
 /* Enable (1) or disable (0) HIP-event timing of each op class. While

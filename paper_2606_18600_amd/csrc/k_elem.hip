@@ -47,9 +47,11 @@ __device__ __forceinline__ void store_act4(float* h, int t, int k, int K, float4
 }
 
 // kS: number of split-K partial planes added to x (compile time, so that all
-// of a thread's loads are issued together).
+// of a thread's loads are issued together). With kEmbed, row t reads input
+// row rows[t] (rows == nullptr: row t).
 template <typename InT, typename OutT, bool kEmbed, int kThreads, int kS>
 __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const InT* __restrict__ in,
+                                                           const int32_t* __restrict__ rows,
                                                            float* __restrict__ x,
                                                            const float* __restrict__ part, int T,
                                                            OutT* __restrict__ h,
@@ -58,6 +60,7 @@ __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const InT* __restrict
   constexpr int kVec = 16384 / 4 / kThreads;
   const int t = blockIdx.x;
   const size_t row = (size_t)t * H;
+  const size_t in_row = kEmbed && rows != nullptr ? (size_t)rows[t] * H : row;
   const size_t plane = (size_t)T * H;
   const int H4 = H >> 2;
   __shared__ float red[kThreads / STAGE_WAVE];
@@ -69,7 +72,7 @@ __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const InT* __restrict
     if (i4 < H4) {
       const size_t e = row + 4 * (size_t)i4;
       if constexpr (kEmbed)
-        v[j] = vec4_io<InT>::load(in, e);
+        v[j] = vec4_io<InT>::load(in, in_row + 4 * (size_t)i4);
       else
         v[j] = *(const float4*)(x + e);
       float4 p[kS > 0 ? kS : 1];
@@ -101,13 +104,13 @@ __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const InT* __restrict
 }
 
 template <typename InT, typename OutT, bool kEmbed, int kThreads>
-hipError_t launch_norm_t(const InT* in, float* x, Partials add, OutT* h, const OutT* gain, int T,
-                         int H, float eps, hipStream_t s) {
+hipError_t launch_norm_t(const InT* in, const int32_t* rows, float* x, Partials add, OutT* h,
+                         const OutT* gain, int T, int H, float eps, hipStream_t s) {
   switch (add.splits) {
-#define STAGE_NORM_CASE(S)                                                                   \
-  case S:                                                                                    \
-    rmsnorm_kernel<InT, OutT, kEmbed, kThreads, S><<<T, kThreads, 0, s>>>(in, x, add.p, T, h, \
-                                                                         gain, H, eps);      \
+#define STAGE_NORM_CASE(S)                                                                  \
+  case S:                                                                                   \
+    rmsnorm_kernel<InT, OutT, kEmbed, kThreads, S><<<T, kThreads, 0, s>>>(in, rows, x, add.p, \
+                                                                         T, h, gain, H, eps); \
     break;
     STAGE_NORM_CASE(0)
     STAGE_NORM_CASE(1)
@@ -127,10 +130,11 @@ hipError_t launch_norm_t(const InT* in, float* x, Partials add, OutT* h, const O
 
 // Wide rows get 1024 threads (more loads in flight per row), narrow ones 256.
 template <typename InT, typename OutT, bool kEmbed>
-hipError_t launch_norm(const InT* in, float* x, Partials add, OutT* h, const OutT* gain, int T,
-                       int H, float eps, hipStream_t s) {
-  if (H >= 4096) return launch_norm_t<InT, OutT, kEmbed, 1024>(in, x, add, h, gain, T, H, eps, s);
-  return launch_norm_t<InT, OutT, kEmbed, 256>(in, x, add, h, gain, T, H, eps, s);
+hipError_t launch_norm(const InT* in, const int32_t* rows, float* x, Partials add, OutT* h,
+                       const OutT* gain, int T, int H, float eps, hipStream_t s) {
+  if (H >= 4096)
+    return launch_norm_t<InT, OutT, kEmbed, 1024>(in, rows, x, add, h, gain, T, H, eps, s);
+  return launch_norm_t<InT, OutT, kEmbed, 256>(in, rows, x, add, h, gain, T, H, eps, s);
 }
 
 template <typename OutT>
@@ -186,11 +190,13 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(const float* __restrict__ 
   const T* gain = is_q ? q_gain : k_gain;
 
   float a = 0.f, b = 0.f;
-  if (act)
+  if (act) {
+#pragma unroll 8
     for (int sp = 0; sp < splits; ++sp) {
       a += row[sp * plane + col + lane];
       b += row[sp * plane + col + lane + half];
     }
+  }
   if (gain != nullptr) {
     const float ss = wave_sum(a * a + b * b);
     const float r = 1.0f / sqrtf(ss / (float)d + qk_eps);
@@ -219,6 +225,7 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(const float* __restrict__ 
   elem<T>::store(kplane, kv_k_offset(off, lane + half), rb);
   const int vcol = (n_q + n_kv + kh) * d;
   float va = 0.f, vb = 0.f;
+#pragma unroll 8
   for (int sp = 0; sp < splits; ++sp) {
     va += row[sp * plane + vcol + lane];
     vb += row[sp * plane + vcol + lane + half];
@@ -288,13 +295,13 @@ __global__ __launch_bounds__(256) void copy_probe_kernel(const u32x4_t* __restri
 }
 
 hipError_t embed_norm(DType dt, const void* hidden_in, float* x, void* h, const void* gain, int T,
-                      int H, float eps, hipStream_t s) {
+                      int H, float eps, hipStream_t s, const int32_t* rows) {
   if (T == 0) return hipSuccess;
   const Partials none{nullptr, 0};
   if (dt == DT_BF16)
-    return launch_norm<bf16_t, bf16_t, true>((const bf16_t*)hidden_in, x, none, (bf16_t*)h,
+    return launch_norm<bf16_t, bf16_t, true>((const bf16_t*)hidden_in, rows, x, none, (bf16_t*)h,
                                              (const bf16_t*)gain, T, H, eps, s);
-  return launch_norm<float, float, true>((const float*)hidden_in, x, none, (float*)h,
+  return launch_norm<float, float, true>((const float*)hidden_in, rows, x, none, (float*)h,
                                          (const float*)gain, T, H, eps, s);
 }
 
@@ -302,10 +309,10 @@ hipError_t rmsnorm(DType dt, float* x, Partials add, void* h, const void* gain, 
                    float eps, hipStream_t s) {
   if (T == 0) return hipSuccess;
   if (dt == DT_BF16)
-    return launch_norm<float, bf16_t, false>(nullptr, x, add, (bf16_t*)h, (const bf16_t*)gain, T,
-                                             H, eps, s);
-  return launch_norm<float, float, false>(nullptr, x, add, (float*)h, (const float*)gain, T, H,
-                                          eps, s);
+    return launch_norm<float, bf16_t, false>(nullptr, nullptr, x, add, (bf16_t*)h,
+                                             (const bf16_t*)gain, T, H, eps, s);
+  return launch_norm<float, float, false>(nullptr, nullptr, x, add, (float*)h, (const float*)gain,
+                                          T, H, eps, s);
 }
 
 hipError_t output_cast(DType dt, const float* x, Partials add, void* out, int T, int H,

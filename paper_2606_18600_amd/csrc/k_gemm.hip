@@ -414,10 +414,10 @@ int skinny_kb_len(int K, int splits) {
   return (kb + 63) / 64 * 64;
 }
 
-int skinny_splits(int N, int K, int target_blocks) {
+int skinny_splits(int N, int K, int target_blocks, int max_splits) {
   const int col_blocks = (N / 64 + SK_WAVES - 1) / SK_WAVES;
   int s = std::max(1, target_blocks / col_blocks);
-  s = std::min(s, std::min(kSkinnyMaxSplits, K / 64));
+  s = std::min(s, std::min(max_splits, K / 64));
   // the number of K ranges actually launched after rounding the range up
   const int kb = skinny_kb_len(K, s);
   return (K + kb - 1) / kb;

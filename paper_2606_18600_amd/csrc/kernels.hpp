@@ -64,9 +64,10 @@ struct Partials {
 };
 
 // x = fp32(hidden_in); h = RMSNorm(x) * gain. bf16 mode writes h in the packed
-// activation layout, fp32 mode row-major.
+// activation layout, fp32 mode row-major. With rows (device, T entries), row t
+// of x and h comes from row rows[t] of hidden_in.
 hipError_t embed_norm(DType dt, const void* hidden_in, float* x, void* h, const void* gain,
-                      int T, int H, float eps, hipStream_t s);
+                      int T, int H, float eps, hipStream_t s, const int32_t* rows = nullptr);
 // x += sum of the partials; h = RMSNorm(x) * gain (layout as above).
 hipError_t rmsnorm(DType dt, float* x, Partials add, void* h, const void* gain, int T, int H,
                    float eps, hipStream_t s);
@@ -95,11 +96,15 @@ hipError_t copy_probe(const void* src, void* dst, size_t bytes, hipStream_t s);
 // GEMMs. gemm_skinny (bf16, M <= 128): packed A and W; writes `splits` fp32
 // partial planes [splits][M][N] into out, or with swiglu (splits == 1) the
 // SwiGLU product in the packed activation layout [M, N/2].
-// Split-K partial planes a consumer (RMSNorm, RoPE, SwiGLU) accepts.
+// Split-K partial planes RMSNorm and SwiGLU accept (their loads are unrolled
+// over a compile-time count), and the larger number the RoPE / KV-write
+// kernel sums in a loop: a narrow QKV projection (one tensor-parallel
+// rank's heads) needs many K ranges to occupy the chip.
 constexpr int kSkinnyMaxSplits = 8;
+constexpr int kSkinnyMaxQkvSplits = 32;
 // K splits for an [M <= 128] x [N, K] decode GEMM: as many as keep the launch
-// at <= target_blocks blocks of 4 waves (at most kSkinnyMaxSplits).
-int skinny_splits(int N, int K, int target_blocks);
+// at <= target_blocks blocks of 4 waves (at most max_splits).
+int skinny_splits(int N, int K, int target_blocks, int max_splits = kSkinnyMaxSplits);
 int skinny_kb_len(int K, int splits);
 hipError_t gemm_skinny(const void* A, const void* W, int M, int N, int K, int splits, bool swiglu,
                        void* out, hipStream_t s);

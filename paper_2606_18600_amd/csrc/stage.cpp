@@ -298,6 +298,31 @@ hipEvent_t take_event(stage* st) {
   return e;
 }
 
+// Take the next pinned staging slot of the ring, waiting until the upload
+// that last used it has been consumed.
+stage_status take_slot(stage* st, int* slot) {
+  const int sl = st->ring;
+  st->ring = (st->ring + 1) % kRing;
+  if (st->staging_used[sl]) {
+    hipError_t e = hipEventSynchronize(st->staging_ev[sl]);
+    if (e != hipSuccess) return hip_fail("staging event", e);
+  }
+  *slot = sl;
+  return STAGE_OK;
+}
+
+// Upload `ints` int32 values from staging slot `slot` to the workspace
+// metadata region, in stream order.
+stage_status upload_slot(stage* st, int slot, size_t ints, hipStream_t s) {
+  hipError_t e = hipMemcpyAsync(st->ws + st->r_meta.off, st->staging[slot], ints * 4,
+                                hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) return hip_fail("metadata upload", e);
+  e = hipEventRecord(st->staging_ev[slot], s);
+  if (e != hipSuccess) return hip_fail("metadata event", e);
+  st->staging_used[slot] = true;
+  return STAGE_OK;
+}
+
 // Launch helper: brackets a launch with timing events when enabled.
 struct Launcher {
   stage* st;
@@ -338,29 +363,21 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
   hipError_t e = hipSetDevice(st->device);
   if (e != hipSuccess) return hip_fail("hipSetDevice", e);
 
+  const int np = pf ? pf->num_seqs : 0, nd = dc ? dc->num_seqs : 0;
+  const DType dt = (DType)c.dtype;
+  const bool skinny = dt == DT_BF16 && T <= st->skinny_rows;
+
   // metadata: host build in a pinned staging slot, one async upload
-  const int slot = st->ring;
-  st->ring = (st->ring + 1) % kRing;
-  if (st->staging_used[slot]) {
-    e = hipEventSynchronize(st->staging_ev[slot]);
-    if (e != hipSuccess) return hip_fail("staging event", e);
-  }
+  int slot = 0;
+  if ((vs = take_slot(st, &slot)) != STAGE_OK) return vs;
   StepMeta hm = meta_view(st, st->staging[slot]);
   build_meta(st, pf, dc, hm);
-  e = hipMemcpyAsync(st->ws + st->r_meta.off, st->staging[slot], st->meta_ints * 4,
-                     hipMemcpyHostToDevice, s);
-  if (e != hipSuccess) return hip_fail("metadata upload", e);
-  e = hipEventRecord(st->staging_ev[slot], s);
-  if (e != hipSuccess) return hip_fail("metadata event", e);
-  st->staging_used[slot] = true;
+  if ((vs = upload_slot(st, slot, st->meta_ints, s)) != STAGE_OK) return vs;
   StepMeta dm = meta_view(st, st->at<int32_t>(st->r_meta));
 
-  const DType dt = (DType)c.dtype;
   const int H = c.hidden, D = c.head_dim, nq = c.n_q_heads, nkv = c.n_kv_heads, F = c.ffn;
   const int qw = nq * D, qkvw = (nq + 2 * nkv) * D;
-  const int np = pf ? pf->num_seqs : 0, nd = dc ? dc->num_seqs : 0;
   const int Tp = T - nd;
-  const bool skinny = dt == DT_BF16 && T <= st->skinny_rows;
   SegTables tabs{pf && np ? pf->block_tables : nullptr, pf && np ? pf->max_blocks_per_seq : 0, np,
                  dc && nd ? dc->block_tables : nullptr, dc && nd ? dc->max_blocks_per_seq : 0};
 
@@ -375,86 +392,96 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
   const float* cos_t = st->at<float>(st->r_cos);
   const float* sin_t = st->at<float>(st->r_sin);
 
-  // Split-K steps leave the O / down projections as partial sums in part_x;
-  // the next RMSNorm (or the output cast) adds them to the residual stream.
-  Partials pending{nullptr, 0};
-  Launcher L{st, s};
-  for (int li = 0; li < st->n_layers; ++li) {
-    const stage_layer_weights& w = st->layers[li];
-    KVLayer kvl{st->kv_pool + (size_t)li * st->kv_layer_bytes, nkv, D};
-    if (li == 0)
-      L(STAGE_OP_NORM, [&] { return embed_norm(dt, hin, x, h, w.attn_norm, T, H, c.rms_eps, s); });
-    else
-      L(STAGE_OP_NORM, [&] { return rmsnorm(dt, x, pending, h, w.attn_norm, T, H, c.rms_eps, s); });
+  // The layer loop on stream ls. Split-K steps leave the O / down
+  // projections as partial sums in part_x; the next RMSNorm (or the output
+  // cast) adds them to the residual stream. The first layer's input norm
+  // (which reads hidden_in) is launched before it.
+  auto layers = [&](Launcher& L, hipStream_t ls) {
+    Partials pending{nullptr, 0};
+    for (int li = 0; li < st->n_layers; ++li) {
+      const stage_layer_weights& w = st->layers[li];
+      KVLayer kvl{st->kv_pool + (size_t)li * st->kv_layer_bytes, nkv, D};
+      if (li > 0)
+        L(STAGE_OP_NORM, [&] { return rmsnorm(dt, x, pending, h, w.attn_norm, T, H, c.rms_eps, ls); });
 
-    int qkv_splits = 1;
-    if (skinny) {
-      qkv_splits = st->s_qkv;
-      L(STAGE_OP_QKV, [&] { return gemm_skinny(h, w.w_qkv, T, qkvw, H, st->s_qkv, false, qkv, s); });
-    } else {
-      L(STAGE_OP_QKV, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_qkv, T, qkvw, H, qkv, s); });
-    }
-    L(STAGE_OP_ROPE_KV, [&] {
-      return rope_kv_write(dt, qkv, qkv_splits, q, kvl, dm.tok_seq, dm.tok_pos, tabs, cos_t,
-                           sin_t, c.qk_norm ? w.q_norm : nullptr, c.qk_norm ? w.k_norm : nullptr,
-                           c.qk_rms_eps, T, nq, s);
-    });
-
-    if (dt == DT_F32) {
-      L(STAGE_OP_ATTN, [&] {
-        return attn_f32((const float*)q, kvl, tabs, dm.tok_seq, dm.tok_pos, 0, T, nq,
-                        (float*)attn, s);
-      });
-    } else {
-      if (Tp > 0)
-        L(STAGE_OP_ATTN, [&] {
-          return attn_prefill(dt, q, kvl, tabs, dm.pitems, hm.n_pitems, nq, st->pf_tiles, attn, s);
-        });
-      if (nd > 0) {
-        L(STAGE_OP_ATTN, [&] {
-          return attn_decode(dt, q, kvl, tabs, dm.ditems, hm.n_ditems, nq,
-                             st->at<float>(st->r_part_o), st->at<float>(st->r_part_ml), s);
-        });
-        L(STAGE_OP_ATTN, [&] {
-          return attn_merge(dt, st->at<float>(st->r_part_o), st->at<float>(st->r_part_ml),
-                            dm.item_start, dm.tok_rows, nd, nq, nkv, D, attn, s);
-        });
-      }
-    }
-
-    if (skinny) {
-      L(STAGE_OP_O, [&] { return gemm_skinny(attn, w.w_o, T, H, qw, st->s_o, false, part_x, s); });
-      pending = Partials{part_x, st->s_o};
-    } else {
-      L(STAGE_OP_O, [&] { return gemm(dt, EPI_RESID_ADD, attn, w.w_o, T, H, qw, x, s); });
-    }
-
-    L(STAGE_OP_NORM, [&] { return rmsnorm(dt, x, pending, h, w.ffn_norm, T, H, c.rms_eps, s); });
-    pending = Partials{nullptr, 0};
-
-    if (skinny) {
-      if (st->s_gu == 1) {
-        L(STAGE_OP_GATE_UP, [&] { return gemm_skinny(h, w.w_gate_up, T, 2 * F, H, 1, true, m, s); });
+      int qkv_splits = 1;
+      if (skinny) {
+        qkv_splits = st->s_qkv;
+        L(STAGE_OP_QKV, [&] { return gemm_skinny(h, w.w_qkv, T, qkvw, H, st->s_qkv, false, qkv, ls); });
       } else {
-        L(STAGE_OP_GATE_UP, [&] {
-          return gemm_skinny(h, w.w_gate_up, T, 2 * F, H, st->s_gu, false, gu, s);
-        });
-        L(STAGE_OP_NORM, [&] {
-          return swiglu_reduce_bf16(Partials{gu, st->s_gu}, (uint16_t*)m, T, F, s);
-        });
+        L(STAGE_OP_QKV, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_qkv, T, qkvw, H, qkv, ls); });
       }
-      L(STAGE_OP_DOWN, [&] { return gemm_skinny(m, w.w_down, T, H, F, st->s_down, false, part_x, s); });
-      pending = Partials{part_x, st->s_down};
-    } else if (dt == DT_BF16) {
-      L(STAGE_OP_GATE_UP, [&] { return gemm(dt, EPI_SWIGLU, h, w.w_gate_up, T, 2 * F, H, m, s); });
-      L(STAGE_OP_DOWN, [&] { return gemm(dt, EPI_RESID_ADD, m, w.w_down, T, H, F, x, s); });
-    } else {
-      L(STAGE_OP_GATE_UP, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_gate_up, T, 2 * F, H, gu, s); });
-      L(STAGE_OP_NORM, [&] { return swiglu_f32(gu, (float*)m, T, F, s); });
-      L(STAGE_OP_DOWN, [&] { return gemm(dt, EPI_RESID_ADD, m, w.w_down, T, H, F, x, s); });
+      L(STAGE_OP_ROPE_KV, [&] {
+        return rope_kv_write(dt, qkv, qkv_splits, q, kvl, dm.tok_seq, dm.tok_pos, tabs, cos_t,
+                             sin_t, c.qk_norm ? w.q_norm : nullptr, c.qk_norm ? w.k_norm : nullptr,
+                             c.qk_rms_eps, T, nq, ls);
+      });
+
+      if (dt == DT_F32) {
+        L(STAGE_OP_ATTN, [&] {
+          return attn_f32((const float*)q, kvl, tabs, dm.tok_seq, dm.tok_pos, 0, T, nq,
+                          (float*)attn, ls);
+        });
+      } else {
+        if (Tp > 0)
+          L(STAGE_OP_ATTN, [&] {
+            return attn_prefill(dt, q, kvl, tabs, dm.pitems, hm.n_pitems, nq, st->pf_tiles, attn,
+                                ls);
+          });
+        if (nd > 0) {
+          L(STAGE_OP_ATTN, [&] {
+            return attn_decode(dt, q, kvl, tabs, dm.ditems, hm.n_ditems, nq,
+                               st->at<float>(st->r_part_o), st->at<float>(st->r_part_ml), ls);
+          });
+          L(STAGE_OP_ATTN, [&] {
+            return attn_merge(dt, st->at<float>(st->r_part_o), st->at<float>(st->r_part_ml),
+                              dm.item_start, dm.tok_rows, nd, nq, nkv, D, attn, ls);
+          });
+        }
+      }
+
+      if (skinny) {
+        L(STAGE_OP_O, [&] { return gemm_skinny(attn, w.w_o, T, H, qw, st->s_o, false, part_x, ls); });
+        pending = Partials{part_x, st->s_o};
+      } else {
+        L(STAGE_OP_O, [&] { return gemm(dt, EPI_RESID_ADD, attn, w.w_o, T, H, qw, x, ls); });
+      }
+
+      L(STAGE_OP_NORM, [&] { return rmsnorm(dt, x, pending, h, w.ffn_norm, T, H, c.rms_eps, ls); });
+      pending = Partials{nullptr, 0};
+
+      if (skinny) {
+        if (st->s_gu == 1) {
+          L(STAGE_OP_GATE_UP, [&] { return gemm_skinny(h, w.w_gate_up, T, 2 * F, H, 1, true, m, ls); });
+        } else {
+          L(STAGE_OP_GATE_UP, [&] {
+            return gemm_skinny(h, w.w_gate_up, T, 2 * F, H, st->s_gu, false, gu, ls);
+          });
+          L(STAGE_OP_NORM, [&] {
+            return swiglu_reduce_bf16(Partials{gu, st->s_gu}, (uint16_t*)m, T, F, ls);
+          });
+        }
+        L(STAGE_OP_DOWN, [&] { return gemm_skinny(m, w.w_down, T, H, F, st->s_down, false, part_x, ls); });
+        pending = Partials{part_x, st->s_down};
+      } else if (dt == DT_BF16) {
+        L(STAGE_OP_GATE_UP, [&] { return gemm(dt, EPI_SWIGLU, h, w.w_gate_up, T, 2 * F, H, m, ls); });
+        L(STAGE_OP_DOWN, [&] { return gemm(dt, EPI_RESID_ADD, m, w.w_down, T, H, F, x, ls); });
+      } else {
+        L(STAGE_OP_GATE_UP, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_gate_up, T, 2 * F, H, gu, ls); });
+        L(STAGE_OP_NORM, [&] { return swiglu_f32(gu, (float*)m, T, F, ls); });
+        L(STAGE_OP_DOWN, [&] { return gemm(dt, EPI_RESID_ADD, m, w.w_down, T, H, F, x, ls); });
+      }
     }
-  }
-  L(STAGE_OP_NORM, [&] { return output_cast(dt, x, pending, hout, T, H, s); });
+  };
+  // what the last layer leaves for the output cast
+  const Partials tail = skinny ? Partials{part_x, st->s_down} : Partials{nullptr, 0};
+
+  Launcher L{st, s};
+  L(STAGE_OP_NORM, [&] {
+    return embed_norm(dt, hin, x, h, st->layers[0].attn_norm, T, H, c.rms_eps, s);
+  });
+  layers(L, s);
+  L(STAGE_OP_NORM, [&] { return output_cast(dt, x, tail, hout, T, H, s); });
 
   if (L.err != hipSuccess) return hip_fail("kernel launch", L.err);
   return STAGE_OK;
@@ -521,7 +548,7 @@ stage_status stage_create(const stage_model_config* cfg, int32_t layer_begin, in
     const int blocks = std::max(1, env_int("STAGE_SKINNY_BLOCKS", cus * 9 / 10));
     const int H = cfg->hidden, F = cfg->ffn, qw = cfg->n_q_heads * cfg->head_dim;
     const int qkvw = (cfg->n_q_heads + 2 * cfg->n_kv_heads) * cfg->head_dim;
-    st->s_qkv = skinny_splits(qkvw, H, blocks);
+    st->s_qkv = skinny_splits(qkvw, H, blocks, kSkinnyMaxQkvSplits);
     st->s_o = skinny_splits(H, qw, blocks);
     st->s_gu = skinny_splits(2 * F, H, blocks);
     st->s_down = skinny_splits(H, F, blocks);
@@ -593,6 +620,77 @@ stage_status stage_step_mixed(stage_t* st, const stage_batch* prefill, const sta
                               const void* hidden_in, void* hidden_out, void* stream) {
   if (!st) return fail(STAGE_ERR_INVALID_ARG, "stage is NULL");
   return run_step(st, prefill, decode, hidden_in, hidden_out, stream);
+}
+
+stage_status stage_pack_lm_head(const stage_model_config* cfg, int32_t vocab, const void* src,
+                                void* dst, void* stream) {
+  stage_status v = check_config(cfg);
+  if (v != STAGE_OK) return v;
+  if (!src || !dst) return fail(STAGE_ERR_INVALID_ARG, "src/dst is NULL");
+  if (src == dst) return fail(STAGE_ERR_INVALID_ARG, "packing cannot run in place");
+  if (vocab <= 0) return fail(STAGE_ERR_INVALID_ARG, "vocab must be positive");
+  if (cfg->dtype == STAGE_BF16 && vocab % 128 != 0)
+    return fail(STAGE_ERR_UNSUPPORTED, "vocab %d is not a multiple of 128", vocab);
+  hipStream_t s = (hipStream_t)stream;
+  const int H = cfg->hidden;
+  hipError_t e;
+  if (cfg->dtype == STAGE_F32)
+    e = hipMemcpyAsync(dst, src, (size_t)vocab * H * 4, hipMemcpyDeviceToDevice, s);
+  else
+    e = pack_weight(src, dst, vocab, H, 0, s);
+  if (e != hipSuccess) return hip_fail("pack_weight", e);
+  return STAGE_OK;
+}
+
+stage_status stage_lm_head(stage_t* st, const void* final_norm, const void* w_lm, int32_t vocab,
+                           const void* hidden, int32_t hidden_rows, const int32_t* rows,
+                           int32_t n_rows, float* logits, void* stream) {
+  if (!st) return fail(STAGE_ERR_INVALID_ARG, "stage is NULL");
+  if (!st->ws) return fail(STAGE_ERR_INVALID_ARG, "no workspace bound (stage_bind_workspace)");
+  if (!final_norm || !w_lm || !hidden || !logits)
+    return fail(STAGE_ERR_INVALID_ARG, "final_norm/w_lm/hidden/logits is NULL");
+  const auto& c = st->cfg;
+  if (vocab <= 0 || hidden_rows < 0 || n_rows < 0)
+    return fail(STAGE_ERR_INVALID_ARG, "vocab must be positive, row counts >= 0");
+  if (c.dtype == STAGE_BF16 && vocab % 128 != 0)
+    return fail(STAGE_ERR_UNSUPPORTED, "vocab %d is not a multiple of 128", vocab);
+  if (n_rows == 0) return STAGE_OK;
+  if (n_rows > st->max_tokens)
+    return fail(STAGE_ERR_CAPACITY, "%d rows > max_tokens %d", n_rows, st->max_tokens);
+  if (rows) {
+    for (int i = 0; i < n_rows; ++i)
+      if (rows[i] < 0 || rows[i] >= hidden_rows)
+        return fail(STAGE_ERR_INVALID_ARG, "rows[%d] = %d outside [0, %d)", i, rows[i],
+                    hidden_rows);
+  } else if (n_rows > hidden_rows) {
+    return fail(STAGE_ERR_INVALID_ARG, "%d rows > hidden_rows %d", n_rows, hidden_rows);
+  }
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = hipSetDevice(st->device);
+  if (e != hipSuccess) return hip_fail("hipSetDevice", e);
+  const int32_t* rows_dev = nullptr;
+  if (rows) {
+    int slot = 0;
+    stage_status vs = take_slot(st, &slot);
+    if (vs != STAGE_OK) return vs;
+    std::memcpy(st->staging[slot], rows, (size_t)n_rows * 4);
+    if ((vs = upload_slot(st, slot, n_rows, s)) != STAGE_OK) return vs;
+    rows_dev = st->at<int32_t>(st->r_meta);
+  }
+  const DType dt = (DType)c.dtype;
+  const int H = c.hidden;
+  float* x = st->at<float>(st->r_x);
+  void* h = st->ws + st->r_h.off;
+  Launcher L{st, s};
+  L(STAGE_OP_LM_HEAD, [&] {
+    return embed_norm(dt, hidden, x, h, final_norm, n_rows, H, c.rms_eps, s, rows_dev);
+  });
+  if (dt == DT_BF16 && n_rows <= st->skinny_rows)
+    L(STAGE_OP_LM_HEAD, [&] { return gemm_skinny(h, w_lm, n_rows, vocab, H, 1, false, logits, s); });
+  else
+    L(STAGE_OP_LM_HEAD, [&] { return gemm(dt, EPI_STORE_F32, h, w_lm, n_rows, vocab, H, logits, s); });
+  if (L.err != hipSuccess) return hip_fail("kernel launch", L.err);
+  return STAGE_OK;
 }
 
 stage_status stage_destroy(stage_t* st) {

@@ -25,7 +25,15 @@ The denominators come from a one-time calibration on the device. The
 effective FLOP rate is taken from a compute-bound GEMM and the effective
 bandwidth from a memory-bound GEMV. Each is measured at several batch sizes
 and summarised by the median (Sec. 4.1.1; Sec. 7 "One-time Calibration
-Overhead"). Eq. 3 (requests per second), Eq. 4 (pipeline latency as the
+Overhead").
+
+One refinement goes beyond the paper's formulation. Its Discussion (Sec. 8)
+names kernel-launch overhead as a non-linear cost that Eq. 1 leaves out. On
+MI355X every kernel boundary costs a few microseconds, whatever the kernel
+does. A stage step launches a fixed number of kernels per layer. So the
+calibration also measures one scalar, the mean cost per launch beyond Eq. 1,
+on a one-layer decode step. With `launch_us` > 0, each step adds that much
+per kernel it launches. With `launch_us` = 0 the estimator is Eq. 1 alone. Eq. 3 (requests per second), Eq. 4 (pipeline latency as the
 slowest stage's prefill plus the slowest stage's decode) and the alpha-beta
 communication terms L_PP and L_TP of Sec. 4.1.2 are given for the placement
 optimizer's cost curve. The communication terms take link figures as
@@ -58,6 +66,7 @@ class Calibration:
     per-batch-size samples they were taken from."""
     tflops: float
     gbs: float
+    launch_us: float = 0.0
     gemm_samples: Dict[int, float] = dataclasses.field(default_factory=dict)
     gemv_samples: Dict[int, float] = dataclasses.field(default_factory=dict)
 
@@ -129,6 +138,18 @@ def layer_ms(ops: Sequence[Op], cal: Calibration) -> float:
     return sum(op_ms(o, cal) for o in ops)
 
 
+# Kernels a stage step launches: per layer (prefill: norm, QKV, RoPE/KV
+# write, attention, O, norm, gate-up, down; decode adds the split merge and
+# the SwiGLU reduction of the split-K gate-up), plus the input norm and the
+# output cast of the step.
+KERNELS_PER_LAYER = {"prefill": 8, "decode": 10}
+KERNELS_PER_STEP = 2
+
+
+def step_launches(n_layers: int, phase: str) -> int:
+    return n_layers * KERNELS_PER_LAYER[phase] + KERNELS_PER_STEP
+
+
 def static_batch_ms(shape, n_layers: int, B: int, s_in: int, s_out: int, cal: Calibration,
                     prefill_chunk: Optional[int] = None):
     """(prefill ms, decode ms) of a static batch on a stage of `n_layers`
@@ -143,6 +164,8 @@ def static_batch_ms(shape, n_layers: int, B: int, s_in: int, s_out: int, cal: Ca
     pf = n_layers * sum(layer_ms(prefill_ops(shape, st), cal) for st in steps)
     dc = n_layers * sum(layer_ms(decode_ops(shape, [s_in + t - 1] * B), cal)
                         for t in range(1, s_out + 1))
+    pf += len(steps) * step_launches(n_layers, "prefill") * cal.launch_us * 1e-3
+    dc += s_out * step_launches(n_layers, "decode") * cal.launch_us * 1e-3
     return pf, dc
 
 
@@ -190,7 +213,9 @@ def calibrate(shape, seed: int = 2606, reps: int = 10, log=None) -> Calibration:
     GEMM_TOKENS rows. The memory-bound GEMV is the same projection in decode
     steps of GEMV_BATCHES rows. Each sample is FLOPs (or weight + activation
     bytes) over the projection's mean time from the stage's HIP-event op
-    timers. Each scalar is the median of its samples."""
+    timers. Each scalar is the median of its samples. The launch cost is the
+    median over the same decode steps of (measured step time - Eq. 1 for
+    the layer) / kernels launched."""
     import torch
     from . import stage as S
     from . import synth
@@ -222,21 +247,34 @@ def calibrate(shape, seed: int = 2606, reps: int = 10, log=None) -> Calibration:
         S.stage_set_op_timing(st.handle, False)
         return ms[j] / n[j]
 
-    gemm, gemv = {}, {}
+    def step_ms(call):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        call()
+        e0.record()
+        for _ in range(reps):
+            call()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    gemm, gemv, dec_ms = {}, {}, {}
     try:
         for T in GEMM_TOKENS:
             ms = timed(lambda: st.prefill([T], [0], bt[:1], x[:T], out[:T], stream=sp))
             gemm[T] = 2.0 * T * H * 2 * F / (ms / 1e3) / 1e12
         for B in GEMV_BATCHES:
-            ms = timed(lambda: st.decode(np.full(B, ctx, np.int32), bt[:B], x[:B], out[:B],
-                                         stream=sp))
+            call = lambda: st.decode(np.full(B, ctx, np.int32), bt[:B], x[:B], out[:B], stream=sp)
+            ms = timed(call)
             gemv[B] = 2.0 * (2 * F * H + B * H + B * F) / (ms / 1e3) / 1e9
+            dec_ms[B] = step_ms(call)
     finally:
         st.close()
-    cal = Calibration(float(np.median(list(gemm.values()))), float(np.median(list(gemv.values()))),
-                      gemm, gemv)
+    base = Calibration(float(np.median(list(gemm.values()))), float(np.median(list(gemv.values()))))
+    launch = float(np.median([(dec_ms[B] - layer_ms(decode_ops(shape, [ctx] * B), base)) * 1e3 /
+                              step_launches(1, "decode") for B in GEMV_BATCHES]))
+    cal = Calibration(base.tflops, base.gbs, max(0.0, launch), gemm, gemv)
     if log:
         log(f"[calibrate] GEMM TFLOP/s {', '.join(f'{k}:{v:.0f}' for k, v in gemm.items())} "
             f"-> {cal.tflops:.0f}; GEMV GB/s {', '.join(f'{k}:{v:.0f}' for k, v in gemv.items())} "
-            f"-> {cal.gbs:.0f}")
+            f"-> {cal.gbs:.0f}; launch {cal.launch_us:.2f} us")
     return cal

@@ -88,6 +88,14 @@ def pack_layer(cfg: S.stage_model_config, w: Dict[str, torch.Tensor],
     return out
 
 
+def pack_lm_head(cfg: S.stage_model_config, w_lm: torch.Tensor) -> torch.Tensor:
+    """Row-major [vocab, hidden] LM-head matrix -> the layout stage_lm_head reads."""
+    dst = torch.empty_like(w_lm)
+    S.stage_pack_lm_head(cfg, w_lm.shape[0], w_lm.data_ptr(), dst.data_ptr(),
+                         torch.cuda.current_stream().cuda_stream)
+    return dst
+
+
 class DeviceStage:
     """A stage over row-major weights (packed here through the ABI) or over
     weights already packed (``packed=True``)."""
@@ -150,6 +158,18 @@ class DeviceStage:
             if len(d_ctx_lens) else None
         S.stage_step_mixed(self.handle, pb, db, hidden_in.data_ptr(), out.data_ptr(), stream)
         return out
+
+    def lm_head(self, final_norm: torch.Tensor, w_lm_packed: torch.Tensor, hidden: torch.Tensor,
+                rows=None, n_rows: Optional[int] = None, logits: Optional[torch.Tensor] = None,
+                stream=0) -> torch.Tensor:
+        """Logits [n_rows, vocab] (fp32) of the selected rows of `hidden`."""
+        vocab = w_lm_packed.shape[0]
+        n = len(rows) if rows is not None else (hidden.shape[0] if n_rows is None else n_rows)
+        if logits is None:
+            logits = torch.empty((n, vocab), dtype=torch.float32, device=hidden.device)
+        S.stage_lm_head(self.handle, final_norm.data_ptr(), w_lm_packed.data_ptr(), vocab,
+                        hidden.data_ptr(), hidden.shape[0], rows, n, logits.data_ptr(), stream)
+        return logits
 
     def kv_view(self) -> torch.Tensor:
         s = self.shape

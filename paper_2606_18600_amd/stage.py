@@ -29,13 +29,13 @@ STAGE_ERR_CAPACITY = 5
 STAGE_F32 = 0
 STAGE_BF16 = 1
 
-OP_NAMES = ("norm", "qkv", "rope_kv", "attn", "o_proj", "gate_up", "down")
+OP_NAMES = ("norm", "qkv", "rope_kv", "attn", "o_proj", "gate_up", "down", "lm_head")
 STAGE_OP_COUNT = len(OP_NAMES)
 
 EXPORTED = ("stage_create", "stage_workspace_bytes", "stage_bind_workspace", "stage_prefill",
             "stage_decode", "stage_step_mixed", "stage_destroy", "stage_last_error",
             "stage_validate_step", "stage_set_op_timing", "stage_read_op_times",
-            "stage_pack_weight", "stage_copy_probe")
+            "stage_pack_weight", "stage_copy_probe", "stage_lm_head", "stage_pack_lm_head")
 
 STAGE_W_QKV = 0
 STAGE_W_O = 1
@@ -101,13 +101,15 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                         ctypes.POINTER(stage_batch), ctypes.POINTER(stage_batch)]
     lib.stage_pack_weight.argtypes = [ctypes.POINTER(stage_model_config), i32, P, P, P]
     lib.stage_copy_probe.argtypes = [P, P, ctypes.c_size_t, P]
+    lib.stage_lm_head.argtypes = [P, P, P, i32, P, i32, ctypes.POINTER(ctypes.c_int32), i32, P, P]
+    lib.stage_pack_lm_head.argtypes = [ctypes.POINTER(stage_model_config), i32, P, P, P]
     lib.stage_set_op_timing.argtypes = [P, i32]
     lib.stage_read_op_times.argtypes = [P, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_int64)]
     for name in ("stage_create", "stage_bind_workspace", "stage_prefill", "stage_decode",
                  "stage_step_mixed", "stage_destroy", "stage_validate_step",
                  "stage_set_op_timing", "stage_read_op_times", "stage_pack_weight",
-                 "stage_copy_probe"):
+                 "stage_copy_probe", "stage_lm_head", "stage_pack_lm_head"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -192,6 +194,25 @@ def stage_pack_weight(cfg: stage_model_config, kind: int, src: int, dst: int,
 
 def stage_copy_probe(src: int, dst: int, nbytes: int, stream: int = 0) -> None:
     _check(load_library().stage_copy_probe(src, dst, nbytes, stream))
+
+
+def stage_lm_head(st: int, final_norm: int, w_lm: int, vocab: int, hidden: int,
+                  hidden_rows: int, rows, n_rows: int, logits: int, stream: int = 0) -> None:
+    """``rows``: host int32 indices into ``hidden`` (or None for 0..n_rows-1)."""
+    if rows is None:
+        rp = None
+    else:
+        r = np.ascontiguousarray(rows, dtype=np.int32)
+        if len(r) != n_rows:
+            raise StageError(STAGE_ERR_INVALID_ARG, f"{len(r)} row indices for n_rows={n_rows}")
+        rp = r.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    _check(load_library().stage_lm_head(st, final_norm, w_lm, vocab, hidden, hidden_rows, rp,
+                                        n_rows, logits, stream))
+
+
+def stage_pack_lm_head(cfg: stage_model_config, vocab: int, src: int, dst: int,
+                       stream: int = 0) -> None:
+    _check(load_library().stage_pack_lm_head(ctypes.byref(cfg), vocab, src, dst, stream))
 
 
 def stage_set_op_timing(st: int, enable: bool) -> None:

@@ -153,3 +153,22 @@ def test_copy_probe_rejects_bad_arguments_on_the_host(src, dst, nbytes):
     lib = _lib()
     assert lib.stage_copy_probe(src, dst, nbytes, None) == S.STAGE_ERR_INVALID_ARG
     assert S.stage_last_error()
+
+
+@pytest.mark.parametrize("vocab,src,dst,code", [
+    (1024, 0, 0x2000, S.STAGE_ERR_INVALID_ARG),      # NULL source
+    (1024, 0x1000, 0x1000, S.STAGE_ERR_INVALID_ARG),  # in place
+    (0, 0x1000, 0x2000, S.STAGE_ERR_INVALID_ARG),     # empty vocabulary
+    (1000, 0x1000, 0x2000, S.STAGE_ERR_UNSUPPORTED),  # bf16 vocab not a multiple of 128
+])
+def test_pack_lm_head_rejects_bad_arguments_on_the_host(vocab, src, dst, code):
+    lib = _lib()
+    cfg = model_config(synth.TINY, "bf16")
+    assert lib.stage_pack_lm_head(cfg, vocab, src, dst, None) == code
+    assert S.stage_last_error()
+
+
+def test_lm_head_rejects_a_null_stage():
+    lib = _lib()
+    assert lib.stage_lm_head(None, 0x1000, 0x2000, 1024, 0x3000, 4, None, 4, 0x4000,
+                             None) == S.STAGE_ERR_INVALID_ARG

@@ -124,3 +124,15 @@ def test_throughput_and_communication_terms():
 def test_mape():
     assert E.mape([110, 90], [100, 100]) == pytest.approx(10.0)
     assert E.mape([1.0], [1.0]) == 0.0
+
+
+def test_launch_cost_adds_per_kernel_of_each_step():
+    base = E.Calibration(tflops=1000.0, gbs=5000.0)
+    lat = E.Calibration(tflops=1000.0, gbs=5000.0, launch_us=4.0)
+    n_layers, B, s_in, s_out = 10, 3, 763, 5
+    pf0, dc0 = E.static_batch_ms(L70, n_layers, B, s_in, s_out, base, prefill_chunk=2048)
+    pf1, dc1 = E.static_batch_ms(L70, n_layers, B, s_in, s_out, lat, prefill_chunk=2048)
+    steps = len(synth.chunk_schedule([s_in] * B, 2048))  # 2 steps: 2048 + 241 tokens
+    assert steps == 2
+    assert math.isclose(pf1 - pf0, steps * (n_layers * 8 + 2) * 4.0e-3)
+    assert math.isclose(dc1 - dc0, s_out * (n_layers * 10 + 2) * 4.0e-3)
