@@ -20,6 +20,8 @@
 //   cache), with the causal mask applied per row.
 // * attn_f32_kernel: plain fp32 SIMT attention, one wave per (token, head),
 //   for the fp32 mode.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "packed.hpp"
@@ -29,6 +31,12 @@ namespace stage_k {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+
+// 2^x with the hardware instruction alone. Softmax arguments are <= 8 here
+// and results below 2^-126 are negligible next to the row sum, so the
+// denormal range handling of exp2f (several more instructions per value, on
+// a path bound by these exponentials) is not needed.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 // Online softmax: move the reference maximum only when a block's maximum
 // exceeds it by more than this (log2 units).
 constexpr float kLazyRescale = 8.0f;
@@ -96,11 +104,15 @@ struct VFrag {
 
 // Lanes l, l^16, l^32 and l^48 hold the same row of a 16x16 C tile; combine
 // their values with the gfx950 lane swaps (VALU only, no LDS round trip).
+// IEEE maximum (NaN-propagating): unlike fmaxf it needs no quieting of its
+// operands, and chains of it become three-operand maximum instructions.
+__device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
 __device__ __forceinline__ float row4_max(float x) {
   auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  x = vmax(__uint_as_float(a[0]), __uint_as_float(a[1]));
   auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+  return vmax(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 __device__ __forceinline__ float row4_sum(float x) {
   auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -125,10 +137,10 @@ __device__ __forceinline__ void softmax_pv(f32x4_t s, RowState& st, f32x4_t* oac
   // a finite max, so mn is finite here. (No data-dependent branch here: a
   // branch inside the pipelined key loop makes the compiler wait for every
   // outstanding load at the join.)
-  const float alpha = exp2f(st.m - mn);
+  const float alpha = fast_exp2(st.m - mn);
   float p[4];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) p[r] = exp2f(s[r] - mn);
+  for (int r = 0; r < 4; ++r) p[r] = fast_exp2(s[r] - mn);
   const float ps = row4_sum(p[0] + p[1] + p[2] + p[3]);
   st.l = st.l * alpha + ps;
   st.m = mn;
@@ -323,8 +335,13 @@ constexpr int kPfBPS = 4;
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
+// Two workgroups per CU (64 KB of LDS each) need the register budget of two
+// waves per SIMD; one would leave no other wave to overlap a wave's
+// exponentials with MFMA work. (Four row tiles per wave do not fit that
+// budget and run one wave per SIMD.)
 template <int D, int RT>
-__global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_bf16(
+__global__ __launch_bounds__(kPfWaves * 64) __attribute__((amdgpu_waves_per_eu(RT <= 2 ? 2 : 1)))
+void attn_prefill_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kv, int n_kv, SegTables tabs,
     const PrefillItem* __restrict__ items, int n_q, bf16_t* __restrict__ out) {
   constexpr int BPS = kPfBPS;
@@ -333,6 +350,7 @@ __global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_bf16(
   constexpr int SF = BPS * FR;         // fragments per stage
   constexpr int PER = SF / kPfWaves;   // fragment copies per wave and stage
   static_assert(SF % kPfWaves == 0, "stage split");
+  static_assert(BPS % 2 == 0, "P V products take key blocks in pairs");
   __shared__ u32x4_t lds[2][SF * 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   // Workgroup b runs on XCD b % 8, each XCD with its own L2. Take the kv head
@@ -392,11 +410,11 @@ __global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_bf16(
     }
   };
 
-  ids = fill_window(bt, 0, min(64, nb), lane);
-  issue(0, 0);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  for (int stg = 0; stg < nst; ++stg) {
+  // One stage of BPS key blocks. Stages whose last key is at or before the
+  // first query position of the item need no causal mask (for a long
+  // context, nearly all of them).
+  auto stage = [&](auto masked, int stg) {
+    constexpr bool kMask = decltype(masked)::value;
     const int buf = stg & 1;
     if (stg + 1 < nst) {
       if ((stg + 1) * BPS - wbase >= 64) {
@@ -406,7 +424,7 @@ __global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_bf16(
       issue(stg + 1, buf ^ 1);
     }
     const u32x4_t* L = lds[buf];
-    // scores of the stage: S^T tiles, lane l: row l%16, keys (l/16)*4 + r
+    // raw scores of the stage: S^T tiles, lane l: row l%16, keys (l/16)*4 + r
     f32x4_t sc[RT][BPS];
 #pragma unroll
     for (int bi = 0; bi < BPS; ++bi) {
@@ -419,29 +437,33 @@ __global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_bf16(
         f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int j = 0; j < NJ; ++j) s = mfma16x16x32(kf[j], qf[i][j], s);
+        if constexpr (kMask) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) s[r] = key0 + r <= rpos[i] ? s[r] * scale : -INFINITY;
+          for (int r = 0; r < 4; ++r) s[r] = key0 + r <= rpos[i] ? s[r] : -INFINITY;
+        }
         sc[i][bi] = s;
       }
     }
-    // softmax statistics of the stage; P as bf16 B operands
+    // softmax statistics of the stage (log2 units: score * scale); P as bf16
+    // B operands
     u32x2_t pb[RT][BPS];
 #pragma unroll
     for (int i = 0; i < RT; ++i) {
       float bm = -INFINITY;
 #pragma unroll
       for (int bi = 0; bi < BPS; ++bi)
-        bm = fmaxf(bm, fmaxf(fmaxf(sc[i][bi][0], sc[i][bi][1]), fmaxf(sc[i][bi][2], sc[i][bi][3])));
-      bm = row4_max(bm);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) bm = vmax(bm, sc[i][bi][r]);
+      bm = row4_max(bm) * scale;
       const bool grow = bm > st[i].m + kLazyRescale;
       const float mn = grow ? bm : st[i].m;
-      const float alpha = exp2f(st[i].m - mn);  // 1 unless the maximum moved
+      const float alpha = fast_exp2(st[i].m - mn);  // 1 unless the maximum moved
       float ps = 0.f;
 #pragma unroll
       for (int bi = 0; bi < BPS; ++bi) {
         float p[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) p[r] = exp2f(sc[i][bi][r] - mn);
+        for (int r = 0; r < 4; ++r) p[r] = fast_exp2(fmaf(sc[i][bi][r], scale, -mn));
         ps += (p[0] + p[1]) + (p[2] + p[3]);
         pb[i][bi] = u32x2_t{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3])};
       }
@@ -452,24 +474,55 @@ __global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_bf16(
         for (int t = 0; t < D / 16; ++t) oacc[i][t] *= alpha;
       }
     }
-    // O^T += V^T P^T
+    // O^T += V^T P^T, two key blocks per 16x16x32 product: the k index runs
+    // over keys 4g..4g+3 of the first block and then of the second (g =
+    // lane / 16), in V^T and in P^T alike, which is how both already sit
+    // in registers.
+    // The two 8-byte halves of each operand are read from LDS straight into
+    // adjacent registers. (The reads are volatile so that the compiler does
+    // not merge neighbouring halves into one 16-byte read and then assemble
+    // the operands with register moves; the reads of the next pair of d
+    // tiles are issued before the products of the current pair.)
+    typedef const volatile u32x2_t __attribute__((address_space(3)))* lds_u32x2_ptr;
+    const lds_u32x2_ptr L2 = (lds_u32x2_ptr)L;
+    auto vload = [&](int bp, int t) {
+      const int h = t & 1;  // words 0-1 or 2-3 of the lane's 16 bytes
+      const u32x2_t a0 = L2[((bp * FR + NJ + (t >> 1)) * 64 + lane) * 2 + h];
+      const u32x2_t a1 = L2[(((bp + 1) * FR + NJ + (t >> 1)) * 64 + lane) * 2 + h];
+      return u32x4_t{a0[0], a0[1], a1[0], a1[1]};
+    };
 #pragma unroll
-    for (int bi = 0; bi < BPS; ++bi) {
-      u32x4_t vf[NJ];
+    for (int bp = 0; bp < BPS; bp += 2) {
+      u32x4_t cur0 = vload(bp, 0), cur1 = vload(bp, 1);
 #pragma unroll
-      for (int j = 0; j < NJ; ++j) vf[j] = L[(bi * FR + NJ + j) * 64 + lane];
-#pragma unroll
-      for (int i = 0; i < RT; ++i)
-#pragma unroll
-        for (int t = 0; t < D / 16; ++t) {
-          const u32x4_t& w = vf[t >> 1];
-          const u32x2_t vt = (t & 1) ? u32x2_t{w[2], w[3]} : u32x2_t{w[0], w[1]};
-          oacc[i][t] = mfma16x16x16(vt, pb[i][bi], oacc[i][t]);
+      for (int tp = 0; tp < D / 32; ++tp) {
+        u32x4_t nxt0 = cur0, nxt1 = cur1;
+        if (tp + 1 < D / 32) {
+          nxt0 = vload(bp, 2 * tp + 2);
+          nxt1 = vload(bp, 2 * tp + 3);
         }
+#pragma unroll
+        for (int i = 0; i < RT; ++i) {
+          const u32x4_t pp{pb[i][bp][0], pb[i][bp][1], pb[i][bp + 1][0], pb[i][bp + 1][1]};
+          oacc[i][2 * tp] = mfma16x16x32(cur0, pp, oacc[i][2 * tp]);
+          oacc[i][2 * tp + 1] = mfma16x16x32(cur1, pp, oacc[i][2 * tp + 1]);
+        }
+        cur0 = nxt0;
+        cur1 = nxt1;
+      }
     }
     __builtin_amdgcn_s_waitcnt(0);  // the next stage has landed in LDS
     __syncthreads();
-  }
+  };
+
+  ids = fill_window(bt, 0, min(64, nb), lane);
+  issue(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  const int nfull = min(nst, (it.p0 + 1) / (BPS * kBlock));
+  int stg = 0;
+  for (; stg < nfull; ++stg) stage(std::false_type{}, stg);
+  for (; stg < nst; ++stg) stage(std::true_type{}, stg);
 
 #pragma unroll
   for (int i = 0; i < RT; ++i) {
