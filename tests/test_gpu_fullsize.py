@@ -319,3 +319,32 @@ def test_l70_mixed_step_sampled():
         _check_rows_one_layer(shape, st, w64, dbt_np, drow, x64, y64, "decode rows")
     finally:
         st.close()
+
+
+def test_l70_one_call_prefill_of_8192_tokens_sampled():
+    """The largest single call the benches never make: one L70 layer, one
+    prefill call of 8192 tokens (prompts of 5000 and 3192, the second after a
+    cached prefix of 700): 32 row tiles in every GEMM, 8192-query attention
+    items. Sampled rows against the exact oracle."""
+    seed, shape, layer = 2661, synth.LLAMA70B, 55
+    log("l70 one prefill call of 8192 tokens, one layer")
+    cfg = model_config(shape, "bf16")
+    w = device_layer_weights(shape, seed, layer, "bf16")
+    w64 = _host64(w)
+    pc = np.array([0, 700], np.int32)
+    pq = np.array([5000, 3192], np.int32)
+    nbs = int(((pc + pq + 15) // 16).max())
+    bt_np = synth.make_block_tables(pc + pq, nbs, synth.BlockAllocator(2 * nbs + 8, seed))
+    st = DeviceStage(shape, "bf16", layer, [pack_layer(cfg, w)], 2 * nbs + 8, 8192, 2, packed=True)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    try:
+        st.kv_pool.normal_(0.0, 1.0, generator=g)  # the cached prefix of the second prompt
+        x = torch.randn((8192, shape.hidden), generator=g, device="cuda").to(torch.bfloat16)
+        y = st.prefill(pq, pc, torch.from_numpy(bt_np).cuda(), x)
+        torch.cuda.synchronize()
+        rng = np.random.default_rng(seed)
+        _check_rows_one_layer(shape, st, w64, bt_np, _sample_rows(rng, pq, pc, 8),
+                              x.double().cpu().numpy(), y.double().cpu().numpy(), "rows")
+    finally:
+        st.close()
