@@ -162,10 +162,10 @@ __device__ __forceinline__ const int32_t* seq_table(const SegTables& t, int seq)
 
 // One wave per (token, head); heads [0, n_q) are query heads, [n_q, n_q+n_kv)
 // key/value heads. Lane j < d/2 owns the rotate-half pair (j, j + d/2). The
-// projection is the sum of `splits` partial planes.
+// projection of a column is the sum of its source's partial planes.
 template <typename T>
-__global__ __launch_bounds__(256) void rope_kv_kernel(const float* __restrict__ qkv, int splits,
-                                                      int n_tok, T* __restrict__ q_out,
+__global__ __launch_bounds__(256) void rope_kv_kernel(ProjSrc qs, ProjSrc kvs, int n_tok,
+                                                      T* __restrict__ q_out,
                                                       T* __restrict__ kv, int n_kv, int d,
                                                       const int32_t* tok_seq,
                                                       const int32_t* tok_pos, SegTables tabs,
@@ -181,20 +181,19 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(const float* __restrict__ 
   const int half = d >> 1;
   const bool act = lane < half;
   const int pos = tok_pos[t];
-  const int width = (n_q + 2 * n_kv) * d;
-  const size_t plane = (size_t)n_tok * width;
-  const float* row = qkv + (size_t)t * width;
   const bool is_q = hh < n_q;
   const int kh = hh - n_q;
-  const int col = is_q ? hh * d : (n_q + kh) * d;
+  const ProjSrc src = is_q ? qs : kvs;
+  const float* row = src.base + (size_t)t * src.ld;
+  const int col = is_q ? hh * d : kh * d;
   const T* gain = is_q ? q_gain : k_gain;
 
   float a = 0.f, b = 0.f;
   if (act) {
-#pragma unroll 8
-    for (int sp = 0; sp < splits; ++sp) {
-      a += row[sp * plane + col + lane];
-      b += row[sp * plane + col + lane + half];
+#pragma unroll 4
+    for (int sp = 0; sp < src.splits; ++sp) {
+      a += row[sp * src.plane + col + lane];
+      b += row[sp * src.plane + col + lane + half];
     }
   }
   if (gain != nullptr) {
@@ -223,12 +222,12 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(const float* __restrict__ 
   T* vplane = kplane + (int64_t)kBlock * d;
   elem<T>::store(kplane, kv_k_offset(off, lane), ra);
   elem<T>::store(kplane, kv_k_offset(off, lane + half), rb);
-  const int vcol = (n_q + n_kv + kh) * d;
+  const int vcol = (n_kv + kh) * d;
   float va = 0.f, vb = 0.f;
-#pragma unroll 8
-  for (int sp = 0; sp < splits; ++sp) {
-    va += row[sp * plane + vcol + lane];
-    vb += row[sp * plane + vcol + lane + half];
+#pragma unroll 4
+  for (int sp = 0; sp < src.splits; ++sp) {
+    va += row[sp * src.plane + vcol + lane];
+    vb += row[sp * src.plane + vcol + lane + half];
   }
   elem<T>::store(vplane, kv_v_offset(off, lane), va);
   elem<T>::store(vplane, kv_v_offset(off, lane + half), vb);
@@ -328,19 +327,20 @@ hipError_t output_cast(DType dt, const float* x, Partials add, void* out, int T,
   return hipGetLastError();
 }
 
-hipError_t rope_kv_write(DType dt, const float* qkv, int splits, void* q_out, KVLayer kv,
+hipError_t rope_kv_write(DType dt, ProjSrc qs, ProjSrc kvs, void* q_out, KVLayer kv,
                          const int32_t* tok_seq, const int32_t* tok_pos, SegTables tabs,
                          const float* cos_tab, const float* sin_tab, const void* q_gain,
                          const void* k_gain, float qk_eps, int T, int n_q, hipStream_t s) {
   if (T == 0) return hipSuccess;
+  if (qs.splits < 1 || kvs.splits < 1) return hipErrorInvalidValue;
   dim3 grid(T, (n_q + kv.n_kv + 3) / 4);
   if (dt == DT_BF16)
-    rope_kv_kernel<bf16_t><<<grid, 256, 0, s>>>(qkv, splits, T, (bf16_t*)q_out, (bf16_t*)kv.base,
+    rope_kv_kernel<bf16_t><<<grid, 256, 0, s>>>(qs, kvs, T, (bf16_t*)q_out, (bf16_t*)kv.base,
                                                 kv.n_kv, kv.head_dim, tok_seq, tok_pos, tabs,
                                                 cos_tab, sin_tab, (const bf16_t*)q_gain,
                                                 (const bf16_t*)k_gain, qk_eps, n_q);
   else
-    rope_kv_kernel<float><<<grid, 256, 0, s>>>(qkv, splits, T, (float*)q_out, (float*)kv.base,
+    rope_kv_kernel<float><<<grid, 256, 0, s>>>(qs, kvs, T, (float*)q_out, (float*)kv.base,
                                                kv.n_kv, kv.head_dim, tok_seq, tok_pos, tabs,
                                                cos_tab, sin_tab, (const float*)q_gain,
                                                (const float*)k_gain, qk_eps, n_q);

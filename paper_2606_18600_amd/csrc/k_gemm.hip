@@ -206,10 +206,13 @@ __global__ __launch_bounds__(SK_WAVES * 64) void gemm_skinny_bf16(const bf16_t* 
 // lands at base + 16 l, which is the fragment's own lane order); two stages
 // alternate in LDS.
 template <int BMT, int BNG, int WM, int WN, int EPI>
+// blockIdx.z selects a K range of k_len (K for an unsplit product) and, for
+// the fp32 store, an output plane out + blockIdx.z * out_plane floats.
 __global__ __launch_bounds__(WM * WN * 64) void gemm_tiled_bf16(const bf16_t* __restrict__ A,
                                                                const bf16_t* __restrict__ W,
                                                                int M, int N, int K,
-                                                               void* __restrict__ out, int ldo) {
+                                                               void* __restrict__ out, int ldo,
+                                                               int k_len, size_t out_plane) {
   constexpr int NW = WM * WN;
   constexpr int AF = BMT * 2;
   constexpr int BF = BNG * 8;
@@ -270,7 +273,12 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tiled_bf16(const bf16_t* __
 #pragma unroll
     for (int j = 0; j < TG * 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  const int KTILES = K / 64;
+  const int KTILES = k_len / 64;
+  if (blockIdx.z != 0) {
+#pragma unroll
+    for (int p = 0; p < PER_WAVE; ++p) src[p] += (size_t)blockIdx.z * KTILES * stride[p];
+    if (EPI == EPI_STORE_F32) out = (float*)out + blockIdx.z * out_plane;
+  }
   issue(0, 0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
@@ -444,6 +452,16 @@ hipError_t gemm_skinny(const void* A, const void* W, int M, int N, int K, int sp
   }
 }
 
+hipError_t gemm_split_k(const void* A, const void* W, int M, int N, int K, int splits, float* out,
+                        hipStream_t s) {
+  if (M == 0) return hipSuccess;
+  if (splits < 1 || N % 256 != 0 || K % (64 * splits) != 0) return hipErrorInvalidValue;
+  dim3 grid((M + 255) / 256, N / 256, splits);
+  gemm_tiled_bf16<16, 4, 2, 4, EPI_STORE_F32><<<grid, 512, 0, s>>>(
+      (const bf16_t*)A, (const bf16_t*)W, M, N, K, out, N, K / splits, (size_t)M * N);
+  return hipGetLastError();
+}
+
 hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int N, int K,
                 void* out, hipStream_t s) {
   if (M == 0) return hipSuccess;
@@ -477,17 +495,17 @@ hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int
     if (big) {
       dim3 grid(mb256, Nl / 256);
       switch (epi) {
-        case EPI_STORE_F32: gemm_tiled_bf16<16, 4, 2, 4, EPI_STORE_F32><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N); break;
-        case EPI_RESID_ADD: gemm_tiled_bf16<16, 4, 2, 4, EPI_RESID_ADD><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N); break;
-        case EPI_SWIGLU: gemm_tiled_bf16<16, 4, 2, 4, EPI_SWIGLU><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N); break;
+        case EPI_STORE_F32: gemm_tiled_bf16<16, 4, 2, 4, EPI_STORE_F32><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0); break;
+        case EPI_RESID_ADD: gemm_tiled_bf16<16, 4, 2, 4, EPI_RESID_ADD><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0); break;
+        case EPI_SWIGLU: gemm_tiled_bf16<16, 4, 2, 4, EPI_SWIGLU><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0); break;
         default: return hipErrorInvalidValue;
       }
     } else {
       dim3 grid(mb128, Nl / 128);
       switch (epi) {
-        case EPI_STORE_F32: gemm_tiled_bf16<8, 2, 2, 2, EPI_STORE_F32><<<grid, 256, 0, s>>>(a, wl, M, Nl, K, ol, N); break;
-        case EPI_RESID_ADD: gemm_tiled_bf16<8, 2, 2, 2, EPI_RESID_ADD><<<grid, 256, 0, s>>>(a, wl, M, Nl, K, ol, N); break;
-        case EPI_SWIGLU: gemm_tiled_bf16<8, 2, 2, 2, EPI_SWIGLU><<<grid, 256, 0, s>>>(a, wl, M, Nl, K, ol, N); break;
+        case EPI_STORE_F32: gemm_tiled_bf16<8, 2, 2, 2, EPI_STORE_F32><<<grid, 256, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0); break;
+        case EPI_RESID_ADD: gemm_tiled_bf16<8, 2, 2, 2, EPI_RESID_ADD><<<grid, 256, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0); break;
+        case EPI_SWIGLU: gemm_tiled_bf16<8, 2, 2, 2, EPI_SWIGLU><<<grid, 256, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0); break;
         default: return hipErrorInvalidValue;
       }
     }

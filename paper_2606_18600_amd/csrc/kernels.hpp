@@ -75,8 +75,19 @@ hipError_t rmsnorm(DType dt, float* x, Partials add, void* h, const void* gain, 
 hipError_t output_cast(DType dt, const float* x, Partials add, void* out, int T, int H,
                        hipStream_t s);
 
-// qkv: fp32 [splits][T][(n_q + 2 n_kv) d] (summed over splits).
-hipError_t rope_kv_write(DType dt, const float* qkv, int splits, void* q_out, KVLayer kv,
+// Where the fp32 projection feeding RoPE lives: `splits` partial planes of
+// `plane` floats each, row t at base + t * ld; the value is the sum over the
+// planes. The query columns and the key/value columns are described
+// separately (they may come from different products).
+struct ProjSrc {
+  const float* base;
+  int ld;
+  int splits;
+  size_t plane;
+};
+
+// q columns [0, n_q d) from qs, key then value columns [0, 2 n_kv d) from kvs.
+hipError_t rope_kv_write(DType dt, ProjSrc qs, ProjSrc kvs, void* q_out, KVLayer kv,
                          const int32_t* tok_seq, const int32_t* tok_pos, SegTables tabs,
                          const float* cos_tab, const float* sin_tab, const void* q_gain,
                          const void* k_gain, float qk_eps, int T, int n_q, hipStream_t s);
@@ -108,6 +119,11 @@ int skinny_splits(int N, int K, int target_blocks, int max_splits = kSkinnyMaxSp
 int skinny_kb_len(int K, int splits);
 hipError_t gemm_skinny(const void* A, const void* W, int M, int N, int K, int splits, bool swiglu,
                        void* out, hipStream_t s);
+// bf16 LDS-tiled product split over K: `splits` fp32 partial planes
+// [splits][M][N] (row stride N) of A [M, K] x W[N, K]^T, 256 x 256 tiles.
+// Needs N % 256 == 0 and K % (64 * splits) == 0.
+hipError_t gemm_split_k(const void* A, const void* W, int M, int N, int K, int splits, float* out,
+                        hipStream_t s);
 // gemm: bf16 = LDS-tiled MFMA over packed A and W; fp32 = SIMT, row-major.
 hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int N, int K,
                 void* out, hipStream_t s);

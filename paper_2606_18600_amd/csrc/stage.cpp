@@ -35,6 +35,7 @@ constexpr int kRing = 4;             // pinned staging buffers in flight
 constexpr int kMaxSplits = 32;       // decode key splits per sequence, at most
 constexpr int kSplitMinBlocks = 4;   // at least 4 blocks (64 keys) per split
 constexpr int kSkinnyMaxRows = 128;  // decode-sized steps use split-K GEMMs
+constexpr int kMaxKvSplits = 4;      // K splits of the key/value columns of a prefill QKV
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -70,12 +71,13 @@ struct stage {
   // decode attention waves to aim for: one resident round (the kernel runs
   // two waves per SIMD, 2048 on the chip) with slack for per-sequence
   // rounding of the split sizes
+  int cus = 256;  // compute units of the device
   int attn_waves = 1600;
   int pf_tiles = 2;  // prefill attention row tiles per wave (2 or 4; 2 measured faster)
 
   // workspace
-  Region r_x, r_h, r_qkv, r_q, r_attn, r_m, r_gu, r_part_x, r_part_o, r_part_ml, r_meta, r_cos,
-      r_sin;
+  Region r_x, r_h, r_qkv, r_kvpart, r_q, r_attn, r_m, r_gu, r_part_x, r_part_o, r_part_ml, r_meta,
+      r_cos, r_sin;
   size_t ws_bytes = 0;
   char* ws = nullptr;
   size_t meta_ints = 0;
@@ -194,6 +196,7 @@ void plan_workspace(stage* st) {
   take(st->r_x, T * H * 4);
   take(st->r_h, Tp * H * es);
   take(st->r_qkv, std::max(T, (size_t)st->s_qkv * R) * qkvw * 4);
+  take(st->r_kvpart, c.dtype == STAGE_BF16 ? kMaxKvSplits * T * (qkvw - qw) * 4 : 0);
   take(st->r_q, T * qw * es);
   take(st->r_attn, Tp * qw * es);
   take(st->r_m, Tp * F * es);
@@ -298,6 +301,24 @@ hipEvent_t take_event(stage* st) {
   return e;
 }
 
+// K splits for the key/value columns of a tiled (prefill) QKV product, or 0
+// to run QKV as one product. With T rows in whole 256-row tiles, when the
+// query columns alone fill whole rounds of one 256 x 256 workgroup per CU,
+// the 2 n_kv d key/value columns would leave most of the chip idle as 256
+// tiles of their own; split over K they fill one round exactly (e.g. Llama
+// 70B at 2048 rows: 8 x 32 query tiles, then 8 x 8 key/value tiles x 4
+// splits).
+int qkv_kv_splits(const stage* st, int T) {
+  const auto& c = st->cfg;
+  const int qw = c.n_q_heads * c.head_dim, kvw = 2 * c.n_kv_heads * c.head_dim;
+  if (c.dtype != STAGE_BF16 || T % 256 != 0 || qw % 256 != 0 || kvw % 256 != 0) return 0;
+  const long mb = T / 256;
+  if ((mb * (qw / 256)) % st->cus != 0) return 0;
+  for (int sp = 2; sp <= kMaxKvSplits; sp *= 2)
+    if (mb * (kvw / 256) * sp == st->cus && c.hidden % (64 * sp) == 0) return sp;
+  return 0;
+}
+
 // Take the next pinned staging slot of the ring, waiting until the upload
 // that last used it has been consumed.
 stage_status take_slot(stage* st, int* slot) {
@@ -396,6 +417,7 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
   // projections as partial sums in part_x; the next RMSNorm (or the output
   // cast) adds them to the residual stream. The first layer's input norm
   // (which reads hidden_in) is launched before it.
+  const int kv_splits = skinny ? 0 : qkv_kv_splits(st, T);
   auto layers = [&](Launcher& L, hipStream_t ls) {
     Partials pending{nullptr, 0};
     for (int li = 0; li < st->n_layers; ++li) {
@@ -404,16 +426,30 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
       if (li > 0)
         L(STAGE_OP_NORM, [&] { return rmsnorm(dt, x, pending, h, w.attn_norm, T, H, c.rms_eps, ls); });
 
-      int qkv_splits = 1;
+      // where RoPE finds the projection: [T][qkvw], possibly in split planes,
+      // or the query columns [T][qw] and split planes of the key/value columns
+      ProjSrc qsrc{qkv, qkvw, 1, 0}, kvsrc{qkv + qw, qkvw, 1, 0};
       if (skinny) {
-        qkv_splits = st->s_qkv;
+        const size_t plane = (size_t)T * qkvw;
+        qsrc = ProjSrc{qkv, qkvw, st->s_qkv, plane};
+        kvsrc = ProjSrc{qkv + qw, qkvw, st->s_qkv, plane};
         L(STAGE_OP_QKV, [&] { return gemm_skinny(h, w.w_qkv, T, qkvw, H, st->s_qkv, false, qkv, ls); });
+      } else if (kv_splits > 0) {
+        float* kvpart = st->at<float>(st->r_kvpart);
+        const int kvw = qkvw - qw;
+        qsrc = ProjSrc{qkv, qw, 1, 0};
+        kvsrc = ProjSrc{kvpart, kvw, kv_splits, (size_t)T * kvw};
+        L(STAGE_OP_QKV, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_qkv, T, qw, H, qkv, ls); });
+        L(STAGE_OP_QKV, [&] {
+          return gemm_split_k(h, (const uint16_t*)w.w_qkv + (size_t)qw * H, T, kvw, H, kv_splits,
+                              kvpart, ls);
+        });
       } else {
         L(STAGE_OP_QKV, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_qkv, T, qkvw, H, qkv, ls); });
       }
       L(STAGE_OP_ROPE_KV, [&] {
-        return rope_kv_write(dt, qkv, qkv_splits, q, kvl, dm.tok_seq, dm.tok_pos, tabs, cos_t,
-                             sin_t, c.qk_norm ? w.q_norm : nullptr, c.qk_norm ? w.k_norm : nullptr,
+        return rope_kv_write(dt, qsrc, kvsrc, q, kvl, dm.tok_seq, dm.tok_pos, tabs, cos_t, sin_t,
+                             c.qk_norm ? w.q_norm : nullptr, c.qk_norm ? w.k_norm : nullptr,
                              c.qk_rms_eps, T, nq, ls);
       });
 
@@ -545,6 +581,7 @@ stage_status stage_create(const stage_model_config* cfg, int32_t layer_begin, in
             hipSuccess ||
         cus <= 0)
       cus = 256;
+    st->cus = cus;
     const int blocks = std::max(1, env_int("STAGE_SKINNY_BLOCKS", cus * 9 / 10));
     const int H = cfg->hidden, F = cfg->ffn, qw = cfg->n_q_heads * cfg->head_dim;
     const int qkvw = (cfg->n_q_heads + 2 * cfg->n_kv_heads) * cfg->head_dim;
