@@ -103,6 +103,65 @@ __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const InT* __restrict
   }
 }
 
+// RMSNorm of many rows into the packed bf16 activation layout, 8 rows per
+// block: thread tau owns row tau % 8 and the 8-column groups tau / 8 + 128 p
+// (p = pass). A store instruction of a wave then covers the 16-byte slots
+// of 8 consecutive rows for 8 column groups, i.e. 8 whole 128-byte lines of
+// the packed layout (one row per block would write 16 bytes per line and
+// leave each line to be completed by 15 other blocks). H % 1024 == 0 and
+// H <= 8192 (at most 8 passes held in registers).
+__global__ __launch_bounds__(1024) void rmsnorm_rows8_kernel(const float* __restrict__ x, int T,
+                                                            int H, bf16_t* __restrict__ h,
+                                                            const bf16_t* __restrict__ gain,
+                                                            float eps) {
+  constexpr int kMaxPass = 8;
+  __shared__ float red[16][8];
+  const int tau = threadIdx.x, r = tau & 7, kg = tau >> 3;
+  const int row = blockIdx.x * 8 + r;
+  const bool ok = row < T;
+  const int passes = H / 1024;
+  float v[kMaxPass][8];
+  float ss = 0.f;
+#pragma unroll
+  for (int p = 0; p < kMaxPass; ++p) {
+    if (p < passes) {
+      const int k = (p * 128 + kg) * 8;
+      float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
+      if (ok) {
+        a = *(const float4*)(x + (size_t)row * H + k);
+        b = *(const float4*)(x + (size_t)row * H + k + 4);
+      }
+      v[p][0] = a.x; v[p][1] = a.y; v[p][2] = a.z; v[p][3] = a.w;
+      v[p][4] = b.x; v[p][5] = b.y; v[p][6] = b.z; v[p][7] = b.w;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss += v[p][e] * v[p][e];
+    }
+  }
+  // lanes with the same row differ in lane bits 3..5, then 16 waves via LDS
+  ss += __shfl_xor(ss, 8, 64);
+  ss += __shfl_xor(ss, 16, 64);
+  ss += __shfl_xor(ss, 32, 64);
+  if ((tau & 63) < 8) red[tau >> 6][r] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < 16; ++w) tot += red[w][r];
+  if (!ok) return;
+  const float sc = 1.0f / sqrtf(tot / (float)H + eps);
+#pragma unroll
+  for (int p = 0; p < kMaxPass; ++p) {
+    if (p < passes) {
+      const int k = (p * 128 + kg) * 8;
+      const u32x4_t gw = *(const u32x4_t*)(gain + k);
+      u32x4_t o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        o[e] = pack_bf16x2(v[p][2 * e] * sc * lo_bf16(gw[e]), v[p][2 * e + 1] * sc * hi_bf16(gw[e]));
+      *(u32x4_t*)(h + packed_a_offset(row, k, H)) = o;
+    }
+  }
+}
+
 template <typename InT, typename OutT, bool kEmbed, int kThreads>
 hipError_t launch_norm_t(const InT* in, const int32_t* rows, float* x, Partials add, OutT* h,
                          const OutT* gain, int T, int H, float eps, hipStream_t s) {
@@ -307,6 +366,11 @@ hipError_t embed_norm(DType dt, const void* hidden_in, float* x, void* h, const 
 hipError_t rmsnorm(DType dt, float* x, Partials add, void* h, const void* gain, int T, int H,
                    float eps, hipStream_t s) {
   if (T == 0) return hipSuccess;
+  if (dt == DT_BF16 && add.splits == 0 && T >= 1024 && H % 1024 == 0 && H <= 8192) {
+    rmsnorm_rows8_kernel<<<(T + 7) / 8, 1024, 0, s>>>(x, T, H, (bf16_t*)h, (const bf16_t*)gain,
+                                                      eps);
+    return hipGetLastError();
+  }
   if (dt == DT_BF16)
     return launch_norm<float, bf16_t, false>(nullptr, nullptr, x, add, (bf16_t*)h,
                                              (const bf16_t*)gain, T, H, eps, s);
