@@ -36,6 +36,7 @@ constexpr int kMaxSplits = 32;       // decode key splits per sequence, at most
 constexpr int kSplitMinBlocks = 4;   // at least 4 blocks (64 keys) per split
 constexpr int kSkinnyMaxRows = 128;  // decode-sized steps use split-K GEMMs
 constexpr int kMaxKvSplits = 4;      // K splits of the key/value columns of a prefill QKV
+constexpr int kMaxMidSplits = 8;     // K splits of the products of a one-row-tile step
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -195,14 +196,16 @@ void plan_workspace(stage* st) {
   };
   take(st->r_x, T * H * 4);
   take(st->r_h, Tp * H * es);
-  take(st->r_qkv, std::max(T, (size_t)st->s_qkv * R) * qkvw * 4);
+  // split-K planes of one-row-tile steps (T <= 256, bf16)
+  const size_t mid_rows = c.dtype == STAGE_BF16 && T > R ? kMaxMidSplits * std::min<size_t>(T, 256) : 0;
+  take(st->r_qkv, std::max({T, (size_t)st->s_qkv * R, mid_rows}) * qkvw * 4);
   take(st->r_kvpart, c.dtype == STAGE_BF16 ? kMaxKvSplits * T * (qkvw - qw) * 4 : 0);
   take(st->r_q, T * qw * es);
   take(st->r_attn, Tp * qw * es);
   take(st->r_m, Tp * F * es);
   const size_t gu_rows = c.dtype == STAGE_F32 ? T : (st->s_gu > 1 ? (size_t)st->s_gu * R : 0);
   take(st->r_gu, gu_rows * 2 * F * 4);
-  take(st->r_part_x, (size_t)std::max(st->s_o, st->s_down) * R * H * 4);
+  take(st->r_part_x, std::max((size_t)std::max(st->s_o, st->s_down) * R, mid_rows) * H * 4);
   const size_t max_items = c.dtype == STAGE_BF16 ? (size_t)st->max_seqs * kMaxSplits : 0;
   take(st->r_part_o, max_items * qw * 4);
   take(st->r_part_ml, max_items * c.n_q_heads * 2 * 4);
@@ -319,6 +322,20 @@ int qkv_kv_splits(const stage* st, int T) {
   return 0;
 }
 
+// K splits for an [T, N] x [N, K]^T product of a bf16 step that fits one
+// 256-row tile (more rows than the split-K decode GEMMs take, T <= 256), or
+// 0. Its 256 x 256 tiles alone would occupy only N / 256 CUs for the whole
+// K; split over K into fp32 partial planes that the consumer sums (as in
+// decode steps), the launch fills up to one round.
+int mid_splits(const stage* st, int T, int N, int K) {
+  if (st->cfg.dtype != STAGE_BF16 || T > 256 || T <= st->skinny_rows || N % 256 != 0) return 0;
+  const int tiles = N / 256;
+  int best = 0;
+  for (int sp = 2; sp <= kMaxMidSplits; sp *= 2)
+    if (tiles * sp <= st->cus && K % (64 * sp) == 0) best = sp;
+  return best;
+}
+
 // Take the next pinned staging slot of the ring, waiting until the upload
 // that last used it has been consumed.
 stage_status take_slot(stage* st, int* slot) {
@@ -418,6 +435,8 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
   // cast) adds them to the residual stream. The first layer's input norm
   // (which reads hidden_in) is launched before it.
   const int kv_splits = skinny ? 0 : qkv_kv_splits(st, T);
+  const int mq = mid_splits(st, T, qkvw, H), mo = mid_splits(st, T, H, qw),
+            md = mid_splits(st, T, H, F);
   auto layers = [&](Launcher& L, hipStream_t ls) {
     Partials pending{nullptr, 0};
     for (int li = 0; li < st->n_layers; ++li) {
@@ -434,6 +453,11 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
         qsrc = ProjSrc{qkv, qkvw, st->s_qkv, plane};
         kvsrc = ProjSrc{qkv + qw, qkvw, st->s_qkv, plane};
         L(STAGE_OP_QKV, [&] { return gemm_skinny(h, w.w_qkv, T, qkvw, H, st->s_qkv, false, qkv, ls); });
+      } else if (mq > 0) {
+        const size_t plane = (size_t)T * qkvw;
+        qsrc = ProjSrc{qkv, qkvw, mq, plane};
+        kvsrc = ProjSrc{qkv + qw, qkvw, mq, plane};
+        L(STAGE_OP_QKV, [&] { return gemm_split_k(h, w.w_qkv, T, qkvw, H, mq, qkv, ls); });
       } else if (kv_splits > 0) {
         float* kvpart = st->at<float>(st->r_kvpart);
         const int kvw = qkvw - qw;
@@ -479,6 +503,9 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
       if (skinny) {
         L(STAGE_OP_O, [&] { return gemm_skinny(attn, w.w_o, T, H, qw, st->s_o, false, part_x, ls); });
         pending = Partials{part_x, st->s_o};
+      } else if (mo > 0) {
+        L(STAGE_OP_O, [&] { return gemm_split_k(attn, w.w_o, T, H, qw, mo, part_x, ls); });
+        pending = Partials{part_x, mo};
       } else {
         L(STAGE_OP_O, [&] { return gemm(dt, EPI_RESID_ADD, attn, w.w_o, T, H, qw, x, ls); });
       }
@@ -501,7 +528,12 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
         pending = Partials{part_x, st->s_down};
       } else if (dt == DT_BF16) {
         L(STAGE_OP_GATE_UP, [&] { return gemm(dt, EPI_SWIGLU, h, w.w_gate_up, T, 2 * F, H, m, ls); });
-        L(STAGE_OP_DOWN, [&] { return gemm(dt, EPI_RESID_ADD, m, w.w_down, T, H, F, x, ls); });
+        if (md > 0) {
+          L(STAGE_OP_DOWN, [&] { return gemm_split_k(m, w.w_down, T, H, F, md, part_x, ls); });
+          pending = Partials{part_x, md};
+        } else {
+          L(STAGE_OP_DOWN, [&] { return gemm(dt, EPI_RESID_ADD, m, w.w_down, T, H, F, x, ls); });
+        }
       } else {
         L(STAGE_OP_GATE_UP, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_gate_up, T, 2 * F, H, gu, ls); });
         L(STAGE_OP_NORM, [&] { return swiglu_f32(gu, (float*)m, T, F, ls); });
@@ -510,7 +542,9 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
     }
   };
   // what the last layer leaves for the output cast
-  const Partials tail = skinny ? Partials{part_x, st->s_down} : Partials{nullptr, 0};
+  const Partials tail = skinny   ? Partials{part_x, st->s_down}
+                        : md > 0 ? Partials{part_x, md}
+                                 : Partials{nullptr, 0};
 
   Launcher L{st, s};
   L(STAGE_OP_NORM, [&] {
