@@ -36,7 +36,8 @@ constexpr int kMaxSplits = 32;       // decode key splits per sequence, at most
 constexpr int kSplitMinBlocks = 4;   // at least 4 blocks (64 keys) per split
 constexpr int kSkinnyMaxRows = 128;  // decode-sized steps use split-K GEMMs
 constexpr int kMaxKvSplits = 4;      // K splits of the key/value columns of a prefill QKV
-constexpr int kMaxMidSplits = 8;     // K splits of the products of a one-row-tile step
+constexpr int kMaxMidSplits = 8;     // K splits of the products of a small tiled step
+constexpr int kMidRows = 2048;       // partial-plane rows of such a step (splits x T)
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -196,8 +197,8 @@ void plan_workspace(stage* st) {
   };
   take(st->r_x, T * H * 4);
   take(st->r_h, Tp * H * es);
-  // split-K planes of one-row-tile steps (T <= 256, bf16)
-  const size_t mid_rows = c.dtype == STAGE_BF16 && T > R ? kMaxMidSplits * std::min<size_t>(T, 256) : 0;
+  // split-K planes of small tiled steps (bf16)
+  const size_t mid_rows = c.dtype == STAGE_BF16 && T > R ? (size_t)kMidRows : 0;
   take(st->r_qkv, std::max({T, (size_t)st->s_qkv * R, mid_rows}) * qkvw * 4);
   take(st->r_kvpart, c.dtype == STAGE_BF16 ? kMaxKvSplits * T * (qkvw - qw) * 4 : 0);
   take(st->r_q, T * qw * es);
@@ -322,17 +323,20 @@ int qkv_kv_splits(const stage* st, int T) {
   return 0;
 }
 
-// K splits for an [T, N] x [N, K]^T product of a bf16 step that fits one
-// 256-row tile (more rows than the split-K decode GEMMs take, T <= 256), or
-// 0. Its 256 x 256 tiles alone would occupy only N / 256 CUs for the whole
-// K; split over K into fp32 partial planes that the consumer sums (as in
-// decode steps), the launch fills up to one round.
+// K splits for an [T, N] x [N, K]^T product of a bf16 tiled step (more rows
+// than the split-K decode GEMMs take), or 0. When its 256 x 256 tiles would
+// occupy less than half of the CUs for the whole K (e.g. O and down with 32
+// tiles per 256 rows), it runs over K ranges into fp32 partial planes that
+// the consumer sums (as in decode steps): as many ranges (a power of two, at
+// most 8) as keep the launch within one round and the planes within
+// kMidRows rows.
 int mid_splits(const stage* st, int T, int N, int K) {
-  if (st->cfg.dtype != STAGE_BF16 || T > 256 || T <= st->skinny_rows || N % 256 != 0) return 0;
-  const int tiles = N / 256;
+  if (st->cfg.dtype != STAGE_BF16 || T <= st->skinny_rows || N % 256 != 0) return 0;
+  const int tiles = (T + 255) / 256 * (N / 256);
+  if (2 * tiles >= st->cus) return 0;
   int best = 0;
   for (int sp = 2; sp <= kMaxMidSplits; sp *= 2)
-    if (tiles * sp <= st->cus && K % (64 * sp) == 0) best = sp;
+    if (tiles * sp <= st->cus && K % (64 * sp) == 0 && sp * T <= kMidRows) best = sp;
   return best;
 }
 
