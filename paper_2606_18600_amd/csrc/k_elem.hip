@@ -47,21 +47,23 @@ __device__ __forceinline__ void store_act4(float* h, int t, int k, int K, float4
 }
 
 // kS: number of split-K partial planes added to x (compile time, so that all
-// of a thread's loads are issued together). With kEmbed, row t reads input
-// row rows[t] (rows == nullptr: row t).
+// of a thread's loads are issued together); rows before r0 have none. With
+// kEmbed, row t reads input row rows[t] (rows == nullptr: row t).
 template <typename InT, typename OutT, bool kEmbed, int kThreads, int kS>
 __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const InT* __restrict__ in,
                                                            const int32_t* __restrict__ rows,
                                                            float* __restrict__ x,
                                                            const float* __restrict__ part, int T,
-                                                           OutT* __restrict__ h,
+                                                           int r0, OutT* __restrict__ h,
                                                            const OutT* __restrict__ gain, int H,
                                                            float eps) {
   constexpr int kVec = 16384 / 4 / kThreads;
   const int t = blockIdx.x;
   const size_t row = (size_t)t * H;
   const size_t in_row = kEmbed && rows != nullptr ? (size_t)rows[t] * H : row;
-  const size_t plane = (size_t)T * H;
+  const size_t plane = (size_t)(T - r0) * H;
+  const size_t prow = (size_t)(t - r0) * H;  // this row in the partial planes (t >= r0)
+  const bool adds = kS > 0 && t >= r0;
   const int H4 = H >> 2;
   __shared__ float red[kThreads / STAGE_WAVE];
   float4 v[kVec];
@@ -75,12 +77,15 @@ __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const InT* __restrict
         v[j] = vec4_io<InT>::load(in, in_row + 4 * (size_t)i4);
       else
         v[j] = *(const float4*)(x + e);
-      float4 p[kS > 0 ? kS : 1];
+      if (adds) {
+        float4 p[kS > 0 ? kS : 1];
 #pragma unroll
-      for (int sp = 0; sp < kS; ++sp) p[sp] = *(const float4*)(part + sp * plane + e);
+        for (int sp = 0; sp < kS; ++sp)
+          p[sp] = *(const float4*)(part + sp * plane + prow + 4 * (size_t)i4);
 #pragma unroll
-      for (int sp = 0; sp < kS; ++sp) add4(v[j], p[sp]);
-      if (kEmbed || kS > 0) *(float4*)(x + e) = v[j];
+        for (int sp = 0; sp < kS; ++sp) add4(v[j], p[sp]);
+      }
+      if (kEmbed || adds) *(float4*)(x + e) = v[j];
       ss += v[j].x * v[j].x + v[j].y * v[j].y + v[j].z * v[j].z + v[j].w * v[j].w;
     }
   }
@@ -109,16 +114,26 @@ __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const InT* __restrict
 // of 8 consecutive rows for 8 column groups, i.e. 8 whole 128-byte lines of
 // the packed layout (one row per block would write 16 bytes per line and
 // leave each line to be completed by 15 other blocks). H % 1024 == 0 and
-// H <= 8192 (at most 8 passes held in registers).
-__global__ __launch_bounds__(1024) void rmsnorm_rows8_kernel(const float* __restrict__ x, int T,
-                                                            int H, bf16_t* __restrict__ h,
+// H <= 8192 (at most 8 passes held in registers). Rows from r0 on (r0 % 8
+// == 0, so a block's rows all have partials or none) first add `splits`
+// (<= kNormMaxSplits) partial planes of (T - r0) rows and store x back.
+// Those blocks read several times the bytes of the others, so blocks are
+// taken in reverse row order: the last rows are dispatched first.
+constexpr int kNormMaxSplits = 8;
+__global__ __launch_bounds__(1024) void rmsnorm_rows8_kernel(float* __restrict__ x, int T, int H,
+                                                            const float* __restrict__ part,
+                                                            int splits, int r0,
+                                                            bf16_t* __restrict__ h,
                                                             const bf16_t* __restrict__ gain,
                                                             float eps) {
   constexpr int kMaxPass = 8;
   __shared__ float red[16][8];
   const int tau = threadIdx.x, r = tau & 7, kg = tau >> 3;
-  const int row = blockIdx.x * 8 + r;
+  const int grp = gridDim.x - 1 - blockIdx.x;
+  const int row = grp * 8 + r;
   const bool ok = row < T;
+  const bool adds = splits > 0 && grp * 8 >= r0;
+  const size_t plane = (size_t)(T - r0) * H;
   const int passes = H / 1024;
   float v[kMaxPass][8];
   float ss = 0.f;
@@ -130,6 +145,25 @@ __global__ __launch_bounds__(1024) void rmsnorm_rows8_kernel(const float* __rest
       if (ok) {
         a = *(const float4*)(x + (size_t)row * H + k);
         b = *(const float4*)(x + (size_t)row * H + k + 4);
+        if (adds) {
+          // all of the pass's partial loads in flight together, summed in plane order
+          const float* pp = part + (size_t)(row - r0) * H + k;
+          float4 pa[kNormMaxSplits], pb[kNormMaxSplits];
+#pragma unroll
+          for (int sp = 0; sp < kNormMaxSplits; ++sp)
+            if (sp < splits) {
+              pa[sp] = *(const float4*)(pp + sp * plane);
+              pb[sp] = *(const float4*)(pp + sp * plane + 4);
+            }
+#pragma unroll
+          for (int sp = 0; sp < kNormMaxSplits; ++sp)
+            if (sp < splits) {
+              add4(a, pa[sp]);
+              add4(b, pb[sp]);
+            }
+          *(float4*)(x + (size_t)row * H + k) = a;
+          *(float4*)(x + (size_t)row * H + k + 4) = b;
+        }
       }
       v[p][0] = a.x; v[p][1] = a.y; v[p][2] = a.z; v[p][3] = a.w;
       v[p][4] = b.x; v[p][5] = b.y; v[p][6] = b.z; v[p][7] = b.w;
@@ -169,7 +203,8 @@ hipError_t launch_norm_t(const InT* in, const int32_t* rows, float* x, Partials 
 #define STAGE_NORM_CASE(S)                                                                  \
   case S:                                                                                   \
     rmsnorm_kernel<InT, OutT, kEmbed, kThreads, S><<<T, kThreads, 0, s>>>(in, rows, x, add.p, \
-                                                                         T, h, gain, H, eps); \
+                                                                         T, add.r0, h, gain, \
+                                                                         H, eps);            \
     break;
     STAGE_NORM_CASE(0)
     STAGE_NORM_CASE(1)
@@ -196,17 +231,20 @@ hipError_t launch_norm(const InT* in, const int32_t* rows, float* x, Partials ad
   return launch_norm_t<InT, OutT, kEmbed, 256>(in, rows, x, add, h, gain, T, H, eps, s);
 }
 
+// Partials cover rows r0 .. T-1 (planes of (T - r0) * H floats).
 template <typename OutT>
 __global__ __launch_bounds__(256) void output_cast_kernel(const float* __restrict__ x,
                                                           const float* __restrict__ part,
-                                                          int splits, int T, int H,
+                                                          int splits, int r0, int T, int H,
                                                           OutT* __restrict__ out) {
-  const size_t plane = (size_t)T * H;
-  const size_t n4 = plane / 4;
+  const size_t n4 = (size_t)T * H / 4;
+  const size_t plane = (size_t)(T - r0) * H, skip = (size_t)r0 * H;
   for (size_t i4 = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i4 < n4;
        i4 += (size_t)gridDim.x * blockDim.x) {
     float4 v = *(const float4*)(x + 4 * i4);
-    for (int sp = 0; sp < splits; ++sp) add4(v, *(const float4*)(part + sp * plane + 4 * i4));
+    if (4 * i4 >= skip)
+      for (int sp = 0; sp < splits; ++sp)
+        add4(v, *(const float4*)(part + sp * plane + 4 * i4 - skip));
     elem<OutT>::store(out, 4 * i4 + 0, v.x);
     elem<OutT>::store(out, 4 * i4 + 1, v.y);
     elem<OutT>::store(out, 4 * i4 + 2, v.z);
@@ -221,9 +259,12 @@ __device__ __forceinline__ const int32_t* seq_table(const SegTables& t, int seq)
 
 // One wave per (token, head); heads [0, n_q) are query heads, [n_q, n_q+n_kv)
 // key/value heads. Lane j < d/2 owns the rotate-half pair (j, j + d/2). The
-// projection of a column is the sum of its source's partial planes.
+// projection of a column is the sum of its source's partial planes. Grid
+// (head groups, tokens) with tokens taken last to first, so that the last
+// rows, whose source may have more planes, are dispatched first.
 template <typename T>
-__global__ __launch_bounds__(256) void rope_kv_kernel(ProjSrc qs, ProjSrc kvs, int n_tok,
+__global__ __launch_bounds__(256) void rope_kv_kernel(ProjSrc qs, ProjSrc kvs, ProjSrc qt,
+                                                      ProjSrc kvt, int r0, int n_tok,
                                                       T* __restrict__ q_out,
                                                       T* __restrict__ kv, int n_kv, int d,
                                                       const int32_t* tok_seq,
@@ -233,8 +274,8 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(ProjSrc qs, ProjSrc kvs, i
                                                       const T* __restrict__ q_gain,
                                                       const T* __restrict__ k_gain, float qk_eps,
                                                       int n_q) {
-  const int t = blockIdx.x;
-  const int hh = blockIdx.y * 4 + (threadIdx.x >> 6);
+  const int t = n_tok - 1 - blockIdx.y;
+  const int hh = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (hh >= n_q + n_kv) return;
   const int lane = threadIdx.x & 63;
   const int half = d >> 1;
@@ -242,8 +283,9 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(ProjSrc qs, ProjSrc kvs, i
   const int pos = tok_pos[t];
   const bool is_q = hh < n_q;
   const int kh = hh - n_q;
-  const ProjSrc src = is_q ? qs : kvs;
-  const float* row = src.base + (size_t)t * src.ld;
+  const bool tail = t >= r0;
+  const ProjSrc src = tail ? (is_q ? qt : kvt) : (is_q ? qs : kvs);
+  const float* row = src.base + (size_t)(tail ? t - r0 : t) * src.ld;
   const int col = is_q ? hh * d : kh * d;
   const T* gain = is_q ? q_gain : k_gain;
 
@@ -366,9 +408,10 @@ hipError_t embed_norm(DType dt, const void* hidden_in, float* x, void* h, const 
 hipError_t rmsnorm(DType dt, float* x, Partials add, void* h, const void* gain, int T, int H,
                    float eps, hipStream_t s) {
   if (T == 0) return hipSuccess;
-  if (dt == DT_BF16 && add.splits == 0 && T >= 1024 && H % 1024 == 0 && H <= 8192) {
-    rmsnorm_rows8_kernel<<<(T + 7) / 8, 1024, 0, s>>>(x, T, H, (bf16_t*)h, (const bf16_t*)gain,
-                                                      eps);
+  if (dt == DT_BF16 && add.r0 % 8 == 0 && add.splits <= kNormMaxSplits && T >= 1024 &&
+      H % 1024 == 0 && H <= 8192) {
+    rmsnorm_rows8_kernel<<<(T + 7) / 8, 1024, 0, s>>>(x, T, H, add.p, add.splits, add.r0,
+                                                      (bf16_t*)h, (const bf16_t*)gain, eps);
     return hipGetLastError();
   }
   if (dt == DT_BF16)
@@ -383,28 +426,32 @@ hipError_t output_cast(DType dt, const float* x, Partials add, void* out, int T,
   const size_t n4 = (size_t)T * H / 4;
   if (n4 == 0) return hipSuccess;
   if (dt == DT_BF16)
-    output_cast_kernel<bf16_t><<<grid_for(n4, 256), 256, 0, s>>>(x, add.p, add.splits, T, H,
-                                                                 (bf16_t*)out);
+    output_cast_kernel<bf16_t><<<grid_for(n4, 256), 256, 0, s>>>(x, add.p, add.splits, add.r0,
+                                                                 T, H, (bf16_t*)out);
   else
-    output_cast_kernel<float><<<grid_for(n4, 256), 256, 0, s>>>(x, add.p, add.splits, T, H,
-                                                                (float*)out);
+    output_cast_kernel<float><<<grid_for(n4, 256), 256, 0, s>>>(x, add.p, add.splits, add.r0,
+                                                                T, H, (float*)out);
   return hipGetLastError();
 }
 
-hipError_t rope_kv_write(DType dt, ProjSrc qs, ProjSrc kvs, void* q_out, KVLayer kv,
-                         const int32_t* tok_seq, const int32_t* tok_pos, SegTables tabs,
-                         const float* cos_tab, const float* sin_tab, const void* q_gain,
-                         const void* k_gain, float qk_eps, int T, int n_q, hipStream_t s) {
+hipError_t rope_kv_write(DType dt, ProjSrc qs, ProjSrc kvs, ProjSrc qt, ProjSrc kvt, int r0,
+                         void* q_out, KVLayer kv, const int32_t* tok_seq, const int32_t* tok_pos,
+                         SegTables tabs, const float* cos_tab, const float* sin_tab,
+                         const void* q_gain, const void* k_gain, float qk_eps, int T, int n_q,
+                         hipStream_t s) {
   if (T == 0) return hipSuccess;
-  if (qs.splits < 1 || kvs.splits < 1) return hipErrorInvalidValue;
-  dim3 grid(T, (n_q + kv.n_kv + 3) / 4);
+  if (r0 < 0 || r0 > T) return hipErrorInvalidValue;
+  if ((r0 > 0 && (qs.splits < 1 || kvs.splits < 1)) || (r0 < T && (qt.splits < 1 || kvt.splits < 1)))
+    return hipErrorInvalidValue;
+  if (T > 65535) return hipErrorInvalidValue;
+  dim3 grid((n_q + kv.n_kv + 3) / 4, T);
   if (dt == DT_BF16)
-    rope_kv_kernel<bf16_t><<<grid, 256, 0, s>>>(qs, kvs, T, (bf16_t*)q_out, (bf16_t*)kv.base,
+    rope_kv_kernel<bf16_t><<<grid, 256, 0, s>>>(qs, kvs, qt, kvt, r0, T, (bf16_t*)q_out, (bf16_t*)kv.base,
                                                 kv.n_kv, kv.head_dim, tok_seq, tok_pos, tabs,
                                                 cos_tab, sin_tab, (const bf16_t*)q_gain,
                                                 (const bf16_t*)k_gain, qk_eps, n_q);
   else
-    rope_kv_kernel<float><<<grid, 256, 0, s>>>(qs, kvs, T, (float*)q_out, (float*)kv.base,
+    rope_kv_kernel<float><<<grid, 256, 0, s>>>(qs, kvs, qt, kvt, r0, T, (float*)q_out, (float*)kv.base,
                                                kv.n_kv, kv.head_dim, tok_seq, tok_pos, tabs,
                                                cos_tab, sin_tab, (const float*)q_gain,
                                                (const float*)k_gain, qk_eps, n_q);
@@ -421,6 +468,7 @@ hipError_t swiglu_f32(const float* gu, float* m, int T, int F, hipStream_t s) {
 hipError_t swiglu_reduce_bf16(Partials gu, uint16_t* m, int T, int F, hipStream_t s) {
   const size_t n4 = (size_t)T * F / 4;
   if (n4 == 0) return hipSuccess;
+  if (gu.r0 != 0) return hipErrorInvalidValue;
   swiglu_reduce_kernel<<<grid_for(n4, 256), 256, 0, s>>>(gu.p, gu.splits, T, F, m);
   return hipGetLastError();
 }

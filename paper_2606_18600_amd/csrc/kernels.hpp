@@ -56,11 +56,14 @@ struct PrefillItem {
   int32_t npos;
 };
 
-// Split-K partial sums of an fp32 [M, N] result: `splits` planes of M * N
-// floats (splits == 0: none).
+// Split-K partial sums of an fp32 [M, N] result (splits == 0: none). Only
+// rows r0 .. M-1 have partials: `splits` planes of (M - r0) * N floats, row
+// t at (t - r0) * N of each plane. r0 > 0 when the first r0 rows of a step
+// were finished by a tiled product and only the remaining rows ran split-K.
 struct Partials {
   const float* p;
   int splits;
+  int r0 = 0;
 };
 
 // x = fp32(hidden_in); h = RMSNorm(x) * gain. bf16 mode writes h in the packed
@@ -86,11 +89,14 @@ struct ProjSrc {
   size_t plane;
 };
 
-// q columns [0, n_q d) from qs, key then value columns [0, 2 n_kv d) from kvs.
-hipError_t rope_kv_write(DType dt, ProjSrc qs, ProjSrc kvs, void* q_out, KVLayer kv,
-                         const int32_t* tok_seq, const int32_t* tok_pos, SegTables tabs,
-                         const float* cos_tab, const float* sin_tab, const void* q_gain,
-                         const void* k_gain, float qk_eps, int T, int n_q, hipStream_t s);
+// q columns [0, n_q d) from qs, key then value columns [0, 2 n_kv d) from kvs,
+// for rows t < r0; rows t >= r0 read row t - r0 of qt and kvt instead (the
+// split-K product of a step's last rows; r0 = T: no such rows).
+hipError_t rope_kv_write(DType dt, ProjSrc qs, ProjSrc kvs, ProjSrc qt, ProjSrc kvt, int r0,
+                         void* q_out, KVLayer kv, const int32_t* tok_seq, const int32_t* tok_pos,
+                         SegTables tabs, const float* cos_tab, const float* sin_tab,
+                         const void* q_gain, const void* k_gain, float qk_eps, int T, int n_q,
+                         hipStream_t s);
 
 // fp32 mode: m = silu(gu[:, :F]) * gu[:, F:] (row-major).
 hipError_t swiglu_f32(const float* gu, float* m, int T, int F, hipStream_t s);

@@ -36,6 +36,7 @@ constexpr int kMaxSplits = 32;       // decode key splits per sequence, at most
 constexpr int kSplitMinBlocks = 4;   // at least 4 blocks (64 keys) per split
 constexpr int kSkinnyMaxRows = 128;  // decode-sized steps use split-K GEMMs
 constexpr int kMaxKvSplits = 4;      // K splits of the key/value columns of a prefill QKV
+constexpr int kMaxTokens = 65535;    // rows of a step (RoPE runs a grid row per token)
 constexpr int kMaxMidSplits = 8;     // K splits of the products of a small tiled step
 constexpr int kMidRows = 2048;       // partial-plane rows of such a step (splits x T)
 
@@ -76,6 +77,7 @@ struct stage {
   int cus = 256;  // compute units of the device
   int attn_waves = 1600;
   int pf_tiles = 2;  // prefill attention row tiles per wave (2 or 4; 2 measured faster)
+  bool row_tail_on = true;  // split-K skinny products for the last rows of large steps
 
   // workspace
   Region r_x, r_h, r_qkv, r_kvpart, r_q, r_attn, r_m, r_gu, r_part_x, r_part_o, r_part_ml, r_meta,
@@ -206,7 +208,12 @@ void plan_workspace(stage* st) {
   take(st->r_m, Tp * F * es);
   const size_t gu_rows = c.dtype == STAGE_F32 ? T : (st->s_gu > 1 ? (size_t)st->s_gu * R : 0);
   take(st->r_gu, gu_rows * 2 * F * 4);
-  take(st->r_part_x, std::max((size_t)std::max(st->s_o, st->s_down) * R, mid_rows) * H * 4);
+  // split-K planes of the O / down products of skinny steps and of the last
+  // rows of a large step, the mid-split planes, and the QKV planes of the
+  // last rows (only one of them is live at a time)
+  take(st->r_part_x, std::max({(size_t)std::max(st->s_o, st->s_down) * R * H, mid_rows * H,
+                               c.dtype == STAGE_BF16 && T > R ? (size_t)st->s_qkv * R * qkvw : 0}) *
+                         4);
   const size_t max_items = c.dtype == STAGE_BF16 ? (size_t)st->max_seqs * kMaxSplits : 0;
   take(st->r_part_o, max_items * qw * 4);
   take(st->r_part_ml, max_items * c.n_q_heads * 2 * 4);
@@ -340,6 +347,34 @@ int mid_splits(const stage* st, int T, int N, int K) {
   return best;
 }
 
+// Rows of a large bf16 step past its last multiple of 256 (at most the
+// skinny limit of them): the candidates for the split-K skinny kernels
+// (row_tail_for), with the rows before them on whole tiles. Only when the
+// whole-tile part needs no K splits of its own.
+int row_tail(const stage* st, int T) {
+  if (st->cfg.dtype != STAGE_BF16 || T <= st->skinny_rows || !st->row_tail_on) return 0;
+  const int rt = T % 256, T0 = T - rt;
+  if (rt == 0 || rt > st->skinny_rows || T0 < 256) return 0;
+  const auto& c = st->cfg;
+  const int qw = c.n_q_heads * c.head_dim, qkvw = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  if (mid_splits(st, T0, qkvw, c.hidden) || mid_splits(st, T0, c.hidden, qw) ||
+      mid_splits(st, T0, c.hidden, c.ffn))
+    return 0;
+  return rt;
+}
+
+// Whether a product with N tile columns (N of them in 256-wide tiles; for
+// QKV with split key/value columns, the query columns) runs its last rt rows
+// on the skinny kernel: only when those rows' extra 256-row tiles would add
+// a round of workgroups (a mostly idle one: the product then costs about one
+// more round of tiles, against one HBM-bound pass over its weights).
+bool row_tail_for(const stage* st, int T, int rt, int N) {
+  if (rt == 0 || N % 256 != 0) return false;
+  const long cols = N / 256;
+  const long with = (T + 255) / 256 * cols, without = (T - rt) / 256 * cols;
+  return (with + st->cus - 1) / st->cus > (without + st->cus - 1) / st->cus;
+}
+
 // Take the next pinned staging slot of the ring, waiting until the upload
 // that last used it has been consumed.
 stage_status take_slot(stage* st, int* slot) {
@@ -438,9 +473,20 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
   // projections as partial sums in part_x; the next RMSNorm (or the output
   // cast) adds them to the residual stream. The first layer's input norm
   // (which reads hidden_in) is launched before it.
-  const int kv_splits = skinny ? 0 : qkv_kv_splits(st, T);
-  const int mq = mid_splits(st, T, qkvw, H), mo = mid_splits(st, T, H, qw),
-            md = mid_splits(st, T, H, F);
+  // rows [T0, T) of a large step may run on the skinny kernels (row_tail):
+  // for each of QKV, O and down separately (rq, ro, rd: 0 or rt)
+  const int rt = skinny ? 0 : row_tail(st, T), T0 = T - rt;
+  const int kv_splits0 = rt ? qkv_kv_splits(st, T0) : 0;
+  const int rq = row_tail_for(st, T, rt, kv_splits0 ? qw : qkvw) ? rt : 0;
+  const int ro = row_tail_for(st, T, rt, H) ? rt : 0, rd = ro;
+  const int Tq = T - rq, To = T - ro, Td = T - rd;  // rows of each product on tiles
+  const int kv_splits = skinny ? 0 : qkv_kv_splits(st, Tq);
+  const int mq = rt ? 0 : mid_splits(st, T, qkvw, H), mo = rt ? 0 : mid_splits(st, T, H, qw),
+            md = rt ? 0 : mid_splits(st, T, H, F);
+  // the tail rows of the packed activations (whole 16-row fragments)
+  auto tail_rows = [&](const void* act, int K) -> const void* {
+    return (const uint16_t*)act + (size_t)(T0 / 16) * (K / 32) * 512;
+  };
   auto layers = [&](Launcher& L, hipStream_t ls) {
     Partials pending{nullptr, 0};
     for (int li = 0; li < st->n_layers; ++li) {
@@ -452,6 +498,15 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
       // where RoPE finds the projection: [T][qkvw], possibly in split planes,
       // or the query columns [T][qw] and split planes of the key/value columns
       ProjSrc qsrc{qkv, qkvw, 1, 0}, kvsrc{qkv + qw, qkvw, 1, 0};
+      ProjSrc qtail = qsrc, kvtail = kvsrc;
+      if (rq > 0) {
+        const size_t plane = (size_t)rq * qkvw;
+        qtail = ProjSrc{part_x, qkvw, st->s_qkv, plane};
+        kvtail = ProjSrc{part_x + qw, qkvw, st->s_qkv, plane};
+        L(STAGE_OP_QKV, [&] {
+          return gemm_skinny(tail_rows(h, H), w.w_qkv, rq, qkvw, H, st->s_qkv, false, part_x, ls);
+        });
+      }
       if (skinny) {
         const size_t plane = (size_t)T * qkvw;
         qsrc = ProjSrc{qkv, qkvw, st->s_qkv, plane};
@@ -466,19 +521,19 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
         float* kvpart = st->at<float>(st->r_kvpart);
         const int kvw = qkvw - qw;
         qsrc = ProjSrc{qkv, qw, 1, 0};
-        kvsrc = ProjSrc{kvpart, kvw, kv_splits, (size_t)T * kvw};
-        L(STAGE_OP_QKV, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_qkv, T, qw, H, qkv, ls); });
+        kvsrc = ProjSrc{kvpart, kvw, kv_splits, (size_t)Tq * kvw};
+        L(STAGE_OP_QKV, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_qkv, Tq, qw, H, qkv, ls); });
         L(STAGE_OP_QKV, [&] {
-          return gemm_split_k(h, (const uint16_t*)w.w_qkv + (size_t)qw * H, T, kvw, H, kv_splits,
+          return gemm_split_k(h, (const uint16_t*)w.w_qkv + (size_t)qw * H, Tq, kvw, H, kv_splits,
                               kvpart, ls);
         });
       } else {
-        L(STAGE_OP_QKV, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_qkv, T, qkvw, H, qkv, ls); });
+        L(STAGE_OP_QKV, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_qkv, Tq, qkvw, H, qkv, ls); });
       }
       L(STAGE_OP_ROPE_KV, [&] {
-        return rope_kv_write(dt, qsrc, kvsrc, q, kvl, dm.tok_seq, dm.tok_pos, tabs, cos_t, sin_t,
-                             c.qk_norm ? w.q_norm : nullptr, c.qk_norm ? w.k_norm : nullptr,
-                             c.qk_rms_eps, T, nq, ls);
+        return rope_kv_write(dt, qsrc, kvsrc, qtail, kvtail, Tq, q, kvl, dm.tok_seq, dm.tok_pos,
+                             tabs, cos_t, sin_t, c.qk_norm ? w.q_norm : nullptr,
+                             c.qk_norm ? w.k_norm : nullptr, c.qk_rms_eps, T, nq, ls);
       });
 
       if (dt == DT_F32) {
@@ -511,7 +566,13 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
         L(STAGE_OP_O, [&] { return gemm_split_k(attn, w.w_o, T, H, qw, mo, part_x, ls); });
         pending = Partials{part_x, mo};
       } else {
-        L(STAGE_OP_O, [&] { return gemm(dt, EPI_RESID_ADD, attn, w.w_o, T, H, qw, x, ls); });
+        L(STAGE_OP_O, [&] { return gemm(dt, EPI_RESID_ADD, attn, w.w_o, To, H, qw, x, ls); });
+        if (ro > 0) {
+          L(STAGE_OP_O, [&] {
+            return gemm_skinny(tail_rows(attn, qw), w.w_o, ro, H, qw, st->s_o, false, part_x, ls);
+          });
+          pending = Partials{part_x, st->s_o, To};
+        }
       }
 
       L(STAGE_OP_NORM, [&] { return rmsnorm(dt, x, pending, h, w.ffn_norm, T, H, c.rms_eps, ls); });
@@ -536,7 +597,14 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
           L(STAGE_OP_DOWN, [&] { return gemm_split_k(m, w.w_down, T, H, F, md, part_x, ls); });
           pending = Partials{part_x, md};
         } else {
-          L(STAGE_OP_DOWN, [&] { return gemm(dt, EPI_RESID_ADD, m, w.w_down, T, H, F, x, ls); });
+          L(STAGE_OP_DOWN, [&] { return gemm(dt, EPI_RESID_ADD, m, w.w_down, Td, H, F, x, ls); });
+          if (rd > 0) {
+            L(STAGE_OP_DOWN, [&] {
+              return gemm_skinny(tail_rows(m, F), w.w_down, rd, H, F, st->s_down, false, part_x,
+                                 ls);
+            });
+            pending = Partials{part_x, st->s_down, Td};
+          }
         }
       } else {
         L(STAGE_OP_GATE_UP, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_gate_up, T, 2 * F, H, gu, ls); });
@@ -548,6 +616,7 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
   // what the last layer leaves for the output cast
   const Partials tail = skinny   ? Partials{part_x, st->s_down}
                         : md > 0 ? Partials{part_x, md}
+                        : rd > 0 ? Partials{part_x, st->s_down, Td}
                                  : Partials{nullptr, 0};
 
   Launcher L{st, s};
@@ -579,6 +648,8 @@ stage_status stage_create(const stage_model_config* cfg, int32_t layer_begin, in
   if (!kv_pool) return fail(STAGE_ERR_INVALID_ARG, "kv_pool is NULL");
   if (num_blocks <= 0 || max_tokens <= 0 || max_seqs <= 0)
     return fail(STAGE_ERR_INVALID_ARG, "num_blocks, max_tokens and max_seqs must be positive");
+  if (max_tokens > kMaxTokens)
+    return fail(STAGE_ERR_INVALID_ARG, "max_tokens %d > %d", max_tokens, kMaxTokens);
   const int n = layer_end - layer_begin;
   for (int i = 0; i < n; ++i) {
     const stage_layer_weights& w = layers[i];
@@ -629,6 +700,7 @@ stage_status stage_create(const stage_model_config* cfg, int32_t layer_begin, in
     st->s_down = skinny_splits(H, F, blocks);
     st->attn_waves = std::max(64, env_int("STAGE_ATTN_WAVES", 1600));
     st->pf_tiles = env_int("STAGE_PF_TILES", 2) == 4 ? 4 : 2;
+    st->row_tail_on = env_int("STAGE_ROW_TAIL", 1) != 0;
   }
   plan_workspace(st);
   for (int i = 0; i < kRing; ++i) {

@@ -179,6 +179,49 @@ def test_mixed_step(dtype, shape):
         pair.close()
 
 
+@pytest.mark.parametrize("shape", [synth.TINY, QWEN_SMALL], ids=["tiny", "qwen-small"])
+def test_last_rows_of_large_steps_on_split_k(shape):
+    """Steps of 256 k + r rows (k >= 5, 0 < r <= 128): the first 256 k rows run
+    on whole 256-row tiles and the last r on the split-K kernels, whose
+    partial planes RoPE, the RMSNorms and the output cast add to those rows
+    only. Covers a prefill-only step with r = 128, a mixed step whose last
+    rows are all decodes (r = 40), and r = 129 (no split) for contrast."""
+    seed = 61
+    dtype = "bf16"
+    log(f"row tail {shape.name}")
+    d_ctx0 = synth.uniform_lengths(seed, 1, 40, 5, 60).astype(np.int32)
+    # four prompts: a first prefill of [500, 480, 300, 128] tokens, then
+    # continuations of [600, 680] and [1280, 129] tokens
+    totals = np.array([1100, 1160, 1580, 257], np.int32)
+    alloc = synth.BlockAllocator(512, seed)
+    dbt = synth.make_block_tables(d_ctx0 + 4, 8, alloc)
+    pbt = synth.make_block_tables(totals, 100, alloc)
+    pair = Pair(shape, dtype, 2, 512, 1536, 48, seed)
+    try:
+        # decode contexts (T = sum of 40 lengths: small, split-K or mid-split)
+        y, yr, x = pair.prefill(d_ctx0, np.zeros(40, np.int32), dbt,
+                                synth.hidden_states(seed, 2, int(d_ctx0.sum()), shape.hidden))
+        _check("context prefill", y, yr, x, TOL[dtype])
+        # prefill-only step of 1408 = 5 * 256 + 128 rows
+        q1 = np.array([500, 480, 300, 128], np.int32)
+        y, yr, x = pair.prefill(q1, np.zeros(4, np.int32), pbt,
+                                synth.hidden_states(seed, 3, int(q1.sum()), shape.hidden))
+        _check("prefill 1408", y, yr, x, TOL[dtype])
+        # mixed step: 1280 prefill rows (continuations) + 40 decodes = 1320 rows
+        pq = np.array([600, 680], np.int32)
+        y, yr, x = pair.mixed(pq, q1[:2], pbt[:2].copy(), d_ctx0, dbt,
+                              synth.hidden_states(seed, 4, 1320, shape.hidden))
+        _check("mixed 1320", y, yr, x, TOL[dtype])
+        # 1409 = 5 * 256 + 129 rows: no split
+        q3 = np.array([1280, 129], np.int32)
+        y, yr, x = pair.prefill(q3, q1[2:], pbt[2:].copy(),
+                                synth.hidden_states(seed, 5, 1409, shape.hidden))
+        _check("prefill 1409", y, yr, x, TOL[dtype])
+        assert pair.kv_errors() <= TOL[dtype]
+    finally:
+        pair.close()
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_qwen_small_long_context_decode(dtype):
     """head_dim 128, GQA group 8, q/k-norm, contexts long enough for many
