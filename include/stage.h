@@ -148,9 +148,8 @@ stage_status stage_pack_weight(const stage_model_config* cfg, stage_weight_kind 
  *            pointers, borrowed: they must outlive the stage).
  *  kv_pool:  device pointer to the KV pool (layout above), borrowed.
  *  num_blocks: blocks per layer in kv_pool.
- *  max_tokens: largest T of any call (at most 65535); max_seqs: largest
- *            number of sequences (prefill + decode) of any call. They size
- *            the workspace.
+ *  max_tokens: largest T of any call; max_seqs: largest number of sequences
+ *            (prefill + decode) of any call. They size the workspace.
  * The stage keeps host-side state only (including a small pinned staging
  * buffer); device scratch memory is supplied by stage_bind_workspace.
  * Returns STAGE_ERR_DEVICE if no HIP device is usable. */

@@ -114,26 +114,16 @@ __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const InT* __restrict
 // of 8 consecutive rows for 8 column groups, i.e. 8 whole 128-byte lines of
 // the packed layout (one row per block would write 16 bytes per line and
 // leave each line to be completed by 15 other blocks). H % 1024 == 0 and
-// H <= 8192 (at most 8 passes held in registers). Rows from r0 on (r0 % 8
-// == 0, so a block's rows all have partials or none) first add `splits`
-// (<= kNormMaxSplits) partial planes of (T - r0) rows and store x back.
-// Those blocks read several times the bytes of the others, so blocks are
-// taken in reverse row order: the last rows are dispatched first.
-constexpr int kNormMaxSplits = 8;
-__global__ __launch_bounds__(1024) void rmsnorm_rows8_kernel(float* __restrict__ x, int T, int H,
-                                                            const float* __restrict__ part,
-                                                            int splits, int r0,
-                                                            bf16_t* __restrict__ h,
+// H <= 8192 (at most 8 passes held in registers).
+__global__ __launch_bounds__(1024) void rmsnorm_rows8_kernel(const float* __restrict__ x, int T,
+                                                            int H, bf16_t* __restrict__ h,
                                                             const bf16_t* __restrict__ gain,
                                                             float eps) {
   constexpr int kMaxPass = 8;
   __shared__ float red[16][8];
   const int tau = threadIdx.x, r = tau & 7, kg = tau >> 3;
-  const int grp = gridDim.x - 1 - blockIdx.x;
-  const int row = grp * 8 + r;
+  const int row = blockIdx.x * 8 + r;
   const bool ok = row < T;
-  const bool adds = splits > 0 && grp * 8 >= r0;
-  const size_t plane = (size_t)(T - r0) * H;
   const int passes = H / 1024;
   float v[kMaxPass][8];
   float ss = 0.f;
@@ -145,25 +135,6 @@ __global__ __launch_bounds__(1024) void rmsnorm_rows8_kernel(float* __restrict__
       if (ok) {
         a = *(const float4*)(x + (size_t)row * H + k);
         b = *(const float4*)(x + (size_t)row * H + k + 4);
-        if (adds) {
-          // all of the pass's partial loads in flight together, summed in plane order
-          const float* pp = part + (size_t)(row - r0) * H + k;
-          float4 pa[kNormMaxSplits], pb[kNormMaxSplits];
-#pragma unroll
-          for (int sp = 0; sp < kNormMaxSplits; ++sp)
-            if (sp < splits) {
-              pa[sp] = *(const float4*)(pp + sp * plane);
-              pb[sp] = *(const float4*)(pp + sp * plane + 4);
-            }
-#pragma unroll
-          for (int sp = 0; sp < kNormMaxSplits; ++sp)
-            if (sp < splits) {
-              add4(a, pa[sp]);
-              add4(b, pb[sp]);
-            }
-          *(float4*)(x + (size_t)row * H + k) = a;
-          *(float4*)(x + (size_t)row * H + k + 4) = b;
-        }
       }
       v[p][0] = a.x; v[p][1] = a.y; v[p][2] = a.z; v[p][3] = a.w;
       v[p][4] = b.x; v[p][5] = b.y; v[p][6] = b.z; v[p][7] = b.w;
@@ -259,9 +230,10 @@ __device__ __forceinline__ const int32_t* seq_table(const SegTables& t, int seq)
 
 // One wave per (token, head); heads [0, n_q) are query heads, [n_q, n_q+n_kv)
 // key/value heads. Lane j < d/2 owns the rotate-half pair (j, j + d/2). The
-// projection of a column is the sum of its source's partial planes. Grid
-// (head groups, tokens) with tokens taken last to first, so that the last
-// rows, whose source may have more planes, are dispatched first.
+// projection of a column is the sum of its source's partial planes. A 1-D
+// grid of (token, group of 4 heads) pairs, token fastest within a group:
+// first the rows t >= r0 (whose source may have several planes, so they
+// are dispatched first), then the rows before r0.
 template <typename T>
 __global__ __launch_bounds__(256) void rope_kv_kernel(ProjSrc qs, ProjSrc kvs, ProjSrc qt,
                                                       ProjSrc kvt, int r0, int n_tok,
@@ -274,8 +246,18 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(ProjSrc qs, ProjSrc kvs, P
                                                       const T* __restrict__ q_gain,
                                                       const T* __restrict__ k_gain, float qk_eps,
                                                       int n_q) {
-  const int t = n_tok - 1 - blockIdx.y;
-  const int hh = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int G = (n_q + n_kv + 3) >> 2;  // head groups
+  const int nt = n_tok - r0;            // rows from r0 on
+  const int wg = blockIdx.x;
+  int t, grp;
+  if (wg < nt * G) {
+    grp = wg / nt;
+    t = r0 + wg % nt;
+  } else {
+    grp = (wg - nt * G) / r0;
+    t = (wg - nt * G) % r0;
+  }
+  const int hh = grp * 4 + (threadIdx.x >> 6);
   if (hh >= n_q + n_kv) return;
   const int lane = threadIdx.x & 63;
   const int half = d >> 1;
@@ -408,10 +390,20 @@ hipError_t embed_norm(DType dt, const void* hidden_in, float* x, void* h, const 
 hipError_t rmsnorm(DType dt, float* x, Partials add, void* h, const void* gain, int T, int H,
                    float eps, hipStream_t s) {
   if (T == 0) return hipSuccess;
-  if (dt == DT_BF16 && add.r0 % 8 == 0 && add.splits <= kNormMaxSplits && T >= 1024 &&
-      H % 1024 == 0 && H <= 8192) {
-    rmsnorm_rows8_kernel<<<(T + 7) / 8, 1024, 0, s>>>(x, T, H, add.p, add.splits, add.r0,
-                                                      (bf16_t*)h, (const bf16_t*)gain, eps);
+  if (dt == DT_BF16 && T >= 1024 && H % 1024 == 0 && H <= 8192 &&
+      (add.splits == 0 || (add.r0 > 0 && add.r0 % 16 == 0))) {
+    // rows with partial sums (a step's last rows) take one row per block,
+    // spread over the chip: 8 such rows in one block would read all their
+    // planes through one CU
+    const int r0 = add.splits ? add.r0 : T;
+    if (r0 < T) {
+      const hipError_t e = launch_norm<float, bf16_t, false>(
+          nullptr, nullptr, x + (size_t)r0 * H, Partials{add.p, add.splits},
+          (bf16_t*)h + packed_a_offset(r0, 0, H), (const bf16_t*)gain, T - r0, H, eps, s);
+      if (e != hipSuccess) return e;
+    }
+    rmsnorm_rows8_kernel<<<(r0 + 7) / 8, 1024, 0, s>>>(x, r0, H, (bf16_t*)h, (const bf16_t*)gain,
+                                                       eps);
     return hipGetLastError();
   }
   if (dt == DT_BF16)
@@ -443,8 +435,7 @@ hipError_t rope_kv_write(DType dt, ProjSrc qs, ProjSrc kvs, ProjSrc qt, ProjSrc 
   if (r0 < 0 || r0 > T) return hipErrorInvalidValue;
   if ((r0 > 0 && (qs.splits < 1 || kvs.splits < 1)) || (r0 < T && (qt.splits < 1 || kvt.splits < 1)))
     return hipErrorInvalidValue;
-  if (T > 65535) return hipErrorInvalidValue;
-  dim3 grid((n_q + kv.n_kv + 3) / 4, T);
+  dim3 grid(T * ((n_q + kv.n_kv + 3) / 4));
   if (dt == DT_BF16)
     rope_kv_kernel<bf16_t><<<grid, 256, 0, s>>>(qs, kvs, qt, kvt, r0, T, (bf16_t*)q_out, (bf16_t*)kv.base,
                                                 kv.n_kv, kv.head_dim, tok_seq, tok_pos, tabs,

@@ -36,7 +36,6 @@ constexpr int kMaxSplits = 32;       // decode key splits per sequence, at most
 constexpr int kSplitMinBlocks = 4;   // at least 4 blocks (64 keys) per split
 constexpr int kSkinnyMaxRows = 128;  // decode-sized steps use split-K GEMMs
 constexpr int kMaxKvSplits = 4;      // K splits of the key/value columns of a prefill QKV
-constexpr int kMaxTokens = 65535;    // rows of a step (RoPE runs a grid row per token)
 constexpr int kMaxMidSplits = 8;     // K splits of the products of a small tiled step
 constexpr int kMidRows = 2048;       // partial-plane rows of such a step (splits x T)
 
@@ -648,8 +647,6 @@ stage_status stage_create(const stage_model_config* cfg, int32_t layer_begin, in
   if (!kv_pool) return fail(STAGE_ERR_INVALID_ARG, "kv_pool is NULL");
   if (num_blocks <= 0 || max_tokens <= 0 || max_seqs <= 0)
     return fail(STAGE_ERR_INVALID_ARG, "num_blocks, max_tokens and max_seqs must be positive");
-  if (max_tokens > kMaxTokens)
-    return fail(STAGE_ERR_INVALID_ARG, "max_tokens %d > %d", max_tokens, kMaxTokens);
   const int n = layer_end - layer_begin;
   for (int i = 0; i < n; ++i) {
     const stage_layer_weights& w = layers[i];
