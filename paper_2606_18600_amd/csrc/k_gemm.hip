@@ -11,7 +11,7 @@
 //   partial tile per K split; the consumer kernel sums the splits. With one
 //   split the gate-up GEMM applies SwiGLU in its epilogue.
 // * gemm_tiled_bf16: many rows (prefill, mixed steps), compute-bound.
-//   256 x 256 (8 waves of 128 x 64) or 128 x 128 block tiles; whole fragments
+//   256 x 256 (8 waves of 64 x 128) or 128 x 128 block tiles; whole fragments
 //   copied HBM -> LDS with direct loads, 64-wide k steps double-buffered;
 //   epilogues: fp32 store, residual add, SwiGLU.
 // * gemm_tiled_f32: plain fp32 SIMT tiles for the fp32 mode (row-major).
@@ -457,7 +457,7 @@ hipError_t gemm_split_k(const void* A, const void* W, int M, int N, int K, int s
   if (M == 0) return hipSuccess;
   if (splits < 1 || N % 256 != 0 || K % (64 * splits) != 0) return hipErrorInvalidValue;
   dim3 grid((M + 255) / 256, N / 256, splits);
-  gemm_tiled_bf16<16, 4, 2, 4, EPI_STORE_F32><<<grid, 512, 0, s>>>(
+  gemm_tiled_bf16<16, 4, 4, 2, EPI_STORE_F32><<<grid, 512, 0, s>>>(
       (const bf16_t*)A, (const bf16_t*)W, M, N, K, out, N, K / splits, (size_t)M * N);
   return hipGetLastError();
 }
@@ -495,9 +495,9 @@ hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int
     if (big) {
       dim3 grid(mb256, Nl / 256);
       switch (epi) {
-        case EPI_STORE_F32: gemm_tiled_bf16<16, 4, 2, 4, EPI_STORE_F32><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0); break;
-        case EPI_RESID_ADD: gemm_tiled_bf16<16, 4, 2, 4, EPI_RESID_ADD><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0); break;
-        case EPI_SWIGLU: gemm_tiled_bf16<16, 4, 2, 4, EPI_SWIGLU><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0); break;
+        case EPI_STORE_F32: gemm_tiled_bf16<16, 4, 4, 2, EPI_STORE_F32><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0); break;
+        case EPI_RESID_ADD: gemm_tiled_bf16<16, 4, 4, 2, EPI_RESID_ADD><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0); break;
+        case EPI_SWIGLU: gemm_tiled_bf16<16, 4, 4, 2, EPI_SWIGLU><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0); break;
         default: return hipErrorInvalidValue;
       }
     } else {
