@@ -233,10 +233,11 @@ __device__ __forceinline__ const int32_t* seq_table(const SegTables& t, int seq)
 // projection of a column is the sum of its source's partial planes. A 1-D
 // grid of (token, group of 4 heads) pairs, token fastest within a group:
 // first the rows t >= r0 (whose source may have several planes, so they
-// are dispatched first), then the rows before r0.
+// are dispatched first), then the rows before r0, whose groups start at
+// g_lo (past the query heads when their queries are already rotated).
 template <typename T>
 __global__ __launch_bounds__(256) void rope_kv_kernel(ProjSrc qs, ProjSrc kvs, ProjSrc qt,
-                                                      ProjSrc kvt, int r0, int n_tok,
+                                                      ProjSrc kvt, int r0, int g_lo, int n_tok,
                                                       T* __restrict__ q_out,
                                                       T* __restrict__ kv, int n_kv, int d,
                                                       const int32_t* tok_seq,
@@ -254,7 +255,7 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(ProjSrc qs, ProjSrc kvs, P
     grp = wg / nt;
     t = r0 + wg % nt;
   } else {
-    grp = (wg - nt * G) / r0;
+    grp = g_lo + (wg - nt * G) / r0;
     t = (wg - nt * G) % r0;
   }
   const int hh = grp * 4 + (threadIdx.x >> 6);
@@ -427,22 +428,24 @@ hipError_t output_cast(DType dt, const float* x, Partials add, void* out, int T,
 }
 
 hipError_t rope_kv_write(DType dt, ProjSrc qs, ProjSrc kvs, ProjSrc qt, ProjSrc kvt, int r0,
-                         void* q_out, KVLayer kv, const int32_t* tok_seq, const int32_t* tok_pos,
-                         SegTables tabs, const float* cos_tab, const float* sin_tab,
-                         const void* q_gain, const void* k_gain, float qk_eps, int T, int n_q,
-                         hipStream_t s) {
+                         bool q_done, void* q_out, KVLayer kv, const int32_t* tok_seq,
+                         const int32_t* tok_pos, SegTables tabs, const float* cos_tab,
+                         const float* sin_tab, const void* q_gain, const void* k_gain,
+                         float qk_eps, int T, int n_q, hipStream_t s) {
   if (T == 0) return hipSuccess;
   if (r0 < 0 || r0 > T) return hipErrorInvalidValue;
   if ((r0 > 0 && (qs.splits < 1 || kvs.splits < 1)) || (r0 < T && (qt.splits < 1 || kvt.splits < 1)))
     return hipErrorInvalidValue;
-  dim3 grid(T * ((n_q + kv.n_kv + 3) / 4));
+  if (q_done && n_q % 4 != 0) return hipErrorInvalidValue;
+  const int G = (n_q + kv.n_kv + 3) / 4, g_lo = q_done ? n_q / 4 : 0;
+  dim3 grid((T - r0) * G + r0 * (G - g_lo));
   if (dt == DT_BF16)
-    rope_kv_kernel<bf16_t><<<grid, 256, 0, s>>>(qs, kvs, qt, kvt, r0, T, (bf16_t*)q_out, (bf16_t*)kv.base,
+    rope_kv_kernel<bf16_t><<<grid, 256, 0, s>>>(qs, kvs, qt, kvt, r0, g_lo, T, (bf16_t*)q_out, (bf16_t*)kv.base,
                                                 kv.n_kv, kv.head_dim, tok_seq, tok_pos, tabs,
                                                 cos_tab, sin_tab, (const bf16_t*)q_gain,
                                                 (const bf16_t*)k_gain, qk_eps, n_q);
   else
-    rope_kv_kernel<float><<<grid, 256, 0, s>>>(qs, kvs, qt, kvt, r0, T, (float*)q_out, (float*)kv.base,
+    rope_kv_kernel<float><<<grid, 256, 0, s>>>(qs, kvs, qt, kvt, r0, g_lo, T, (float*)q_out, (float*)kv.base,
                                                kv.n_kv, kv.head_dim, tok_seq, tok_pos, tabs,
                                                cos_tab, sin_tab, (const float*)q_gain,
                                                (const float*)k_gain, qk_eps, n_q);

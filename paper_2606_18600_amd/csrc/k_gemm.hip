@@ -212,7 +212,8 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tiled_bf16(const bf16_t* __
                                                                const bf16_t* __restrict__ W,
                                                                int M, int N, int K,
                                                                void* __restrict__ out, int ldo,
-                                                               int k_len, size_t out_plane) {
+                                                               int k_len, size_t out_plane,
+                                                               RopeRows rope) {
   constexpr int NW = WM * WN;
   constexpr int AF = BMT * 2;
   constexpr int BF = BNG * 8;
@@ -308,6 +309,31 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tiled_bf16(const bf16_t* __
   // Epilogue: lane l holds column (g*64 + j*16 + l%16), rows (l/16)*4 + r of
   // m-tile (mt0 + wm*TM + i).
   const int r16 = lane & 15;
+  if constexpr (EPI == EPI_ROPE_Q) {
+    // The wave's two groups are the 128 columns of one head, so both members
+    // of each rotate-half pair (jj, jj + 64) are in this lane: tile j of the
+    // first group and tile j of the second.
+    static_assert(TG == 2, "one 128-column head per wave");
+    const int hc = (g0 + wn * TG) * 64;  // the head's first column
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = (mt0 + wm * TM + i) * 16 + (lane >> 4) * 4 + r;
+        if (m >= M) continue;
+        const size_t pr = (size_t)rope.pos[m] * 64;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int jj = j * 16 + r16;
+          const float c = rope.cos_tab[pr + jj], sn = rope.sin_tab[pr + jj];
+          const float a = acc[i][j][r], b = acc[i][4 + j][r];
+          bf16_t* o = (bf16_t*)out + (size_t)m * ldo + hc + jj;
+          o[0] = f32_to_bf16(a * c - b * sn);
+          o[64] = f32_to_bf16(a * sn + b * c);
+        }
+      }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -458,13 +484,23 @@ hipError_t gemm_split_k(const void* A, const void* W, int M, int N, int K, int s
   if (splits < 1 || N % 256 != 0 || K % (64 * splits) != 0) return hipErrorInvalidValue;
   dim3 grid((M + 255) / 256, N / 256, splits);
   gemm_tiled_bf16<16, 4, 4, 2, EPI_STORE_F32><<<grid, 512, 0, s>>>(
-      (const bf16_t*)A, (const bf16_t*)W, M, N, K, out, N, K / splits, (size_t)M * N);
+      (const bf16_t*)A, (const bf16_t*)W, M, N, K, out, N, K / splits, (size_t)M * N, RopeRows{});
   return hipGetLastError();
 }
 
 hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int N, int K,
-                void* out, hipStream_t s) {
+                void* out, hipStream_t s, RopeRows rope) {
   if (M == 0) return hipSuccess;
+  if (epi == EPI_ROPE_Q) {
+    // 256 x 256 tiles only: their waves own one 128-column head each
+    if (dt != DT_BF16 || N % 256 != 0 || K % 64 != 0 || !rope.pos || !rope.cos_tab ||
+        !rope.sin_tab)
+      return hipErrorInvalidValue;
+    dim3 grid((M + 255) / 256, N / 256);
+    gemm_tiled_bf16<16, 4, 4, 2, EPI_ROPE_Q><<<grid, 512, 0, s>>>(
+        (const bf16_t*)A, (const bf16_t*)W, M, N, K, out, N, K, 0, rope);
+    return hipGetLastError();
+  }
   if (dt == DT_F32) {
     dim3 grid((M + TF - 1) / TF, (N + TF - 1) / TF);
     if (epi == EPI_RESID_ADD)
@@ -495,17 +531,17 @@ hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int
     if (big) {
       dim3 grid(mb256, Nl / 256);
       switch (epi) {
-        case EPI_STORE_F32: gemm_tiled_bf16<16, 4, 4, 2, EPI_STORE_F32><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0); break;
-        case EPI_RESID_ADD: gemm_tiled_bf16<16, 4, 4, 2, EPI_RESID_ADD><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0); break;
-        case EPI_SWIGLU: gemm_tiled_bf16<16, 4, 4, 2, EPI_SWIGLU><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0); break;
+        case EPI_STORE_F32: gemm_tiled_bf16<16, 4, 4, 2, EPI_STORE_F32><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0, RopeRows{}); break;
+        case EPI_RESID_ADD: gemm_tiled_bf16<16, 4, 4, 2, EPI_RESID_ADD><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0, RopeRows{}); break;
+        case EPI_SWIGLU: gemm_tiled_bf16<16, 4, 4, 2, EPI_SWIGLU><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0, RopeRows{}); break;
         default: return hipErrorInvalidValue;
       }
     } else {
       dim3 grid(mb128, Nl / 128);
       switch (epi) {
-        case EPI_STORE_F32: gemm_tiled_bf16<8, 2, 2, 2, EPI_STORE_F32><<<grid, 256, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0); break;
-        case EPI_RESID_ADD: gemm_tiled_bf16<8, 2, 2, 2, EPI_RESID_ADD><<<grid, 256, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0); break;
-        case EPI_SWIGLU: gemm_tiled_bf16<8, 2, 2, 2, EPI_SWIGLU><<<grid, 256, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0); break;
+        case EPI_STORE_F32: gemm_tiled_bf16<8, 2, 2, 2, EPI_STORE_F32><<<grid, 256, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0, RopeRows{}); break;
+        case EPI_RESID_ADD: gemm_tiled_bf16<8, 2, 2, 2, EPI_RESID_ADD><<<grid, 256, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0, RopeRows{}); break;
+        case EPI_SWIGLU: gemm_tiled_bf16<8, 2, 2, 2, EPI_SWIGLU><<<grid, 256, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0, RopeRows{}); break;
         default: return hipErrorInvalidValue;
       }
     }

@@ -16,7 +16,16 @@ enum Epilogue {
   EPI_STORE_F32 = 0,  // out (fp32, [M, N]) = acc
   EPI_RESID_ADD = 1,  // out (fp32 residual, [M, N]) += acc
   EPI_SWIGLU = 2,     // W = [gate (N/2 rows); up (N/2 rows)]; out (mode dtype, [M, N/2]) = silu(g) * u
-  EPI_ATOMIC_F32 = 3  // out (fp32, [M, N]) += acc with atomics (split-K partial sums)
+  EPI_ROPE_Q = 3      // query columns, head_dim 128 (bf16 only): out (bf16, [M, N] row-major) =
+                      // rotate-half RoPE of acc at the row's position (RopeRows)
+};
+
+// Positions of the rows and the rotary tables ([positions][64] cos and sin)
+// for EPI_ROPE_Q.
+struct RopeRows {
+  const int32_t* pos = nullptr;
+  const float* cos_tab = nullptr;
+  const float* sin_tab = nullptr;
 };
 
 // Block tables of the (at most) two segments of a step: sequences
@@ -91,12 +100,15 @@ struct ProjSrc {
 
 // q columns [0, n_q d) from qs, key then value columns [0, 2 n_kv d) from kvs,
 // for rows t < r0; rows t >= r0 read row t - r0 of qt and kvt instead (the
-// split-K product of a step's last rows; r0 = T: no such rows).
+// split-K product of a step's last rows; r0 = T: no such rows). With
+// q_done, rows t < r0 already have their rotated queries in q_out (the QKV
+// product applied RoPE, EPI_ROPE_Q) and only their key/value heads are
+// processed (n_q % 4 == 0).
 hipError_t rope_kv_write(DType dt, ProjSrc qs, ProjSrc kvs, ProjSrc qt, ProjSrc kvt, int r0,
-                         void* q_out, KVLayer kv, const int32_t* tok_seq, const int32_t* tok_pos,
-                         SegTables tabs, const float* cos_tab, const float* sin_tab,
-                         const void* q_gain, const void* k_gain, float qk_eps, int T, int n_q,
-                         hipStream_t s);
+                         bool q_done, void* q_out, KVLayer kv, const int32_t* tok_seq,
+                         const int32_t* tok_pos, SegTables tabs, const float* cos_tab,
+                         const float* sin_tab, const void* q_gain, const void* k_gain,
+                         float qk_eps, int T, int n_q, hipStream_t s);
 
 // fp32 mode: m = silu(gu[:, :F]) * gu[:, F:] (row-major).
 hipError_t swiglu_f32(const float* gu, float* m, int T, int F, hipStream_t s);
@@ -132,7 +144,7 @@ hipError_t gemm_split_k(const void* A, const void* W, int M, int N, int K, int s
                         hipStream_t s);
 // gemm: bf16 = LDS-tiled MFMA over packed A and W; fp32 = SIMT, row-major.
 hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int N, int K,
-                void* out, hipStream_t s);
+                void* out, hipStream_t s, RopeRows rope = RopeRows{});
 
 hipError_t attn_decode(DType dt, const void* q, KVLayer kv, SegTables tabs,
                        const DecodeItem* items, int n_items, int n_q, float* part_o,

@@ -77,6 +77,7 @@ struct stage {
   int attn_waves = 1600;
   int pf_tiles = 2;  // prefill attention row tiles per wave (2 or 4; 2 measured faster)
   bool row_tail_on = true;  // split-K skinny products for the last rows of large steps
+  bool q_rope_fused = true;  // RoPE in the epilogue of a step's query product (when possible)
 
   // workspace
   Region r_x, r_h, r_qkv, r_kvpart, r_q, r_attn, r_m, r_gu, r_part_x, r_part_o, r_part_ml, r_meta,
@@ -480,6 +481,10 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
   const int ro = row_tail_for(st, T, rt, H) ? rt : 0, rd = ro;
   const int Tq = T - rq, To = T - ro, Td = T - rd;  // rows of each product on tiles
   const int kv_splits = skinny ? 0 : qkv_kv_splits(st, Tq);
+  // with split key/value columns the query product applies RoPE in its
+  // epilogue (one 128-column head per wave) unless q/k RMSNorm comes first
+  const bool q_fused = kv_splits > 0 && !c.qk_norm && D == 128 && nq % 4 == 0 &&
+                       st->q_rope_fused;
   const int mq = rt ? 0 : mid_splits(st, T, qkvw, H), mo = rt ? 0 : mid_splits(st, T, H, qw),
             md = rt ? 0 : mid_splits(st, T, H, F);
   // the tail rows of the packed activations (whole 16-row fragments)
@@ -521,7 +526,13 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
         const int kvw = qkvw - qw;
         qsrc = ProjSrc{qkv, qw, 1, 0};
         kvsrc = ProjSrc{kvpart, kvw, kv_splits, (size_t)Tq * kvw};
-        L(STAGE_OP_QKV, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_qkv, Tq, qw, H, qkv, ls); });
+        if (q_fused)
+          L(STAGE_OP_QKV, [&] {
+            return gemm(dt, EPI_ROPE_Q, h, w.w_qkv, Tq, qw, H, q, ls,
+                        RopeRows{dm.tok_pos, cos_t, sin_t});
+          });
+        else
+          L(STAGE_OP_QKV, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_qkv, Tq, qw, H, qkv, ls); });
         L(STAGE_OP_QKV, [&] {
           return gemm_split_k(h, (const uint16_t*)w.w_qkv + (size_t)qw * H, Tq, kvw, H, kv_splits,
                               kvpart, ls);
@@ -530,8 +541,8 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
         L(STAGE_OP_QKV, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_qkv, Tq, qkvw, H, qkv, ls); });
       }
       L(STAGE_OP_ROPE_KV, [&] {
-        return rope_kv_write(dt, qsrc, kvsrc, qtail, kvtail, Tq, q, kvl, dm.tok_seq, dm.tok_pos,
-                             tabs, cos_t, sin_t, c.qk_norm ? w.q_norm : nullptr,
+        return rope_kv_write(dt, qsrc, kvsrc, qtail, kvtail, Tq, q_fused, q, kvl, dm.tok_seq,
+                             dm.tok_pos, tabs, cos_t, sin_t, c.qk_norm ? w.q_norm : nullptr,
                              c.qk_norm ? w.k_norm : nullptr, c.qk_rms_eps, T, nq, ls);
       });
 
@@ -698,6 +709,7 @@ stage_status stage_create(const stage_model_config* cfg, int32_t layer_begin, in
     st->attn_waves = std::max(64, env_int("STAGE_ATTN_WAVES", 1600));
     st->pf_tiles = env_int("STAGE_PF_TILES", 2) == 4 ? 4 : 2;
     st->row_tail_on = env_int("STAGE_ROW_TAIL", 1) != 0;
+    st->q_rope_fused = env_int("STAGE_Q_ROPE", 1) != 0;
   }
   plan_workspace(st);
   for (int i = 0; i < kRing; ++i) {
