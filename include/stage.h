@@ -38,7 +38,15 @@
  *    load of the attention kernels is contiguous:
  *      K[o][d] at (d / 32) * 512 + (o + 16 * ((d % 32) / 8)) * 8 + d % 8
  *      V[o][d] at (d / 32) * 512 + (d % 16 + 16 * (o / 4)) * 8 + ((d / 16) % 2) * 4 + o % 4
- *    Block ids index the same blocks in every layer of the stage.
+ *    Block ids index the same blocks in every layer of the stage. The
+ *    entries a call reads (the first ceil((ctx_lens[i] + q_lens[i]) /
+ *    block_size) of row i) must lie in [0, num_blocks): the kernels read
+ *    them on the device and do not check them, so an id outside that range
+ *    is an out-of-bounds access of the pool. With the environment variable
+ *    STAGE_DEBUG=1 set when a stage is created, every forward call first
+ *    copies the tables it uses to the host (synchronising the stream) and
+ *    rejects out-of-range ids with STAGE_ERR_INVALID_ARG before enqueuing
+ *    anything: a debugging aid, not for serving.
  *  - hidden_in / hidden_out: [T, hidden] in the mode dtype, rows packed
  *    sequence by sequence in batch order (for stage_step_mixed: all prefill
  *    rows first, then the decode rows). hidden_out may alias hidden_in.
@@ -162,9 +170,9 @@ stage_status stage_create(const stage_model_config* cfg, int32_t layer_begin, in
 size_t stage_workspace_bytes(const stage_t* st);
 
 /* Bind caller-owned device memory of at least stage_workspace_bytes() bytes
- * (256-byte aligned). Synchronously uploads the rotary table and clears the
- * accumulators. Must be called before the first forward call; may be called
- * again to move the workspace. */
+ * (256-byte aligned). Synchronously uploads the rotary cos/sin table into
+ * it; nothing else in it needs initialising. Must be called before the first
+ * forward call; may be called again to move the workspace. */
 stage_status stage_bind_workspace(stage_t* st, void* dev, size_t bytes);
 
 /* Prefill (or chunked prefill / recomputation): every sequence has

@@ -78,6 +78,7 @@ struct stage {
   int pf_tiles = 2;  // prefill attention row tiles per wave (2 or 4; 2 measured faster)
   bool row_tail_on = true;  // split-K skinny products for the last rows of large steps
   bool q_rope_fused = true;  // RoPE in the epilogue of a step's query product (when possible)
+  bool check_tables = false;  // copy block tables to the host and check ids (STAGE_DEBUG)
 
   // workspace
   Region r_x, r_h, r_qkv, r_kvpart, r_q, r_attn, r_m, r_gu, r_part_x, r_part_o, r_part_ml, r_meta,
@@ -426,6 +427,29 @@ struct Launcher {
   }
 };
 
+// Debug mode: bring the table rows a batch reads to the host (after the
+// stream's earlier work, which may have written them) and check every block
+// id the call would read.
+stage_status check_tables_on_host(const stage* st, const stage_batch* b, const char* what,
+                                  hipStream_t s) {
+  if (!b || b->num_seqs == 0) return STAGE_OK;
+  std::vector<int32_t> tab((size_t)b->num_seqs * b->max_blocks_per_seq);
+  hipError_t e = hipMemcpyAsync(tab.data(), b->block_tables, tab.size() * 4,
+                                hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail("block table copy", e);
+  for (int i = 0; i < b->num_seqs; ++i) {
+    const long long nb = ((long long)b->ctx_lens[i] + b->q_lens[i] + kBlock - 1) / kBlock;
+    for (long long j = 0; j < nb; ++j) {
+      const int32_t id = tab[(size_t)i * b->max_blocks_per_seq + j];
+      if (id < 0 || id >= st->num_blocks)
+        return fail(STAGE_ERR_INVALID_ARG, "%s: block_tables[%d][%lld] = %d outside [0, %d)",
+                    what, i, j, id, st->num_blocks);
+    }
+  }
+  return STAGE_OK;
+}
+
 stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, const void* hin,
                       void* hout, void* stream_v) {
   const auto& c = st->cfg;
@@ -439,6 +463,10 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
   hipStream_t s = (hipStream_t)stream_v;
   hipError_t e = hipSetDevice(st->device);
   if (e != hipSuccess) return hip_fail("hipSetDevice", e);
+  if (st->check_tables) {
+    if ((vs = check_tables_on_host(st, pf, "prefill", s)) != STAGE_OK) return vs;
+    if ((vs = check_tables_on_host(st, dc, "decode", s)) != STAGE_OK) return vs;
+  }
 
   const int np = pf ? pf->num_seqs : 0, nd = dc ? dc->num_seqs : 0;
   const DType dt = (DType)c.dtype;
@@ -710,6 +738,7 @@ stage_status stage_create(const stage_model_config* cfg, int32_t layer_begin, in
     st->pf_tiles = env_int("STAGE_PF_TILES", 2) == 4 ? 4 : 2;
     st->row_tail_on = env_int("STAGE_ROW_TAIL", 1) != 0;
     st->q_rope_fused = env_int("STAGE_Q_ROPE", 1) != 0;
+    st->check_tables = env_int("STAGE_DEBUG", 0) != 0;
   }
   plan_workspace(st);
   for (int i = 0; i < kRing; ++i) {

@@ -280,6 +280,37 @@ def test_hidden_out_may_alias_hidden_in(lens):
         pair.close()
 
 
+def test_debug_mode_checks_block_ids_on_the_host(monkeypatch):
+    """With STAGE_DEBUG=1 a call whose block table sends a read past the pool
+    (or below 0) is rejected before anything is enqueued; entries past a
+    sequence's length are not read and not checked."""
+    monkeypatch.setenv("STAGE_DEBUG", "1")
+    seed = 71
+    shape = synth.TINY
+    lens = np.array([20, 9], np.int32)
+    zeros = np.zeros(2, np.int32)
+    bt = synth.make_block_tables(lens, 4, synth.BlockAllocator(16, seed))
+    pair = Pair(shape, "bf16", 2, 16, 64, 4, seed)
+    try:
+        y, yr, x = pair.prefill(lens, zeros, bt, synth.hidden_states(seed, 1, 29, shape.hidden))
+        _check("prefill", y, yr, x, TOL["bf16"])
+        xin = torch.zeros((29, shape.hidden), dtype=torch.bfloat16, device="cuda")
+        for row, col, bad_id in [(1, 0, 16), (0, 1, -1)]:
+            bad = bt.copy()
+            bad[row, col] = bad_id
+            with pytest.raises(S.StageError) as e:
+                pair.gpu.prefill(lens, zeros, torch.from_numpy(bad).cuda(), xin)
+            assert e.value.code == S.STAGE_ERR_INVALID_ARG
+            assert f"block_tables[{row}][{col}]" in str(e.value)
+        unused = bt.copy()
+        unused[1, 3] = 999  # sequence 1 (9 tokens) reads only entry 0
+        torch.cuda.synchronize()
+        pair.gpu.decode(lens, torch.from_numpy(unused).cuda(), xin[:2])
+        torch.cuda.synchronize()
+    finally:
+        pair.close()
+
+
 def test_forward_calls_return_validation_codes():
     shape = synth.TINY
     bt = torch.zeros((2, 4), dtype=torch.int32, device="cuda")
