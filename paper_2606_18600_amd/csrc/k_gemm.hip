@@ -514,26 +514,37 @@ hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int
     return hipGetLastError();
   }
   if (N % 128 != 0 || K % 64 != 0) return hipErrorInvalidValue;
-  // Two tilings: 256 x 256 (8 waves, 128 KB LDS, one block per CU) reaches
-  // about 1.1 PFLOP/s on these shapes, 128 x 128 (4 waves, 64 KB, two per CU)
-  // about 0.97; weigh each by how full its last round of blocks is.
-  auto util = [](long blocks, long slots) {
-    const long rounds = (blocks + slots - 1) / slots;
-    return (double)blocks / (double)(rounds * slots);
-  };
-  const long mb256 = (M + 255) / 256, mb128 = (M + 127) / 128;
+  // Three tilings: 256 x 256 and 192 x 256 (8 waves, one block per CU) and
+  // 128 x 128 (4 waves, two per CU). A product costs about its number of
+  // rounds of workgroups times the time of one round. Taking a round of 256
+  // 256-row tiles as 1: a round of 256 192-row tiles (3/4 of the work) takes
+  // ~0.85 (measured 0.78-0.90), and a round of 512 128 x 128 tiles (half the
+  // work, at ~0.97 against ~1.12 PFLOP/s) ~0.58. 192-row tiles win when they
+  // fill a round that 256-row tiles leave partly idle (e.g. 2176 x 5120
+  // products: 240 tiles instead of 180).
+  auto rounds = [](long blocks, long slots) { return (blocks + slots - 1) / slots; };
+  const long mb256 = (M + 255) / 256, mb192 = (M + 191) / 192, mb128 = (M + 127) / 128;
   const bf16_t* a = (const bf16_t*)A;
   const bf16_t* w = (const bf16_t*)W;
+  enum Tiling { T256, T192, T128 };
   // columns [n0, n0 + Nl) of the product; fp32 outputs keep the row stride N
-  auto launch = [&](bool big, int n0, int Nl) -> hipError_t {
+  auto launch = [&](Tiling t, int n0, int Nl) -> hipError_t {
     const bf16_t* wl = w + (size_t)n0 * K;  // packed groups of 64 rows stay in row order
     void* ol = epi == EPI_SWIGLU ? out : (void*)((float*)out + n0);
-    if (big) {
+    if (t == T256) {
       dim3 grid(mb256, Nl / 256);
       switch (epi) {
         case EPI_STORE_F32: gemm_tiled_bf16<16, 4, 4, 2, EPI_STORE_F32><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0, RopeRows{}); break;
         case EPI_RESID_ADD: gemm_tiled_bf16<16, 4, 4, 2, EPI_RESID_ADD><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0, RopeRows{}); break;
         case EPI_SWIGLU: gemm_tiled_bf16<16, 4, 4, 2, EPI_SWIGLU><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0, RopeRows{}); break;
+        default: return hipErrorInvalidValue;
+      }
+    } else if (t == T192) {
+      dim3 grid(mb192, Nl / 256);
+      switch (epi) {
+        case EPI_STORE_F32: gemm_tiled_bf16<12, 4, 4, 2, EPI_STORE_F32><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0, RopeRows{}); break;
+        case EPI_RESID_ADD: gemm_tiled_bf16<12, 4, 4, 2, EPI_RESID_ADD><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0, RopeRows{}); break;
+        case EPI_SWIGLU: gemm_tiled_bf16<12, 4, 4, 2, EPI_SWIGLU><<<grid, 512, 0, s>>>(a, wl, M, Nl, K, ol, N, K, 0, RopeRows{}); break;
         default: return hipErrorInvalidValue;
       }
     } else {
@@ -547,23 +558,28 @@ hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int
     }
     return hipGetLastError();
   };
-  const bool big = N % 256 == 0 &&
-                   1.12 * util(mb256 * (N / 256), 256) >= 0.97 * util(mb128 * (N / 128), 512);
-  if (!big && epi != EPI_SWIGLU && N % 256 == 0) {
+  Tiling best = T128;
+  double cost = 0.58 * rounds(mb128 * (N / 128), 512);
+  if (N % 256 == 0) {
+    const double c256 = (double)rounds(mb256 * (N / 256), 256);
+    const double c192 = 0.85 * rounds(mb192 * (N / 256), 256);
+    if (c192 < cost) best = T192, cost = c192;
+    if (c256 <= cost) best = T256, cost = c256;
+  }
+  if (best == T128 && epi != EPI_SWIGLU && N % 256 == 0) {
     // When 256-tiles would leave a partial last round, run the columns that
-    // fill whole rounds on 256-tiles and only the rest on 128-tiles (e.g.
-    // QKV at 2048 rows: 8192 columns = one round of 256 blocks, 2048 left).
+    // fill whole rounds on 256-tiles and only the rest on 128-tiles.
     long g = mb256, b = 256;
     while (b) { const long t = g % b; g = b; b = t; }  // gcd(mb256, 256)
     const long per_round = 256 / g;                     // column blocks per whole round
     const int n1 = (int)((N / 256) / per_round * per_round * 256);
     if (n1 >= N / 2 && n1 < N) {
-      const hipError_t e = launch(true, 0, n1);
+      const hipError_t e = launch(T256, 0, n1);
       if (e != hipSuccess) return e;
-      return launch(false, n1, N - n1);
+      return launch(T128, n1, N - n1);
     }
   }
-  return launch(big, 0, N);
+  return launch(best, 0, N);
 }
 
 }  // namespace stage_k

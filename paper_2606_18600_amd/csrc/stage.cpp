@@ -189,8 +189,8 @@ void plan_workspace(stage* st) {
   const size_t T = st->max_tokens, H = c.hidden, D = c.head_dim;
   const size_t qw = (size_t)c.n_q_heads * D, qkvw = (size_t)(c.n_q_heads + 2 * c.n_kv_heads) * D;
   const size_t F = c.ffn, es = st->esize;
-  // GEMM inputs (packed activations) are read in whole 256-row tiles
-  const size_t Tp = (T + 255) / 256 * 256;
+  // GEMM inputs (packed activations) are read in whole 256- or 192-row tiles
+  const size_t Tp = std::max((T + 255) / 256 * 256, (T + 191) / 192 * 192);
   const size_t R = st->skinny_rows;
   size_t off = 0;
   auto take = [&](Region& r, size_t bytes) {

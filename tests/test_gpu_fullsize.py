@@ -196,19 +196,21 @@ def _sample_rows(rng, q_lens, ctx_lens, n):
 
 def test_l70_prefill_chunks_sampled():
     seed, shape, layer = 11, synth.LLAMA70B, 20
-    log("l70 chunked prefill, one layer, 2048 + 952 + 200 tokens")
+    log("l70 chunked prefill, one layer, 2048 + 952 + 200 + 1280 tokens")
     cfg = model_config(shape, "bf16")
     w = device_layer_weights(shape, seed, layer, "bf16")
     w64 = _host64(w)
-    n = 3200
-    bt_np = synth.make_block_tables([n], (n + 15) // 16, synth.BlockAllocator(210, seed))
+    n = 4480
+    bt_np = synth.make_block_tables([n], (n + 15) // 16, synth.BlockAllocator(300, seed))
     bt = torch.from_numpy(bt_np).cuda()
-    st = DeviceStage(shape, "bf16", layer, [pack_layer(cfg, w)], 210, 2048, 4, packed=True)
+    st = DeviceStage(shape, "bf16", layer, [pack_layer(cfg, w)], 300, 2048, 4, packed=True)
     rng = np.random.default_rng(seed)
     try:
-        # 2048 rows: split query / key-value QKV; 952: plain tiles; 200: one
-        # row tile, products split over K
-        for ctx0, q in ((0, 2048), (2048, 952), (3000, 200)):
+        # 2048 rows: split query / key-value QKV with RoPE in the query
+        # product; 952: plain tiles; 200: one row tile, products split over K;
+        # 1280: O and down on 192-row tiles (224 tiles fill a round, 160
+        # 256-row tiles would not)
+        for ctx0, q in ((0, 2048), (2048, 952), (3000, 200), (3200, 1280)):
             x = torch.from_numpy(synth.hidden_states(seed, ctx0, q, shape.hidden)).cuda().to(
                 torch.bfloat16)
             y = st.prefill([q], [ctx0], bt, x)
