@@ -332,15 +332,17 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const float* __restrict
 // below 256 and the rescale is rare after the first stage.
 constexpr int kPfWaves = 4;
 constexpr int kPfBPS = 4;
+// Row tiles per wave. Four tiles per wave do not fit the register budget of
+// two waves per SIMD and measured slower, so only two are built.
+constexpr int kPfRowTiles = 2;
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 // Two workgroups per CU (64 KB of LDS each) need the register budget of two
 // waves per SIMD; one would leave no other wave to overlap a wave's
-// exponentials with MFMA work. (Four row tiles per wave do not fit that
-// budget and run one wave per SIMD.)
+// exponentials with MFMA work.
 template <int D, int RT>
-__global__ __launch_bounds__(kPfWaves * 64) __attribute__((amdgpu_waves_per_eu(RT <= 2 ? 2 : 1)))
+__global__ __launch_bounds__(kPfWaves * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_prefill_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kv, int n_kv, SegTables tabs,
     const PrefillItem* __restrict__ items, int n_q, bf16_t* __restrict__ out) {
@@ -595,9 +597,9 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__
 
 }  // namespace
 
-int prefill_item_positions(DType dt, int group, int row_tiles) {
+int prefill_item_positions(DType dt, int group) {
   (void)dt;
-  return kPfWaves * row_tiles * 16 / group;
+  return kPfWaves * kPfRowTiles * 16 / group;
 }
 
 hipError_t attn_decode(DType dt, const void* q, KVLayer kv, SegTables tabs,
@@ -655,21 +657,18 @@ static void launch_prefill(dim3 grid, hipStream_t s, const void* q, KVLayer kv, 
 }
 
 hipError_t attn_prefill(DType dt, const void* q, KVLayer kv, SegTables tabs,
-                        const PrefillItem* items, int n_items, int n_q, int row_tiles, void* out,
+                        const PrefillItem* items, int n_items, int n_q, void* out,
                         hipStream_t s) {
   if (n_items == 0) return hipSuccess;
-  if (dt != DT_BF16 || (row_tiles != 2 && row_tiles != 4)) return hipErrorInvalidValue;
-  if ((kPfWaves * row_tiles * 16) % (n_q / kv.n_kv) != 0) return hipErrorInvalidValue;
+  if (dt != DT_BF16) return hipErrorInvalidValue;
+  if ((kPfWaves * kPfRowTiles * 16) % (n_q / kv.n_kv) != 0) return hipErrorInvalidValue;
   dim3 grid(n_items, kv.n_kv);
-  if (kv.head_dim == 128) {
-    if (row_tiles == 4) launch_prefill<128, 4>(grid, s, q, kv, tabs, items, n_q, out);
-    else launch_prefill<128, 2>(grid, s, q, kv, tabs, items, n_q, out);
-  } else if (kv.head_dim == 64) {
-    if (row_tiles == 4) launch_prefill<64, 4>(grid, s, q, kv, tabs, items, n_q, out);
-    else launch_prefill<64, 2>(grid, s, q, kv, tabs, items, n_q, out);
-  } else {
+  if (kv.head_dim == 128)
+    launch_prefill<128, kPfRowTiles>(grid, s, q, kv, tabs, items, n_q, out);
+  else if (kv.head_dim == 64)
+    launch_prefill<64, kPfRowTiles>(grid, s, q, kv, tabs, items, n_q, out);
+  else
     return hipErrorInvalidValue;
-  }
   return hipGetLastError();
 }
 

@@ -153,9 +153,9 @@ hipError_t attn_merge(DType dt, const float* part_o, const float* part_ml,
                       const int32_t* tok_item_start, const int32_t* tok_rows, int n_tok, int n_q,
                       int n_kv, int head_dim, void* out, hipStream_t s);
 // Prefill attention: one 4-wave workgroup per (item, kv head), each wave
-// holding row_tiles (2 or 4) tiles of 16 (position, head) rows.
+// holding 2 tiles of 16 (position, head) rows.
 hipError_t attn_prefill(DType dt, const void* q, KVLayer kv, SegTables tabs,
-                        const PrefillItem* items, int n_items, int n_q, int row_tiles, void* out,
+                        const PrefillItem* items, int n_items, int n_q, void* out,
                         hipStream_t s);
 
 // fp32 mode: one wave per (token, head) over rows [t_begin, t_begin + n_tok).
@@ -164,6 +164,6 @@ hipError_t attn_f32(const float* q, KVLayer kv, SegTables tabs, const int32_t* t
                     hipStream_t s);
 
 // Positions handled by one prefill work item for a GQA group size.
-int prefill_item_positions(DType dt, int group, int row_tiles);
+int prefill_item_positions(DType dt, int group);
 
 }  // namespace stage_k

@@ -75,7 +75,6 @@ struct stage {
   // rounding of the split sizes
   int cus = 256;  // compute units of the device
   int attn_waves = 1600;
-  int pf_tiles = 2;  // prefill attention row tiles per wave (2 or 4; 2 measured faster)
   bool row_tail_on = true;  // split-K skinny products for the last rows of large steps
   bool q_rope_fused = true;  // RoPE in the epilogue of a step's query product (when possible)
   bool check_tables = false;  // copy block tables to the host and check ids (STAGE_DEBUG)
@@ -254,7 +253,7 @@ void build_meta(const stage* st, const stage_batch* pf, const stage_batch* dc, S
   const int np = pf ? pf->num_seqs : 0, nd = dc ? dc->num_seqs : 0;
   int row = 0;
   const int ppw = prefill_item_positions((DType)st->cfg.dtype,
-                                         st->cfg.n_q_heads / st->cfg.n_kv_heads, st->pf_tiles);
+                                         st->cfg.n_q_heads / st->cfg.n_kv_heads);
   m.n_pitems = 0;
   for (int s = 0; s < np; ++s) {
     const int q = pf->q_lens[s], ctx = pf->ctx_lens[s];
@@ -582,8 +581,7 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
       } else {
         if (Tp > 0)
           L(STAGE_OP_ATTN, [&] {
-            return attn_prefill(dt, q, kvl, tabs, dm.pitems, hm.n_pitems, nq, st->pf_tiles, attn,
-                                ls);
+            return attn_prefill(dt, q, kvl, tabs, dm.pitems, hm.n_pitems, nq, attn, ls);
           });
         if (nd > 0) {
           L(STAGE_OP_ATTN, [&] {
@@ -735,7 +733,6 @@ stage_status stage_create(const stage_model_config* cfg, int32_t layer_begin, in
     st->s_gu = skinny_splits(2 * F, H, blocks);
     st->s_down = skinny_splits(H, F, blocks);
     st->attn_waves = std::max(64, env_int("STAGE_ATTN_WAVES", 1600));
-    st->pf_tiles = env_int("STAGE_PF_TILES", 2) == 4 ? 4 : 2;
     st->row_tail_on = env_int("STAGE_ROW_TAIL", 1) != 0;
     st->q_rope_fused = env_int("STAGE_Q_ROPE", 1) != 0;
     st->check_tables = env_int("STAGE_DEBUG", 0) != 0;
