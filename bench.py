@@ -591,7 +591,7 @@ def main():
                             args.summary_cmd, alg))
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU: the stage runs on a single MI355X and this build "
+        print(f"bench.py measures one GPU: the stage runs on a single MI355X and the library "
               f"has no multi-GPU path (asked for --gpus {args.gpus}).", file=sys.stderr)
         sys.exit(2)
 

@@ -77,7 +77,7 @@ typedef struct stage stage_t; /* opaque */
 typedef enum {
   STAGE_OK = 0,
   STAGE_ERR_INVALID_ARG = 1, /* null pointer, bad length, inconsistent batch */
-  STAGE_ERR_UNSUPPORTED = 2, /* shape or dtype this build does not implement */
+  STAGE_ERR_UNSUPPORTED = 2, /* shape or dtype the library does not implement */
   STAGE_ERR_OUT_OF_MEMORY = 3, /* host allocation failed */
   STAGE_ERR_DEVICE = 4,      /* a HIP call failed (no device, launch error) */
   STAGE_ERR_CAPACITY = 5     /* batch exceeds max_tokens / max_seqs / table
