@@ -222,6 +222,41 @@ def test_l70_prefill_chunks_sampled():
         st.close()
 
 
+def test_l70_bench_prefill_schedule_sampled():
+    """The prefill bench's launch configuration on one L70 layer: its 8 prompts
+    (U[1024, 4096], the bench's seed) in its 11 chunked steps of at most 2048
+    tokens, among them a step of three prompts with a 3689-token prefix and
+    the final 154-token step. Each step's first and last rows of every prompt
+    plus 4 random rows against the oracle."""
+    seed, shape, layer = 2606, synth.LLAMA70B, 20
+    p_lens = synth.uniform_lengths(seed, 2, 8, 1024, 4096)
+    steps = synth.chunk_schedule(p_lens, 2048)
+    log(f"l70 bench prefill schedule, one layer: {len(steps)} steps, {int(p_lens.sum())} tokens")
+    cfg = model_config(shape, "bf16")
+    w = device_layer_weights(shape, seed, layer, "bf16")
+    w64 = _host64(w)
+    nblk = int(((p_lens + 15) // 16).sum()) + 1
+    bt_np = synth.make_block_tables(p_lens, int(((p_lens + 15) // 16).max()),
+                                    synth.BlockAllocator(nblk, seed))
+    bt_all = torch.from_numpy(bt_np).cuda()
+    st = DeviceStage(shape, "bf16", layer, [pack_layer(cfg, w)], nblk, 2048, 8, packed=True)
+    rng = np.random.default_rng(seed)
+    try:
+        for k, step in enumerate(steps):
+            idx = [int(i) for i, _, _ in step]
+            ctx = [int(c) for _, c, _ in step]
+            q = [int(n) for _, _, n in step]
+            x = torch.from_numpy(synth.hidden_states(seed, 100 + k, sum(q), shape.hidden)).cuda().to(
+                torch.bfloat16)
+            y = st.prefill(q, ctx, bt_all[idx].contiguous(), x)
+            torch.cuda.synchronize()
+            rows = _sample_rows(rng, q, ctx, 4)
+            _check_rows_one_layer(shape, st, w64, bt_np[idx], rows, x.double().cpu().numpy(),
+                                  y.double().cpu().numpy(), f"step {k} {list(zip(ctx, q))}")
+    finally:
+        st.close()
+
+
 def test_q32_mixed_step_sampled():
     seed, shape, layer = 24, synth.QWEN32B, 24
     log("qwen3-32b mixed step, one layer: 4 x 512 prefill + 128 decodes")
