@@ -16,6 +16,7 @@
 //   epilogues: fp32 store, residual add, SwiGLU.
 // * gemm_tiled_f32: plain fp32 SIMT tiles for the fp32 mode (row-major).
 #include <algorithm>
+#include <type_traits>
 
 #include "common.hpp"
 #include "kernels.hpp"
@@ -200,29 +201,31 @@ __global__ __launch_bounds__(SK_WAVES * 64) void gemm_skinny_bf16(const bf16_t* 
 // ---------------------------------------------------------------------------
 // Block tile: BMT m-tiles (16 rows each) x BNG weight groups (64 columns
 // each); waves WM x WN, each owning (BMT/WM) m-tiles x (BNG/WN) groups. One
-// stage = 64 of K = 2 k-tiles: BMT*2 A fragments and BNG*8 W fragments. The
-// packed layouts make every fragment 1 KB contiguous in HBM, so each wave
-// copies its share straight into LDS with global_load_lds_dwordx4 (lane l
-// lands at base + 16 l, which is the fragment's own lane order); two stages
-// alternate in LDS.
+// stage = 64 of K = 2 k-tiles: BNG*8 W fragments, shared by the WM waves of a
+// column, and (BMT/WM)*2 A fragments per wave. The packed layouts make every
+// fragment 1 KB contiguous in HBM. The W fragments are copied straight into
+// LDS with global_load_lds_dwordx4 (lane l lands at base + 16 l, which is the
+// fragment's own lane order), two stages alternating. Each wave loads its A
+// fragments straight into registers, a stage ahead, one k-tile half at a
+// time: an A fragment feeds 4*(BNG/WN) MFMAs of one wave and at most WN waves
+// need it, so staging it in LDS would cost more LDS bandwidth (a write and WN
+// reads) than the global load (two L1/L2 hits) it saves.
 template <int BMT, int BNG, int WM, int WN, int EPI>
 // blockIdx.z selects a K range of k_len (K for an unsplit product) and, for
 // the fp32 store, an output plane out + blockIdx.z * out_plane floats.
-__global__ __launch_bounds__(WM * WN * 64) void gemm_tiled_bf16(const bf16_t* __restrict__ A,
+__global__ __launch_bounds__(WM * WN * 64, 512 / (WM * WN * 64)) void gemm_tiled_bf16(const bf16_t* __restrict__ A,
                                                                const bf16_t* __restrict__ W,
                                                                int M, int N, int K,
                                                                void* __restrict__ out, int ldo,
                                                                int k_len, size_t out_plane,
                                                                RopeRows rope) {
   constexpr int NW = WM * WN;
-  constexpr int AF = BMT * 2;
   constexpr int BF = BNG * 8;
-  constexpr int FR = AF + BF;
-  constexpr int PER_WAVE = FR / NW;
+  constexpr int PER_WAVE = BF / NW;
   constexpr int TM = BMT / WM;
   constexpr int TG = BNG / WN;
-  static_assert(FR % NW == 0 && BMT % WM == 0 && BNG % WN == 0, "tile split");
-  __shared__ u32x4_t lds[2][FR * 64];
+  static_assert(BF % NW == 0 && BMT % WM == 0 && BNG % WN == 0, "tile split");
+  __shared__ u32x4_t lds[2][BF * 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WN, wn = wave % WN;
   // Blocks are dealt round-robin to the 8 XCDs (block b -> XCD b % 8), each
@@ -245,66 +248,96 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_tiled_bf16(const bf16_t* __
     }
   }
   const int mt0 = mb * BMT, g0 = nb * BNG, KT = K / 32;
+  const int KTILES = k_len / 64;
+  const size_t k0 = (size_t)blockIdx.z * KTILES;  // first stage of this K range
 
-  // this wave's fragments of a stage: source (at stage 0) and LDS slot
+  // this wave's W fragments of a stage: source at stage k0, LDS slot
   const bf16_t* src[PER_WAVE];
-  size_t stride[PER_WAVE];
 #pragma unroll
   for (int p = 0; p < PER_WAVE; ++p) {
-    const int f = wave * PER_WAVE + p;
-    if (f < AF) {
-      src[p] = A + ((size_t)(mt0 + f / 2) * KT + f % 2) * 512 + lane * 8;
-      stride[p] = 2 * 512;
-    } else {
-      const int fb = f - AF;
-      src[p] = W + (((size_t)(g0 + fb / 8) * KT + (fb / 4) % 2) * 4 + fb % 4) * 512 + lane * 8;
-      stride[p] = 2 * 4 * 512;
-    }
+    const int fb = wave * PER_WAVE + p;
+    src[p] = W + ((((size_t)(g0 + fb / 8) * KT + (fb / 4) % 2) * 4 + fb % 4) + k0 * 8) * 512 + lane * 8;
   }
   auto issue = [&](int kt, int buf) {
 #pragma unroll
     for (int p = 0; p < PER_WAVE; ++p)
-      __builtin_amdgcn_global_load_lds((const void*)(src[p] + (size_t)kt * stride[p]),
+      __builtin_amdgcn_global_load_lds((const void*)(src[p] + (size_t)kt * 8 * 512),
                                        (lds_ptr_t)&lds[buf][(wave * PER_WAVE + p) * 64], 16, 0, 0);
   };
+  // A fragment (m-tile mt0 + wm*TM + i, k-tile 2*(k0 + kt) + h)
+  const bf16_t* asrc = A + ((size_t)(mt0 + wm * TM) * KT + 2 * k0) * 512 + lane * 8;
+  // The A loads are written as inline asm: the compiler counts direct-to-LDS
+  // copies and register loads as completing out of order and would wait for
+  // all of them before the first use of an A register. The waits below are
+  // explicit instead; each takes the A registers as in/out operands, which
+  // keeps their MFMAs after it. Counts: a stage issues PER_WAVE copies and
+  // 2*TM A loads, and loads complete in issue order.
+  auto aload = [&](u32x4_t (&a)[TM], int kt, int h) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+      asm volatile("global_load_dwordx4 %0, %1, off"
+                   : "=v"(a[i])
+                   : "v"(asrc + ((size_t)i * KT + 2 * kt + h) * 512)
+                   : "memory");
+  };
+  auto await_a = [&](u32x4_t (&a)[TM], auto n) {
+    asm volatile("s_waitcnt vmcnt(%1)" : "+v"(a[0]) : "n"(decltype(n)::value) : "memory");
+#pragma unroll
+    for (int i = 1; i < TM; ++i) asm volatile("" : "+v"(a[i]));
+  };
+  using in_flight = std::integral_constant<int, TM + PER_WAVE>;
 
   f32x4_t acc[TM][TG * 4];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TG * 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  const int KTILES = k_len / 64;
-  if (blockIdx.z != 0) {
+  auto half = [&](int buf, int h, const u32x4_t (&a)[TM]) {
+    u32x4_t fb[TG * 4];
 #pragma unroll
-    for (int p = 0; p < PER_WAVE; ++p) src[p] += (size_t)blockIdx.z * KTILES * stride[p];
-    if (EPI == EPI_STORE_F32) out = (float*)out + blockIdx.z * out_plane;
-  }
+    for (int gi = 0; gi < TG; ++gi)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        fb[gi * 4 + j] = lds[buf][(((wn * TG + gi) * 2 + h) * 4 + j) * 64 + lane];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TG * 4; ++j) acc[i][j] = mfma16x16x32(a[i], fb[j], acc[i][j]);
+  };
+
+  u32x4_t a0[TM], a1[TM];  // A of the current stage, k-tile halves 0 and 1
   issue(0, 0);
-  __builtin_amdgcn_s_waitcnt(0);
+  aload(a0, 0, 0);
+  aload(a1, 0, 1);
+  await_a(a0, std::integral_constant<int, 0>{});
+  await_a(a1, std::integral_constant<int, 0>{});
   __syncthreads();
-  for (int kt = 0; kt < KTILES; ++kt) {
+  int kt = 0;
+  for (; kt + 1 < KTILES; ++kt) {
     const int buf = kt & 1;
     // the other buffer was last read in the previous stage, before its barrier
-    if (kt + 1 < KTILES) issue(kt + 1, buf ^ 1);
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      u32x4_t fb[TG * 4];
-#pragma unroll
-      for (int gi = 0; gi < TG; ++gi)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          fb[gi * 4 + j] = lds[buf][(AF + ((wn * TG + gi) * 2 + h) * 4 + j) * 64 + lane];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const u32x4_t fa = lds[buf][((wm * TM + i) * 2 + h) * 64 + lane];
-#pragma unroll
-        for (int j = 0; j < TG * 4; ++j) acc[i][j] = mfma16x16x32(fa, fb[j], acc[i][j]);
-      }
-    }
-    __builtin_amdgcn_s_waitcnt(0);  // next stage landed in LDS
-    __syncthreads();
+    issue(kt + 1, buf ^ 1);
+    await_a(a0, in_flight{});  // later: a1's loads, this stage's copies
+    half(buf, 0, a0);
+    aload(a0, kt + 1, 0);
+    await_a(a1, in_flight{});  // later: the copies, the new a0 loads
+    half(buf, 1, a1);
+    aload(a1, kt + 1, 1);
+    // the next stage's copies have landed (only the 2*TM A loads issued
+    // after them may be in flight); then no wave reads this buffer again
+    // (A bare barrier: __syncthreads() would also wait for those A loads.
+    // LDS accesses cannot move across it, since the inline asm next to it
+    // clobbers memory.)
+    __builtin_amdgcn_s_waitcnt(vmcnt_at_most(2 * TM));
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
   }
+  await_a(a0, std::integral_constant<int, TM>{});
+  half(kt & 1, 0, a0);
+  await_a(a1, std::integral_constant<int, 0>{});
+  half(kt & 1, 1, a1);
+
+  if (EPI == EPI_STORE_F32 && blockIdx.z != 0) out = (float*)out + blockIdx.z * out_plane;
 
   // Epilogue: lane l holds column (g*64 + j*16 + l%16), rows (l/16)*4 + r of
   // m-tile (mt0 + wm*TM + i).
