@@ -2,6 +2,8 @@
 // the stage-input conversion, or with the residual add of split-K partial
 // sums), per-head q/k RMSNorm + RoPE + paged KV write, SwiGLU, and the
 // stage-output cast.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "packed.hpp"
@@ -228,14 +230,21 @@ __device__ __forceinline__ const int32_t* seq_table(const SegTables& t, int seq)
                        : t.bt1 + (size_t)(seq - t.nseq0) * t.stride1;
 }
 
-// One wave per (token, head); heads [0, n_q) are query heads, [n_q, n_q+n_kv)
-// key/value heads. Lane j < d/2 owns the rotate-half pair (j, j + d/2). The
-// projection of a column is the sum of its source's partial planes. A 1-D
-// grid of (token, group of 4 heads) pairs, token fastest within a group:
-// first the rows t >= r0 (whose source may have several planes, so they
-// are dispatched first), then the rows before r0, whose groups start at
-// g_lo (past the query heads when their queries are already rotated).
-template <typename T>
+// One wave per (TPW consecutive tokens, head); heads [0, n_q)
+// are query heads, [n_q, n_q+n_kv) key/value heads. Lane j < d/2 owns the
+// rotate-half pair (j, j + d/2). The projection of a column is the sum of
+// its source's partial planes. A 1-D grid of (token group, group of 4
+// heads) pairs, token group fastest within a head group: first the rows
+// t >= r0 (whose source may have several planes, so they are dispatched
+// first), then the rows before r0, whose head groups start at g_lo (past
+// the query heads when their queries are already rotated). A wave's loads
+// for its tokens are independent, so their latency chains (position ->
+// rotary table, sequence -> block table) overlap instead of each running in
+// a short wave of its own. Steps of a few hundred rows keep one token per
+// wave: they need the waves to fill the chip (a decode step of 64 rows has
+// 1152), and their sources have several partial planes each.
+
+template <typename T, int TPW>
 __global__ __launch_bounds__(256) void rope_kv_kernel(ProjSrc qs, ProjSrc kvs, ProjSrc qt,
                                                       ProjSrc kvt, int r0, int g_lo, int n_tok,
                                                       T* __restrict__ q_out,
@@ -249,72 +258,95 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(ProjSrc qs, ProjSrc kvs, P
                                                       int n_q) {
   const int G = (n_q + n_kv + 3) >> 2;  // head groups
   const int nt = n_tok - r0;            // rows from r0 on
+  const int ntg = (nt + TPW - 1) / TPW, r0g = (r0 + TPW - 1) / TPW;
   const int wg = blockIdx.x;
-  int t, grp;
-  if (wg < nt * G) {
-    grp = wg / nt;
-    t = r0 + wg % nt;
+  int t0, t_end, grp;
+  if (wg < ntg * G) {
+    grp = wg / ntg;
+    t0 = r0 + (wg % ntg) * TPW;
+    t_end = n_tok;
   } else {
-    grp = g_lo + (wg - nt * G) / r0;
-    t = (wg - nt * G) % r0;
+    const int w = wg - ntg * G;
+    grp = g_lo + w / r0g;
+    t0 = (w % r0g) * TPW;
+    t_end = r0;
   }
   const int hh = grp * 4 + (threadIdx.x >> 6);
   if (hh >= n_q + n_kv) return;
   const int lane = threadIdx.x & 63;
   const int half = d >> 1;
   const bool act = lane < half;
-  const int pos = tok_pos[t];
   const bool is_q = hh < n_q;
   const int kh = hh - n_q;
-  const bool tail = t >= r0;
+  const bool tail = t0 >= r0;  // a wave's tokens all lie on one side of r0
   const ProjSrc src = tail ? (is_q ? qt : kvt) : (is_q ? qs : kvs);
-  const float* row = src.base + (size_t)(tail ? t - r0 : t) * src.ld;
   const int col = is_q ? hh * d : kh * d;
+  const int vcol = (n_kv + kh) * d;
   const T* gain = is_q ? q_gain : k_gain;
 
-  float a = 0.f, b = 0.f;
+  // Loads for all tokens first (independent, so their latencies overlap);
+  // tokens past t_end repeat the last one and are not stored.
+  int tt[TPW], pos[TPW];
+  const float* row[TPW];
+#pragma unroll
+  for (int u = 0; u < TPW; ++u) {
+    tt[u] = min(t0 + u, t_end - 1);
+    pos[u] = tok_pos[tt[u]];
+    row[u] = src.base + (size_t)(tail ? tt[u] - r0 : tt[u]) * src.ld;
+  }
+  float a[TPW], b[TPW], va[TPW], vb[TPW];
+#pragma unroll
+  for (int u = 0; u < TPW; ++u) a[u] = b[u] = va[u] = vb[u] = 0.f;
   if (act) {
-#pragma unroll 4
     for (int sp = 0; sp < src.splits; ++sp) {
-      a += row[sp * src.plane + col + lane];
-      b += row[sp * src.plane + col + lane + half];
+      const size_t o = (size_t)sp * src.plane;
+#pragma unroll
+      for (int u = 0; u < TPW; ++u) {
+        a[u] += row[u][o + col + lane];
+        b[u] += row[u][o + col + lane + half];
+        if (!is_q) {
+          va[u] += row[u][o + vcol + lane];
+          vb[u] += row[u][o + vcol + lane + half];
+        }
+      }
     }
   }
   if (gain != nullptr) {
-    const float ss = wave_sum(a * a + b * b);
-    const float r = 1.0f / sqrtf(ss / (float)d + qk_eps);
-    if (act) {
-      a = a * r * elem<T>::load(gain, lane);
-      b = b * r * elem<T>::load(gain, lane + half);
+    const float ga = act ? elem<T>::load(gain, lane) : 0.f;
+    const float gb = act ? elem<T>::load(gain, lane + half) : 0.f;
+#pragma unroll
+    for (int u = 0; u < TPW; ++u) {
+      const float ss = wave_sum(a[u] * a[u] + b[u] * b[u]);
+      const float r = 1.0f / sqrtf(ss / (float)d + qk_eps);
+      a[u] = a[u] * r * ga;
+      b[u] = b[u] * r * gb;
     }
   }
   if (!act) return;
-  const float c = cos_tab[(size_t)pos * half + lane];
-  const float s = sin_tab[(size_t)pos * half + lane];
-  const float ra = a * c - b * s;
-  const float rb = a * s + b * c;
-  if (is_q) {
-    T* qo = q_out + ((size_t)t * n_q + hh) * d;
-    elem<T>::store(qo, lane, ra);
-    elem<T>::store(qo, lane + half, rb);
-    return;
+#pragma unroll
+  for (int u = 0; u < TPW; ++u) {
+    if (t0 + u >= t_end) break;
+    const int t = tt[u];
+    const float c = cos_tab[(size_t)pos[u] * half + lane];
+    const float s = sin_tab[(size_t)pos[u] * half + lane];
+    const float ra = a[u] * c - b[u] * s;
+    const float rb = a[u] * s + b[u] * c;
+    if (is_q) {
+      T* qo = q_out + ((size_t)t * n_q + hh) * d;
+      elem<T>::store(qo, lane, ra);
+      elem<T>::store(qo, lane + half, rb);
+      continue;
+    }
+    const int32_t* bt = seq_table(tabs, tok_seq[t]);
+    const int64_t blk = bt[pos[u] / kBlock];
+    const int off = pos[u] % kBlock;
+    T* kplane = kv + ((blk * n_kv + kh) * 2 + 0) * (int64_t)kBlock * d;
+    T* vplane = kplane + (int64_t)kBlock * d;
+    elem<T>::store(kplane, kv_k_offset(off, lane), ra);
+    elem<T>::store(kplane, kv_k_offset(off, lane + half), rb);
+    elem<T>::store(vplane, kv_v_offset(off, lane), va[u]);
+    elem<T>::store(vplane, kv_v_offset(off, lane + half), vb[u]);
   }
-  const int32_t* bt = seq_table(tabs, tok_seq[t]);
-  const int64_t blk = bt[pos / kBlock];
-  const int off = pos % kBlock;
-  T* kplane = kv + ((blk * n_kv + kh) * 2 + 0) * (int64_t)kBlock * d;
-  T* vplane = kplane + (int64_t)kBlock * d;
-  elem<T>::store(kplane, kv_k_offset(off, lane), ra);
-  elem<T>::store(kplane, kv_k_offset(off, lane + half), rb);
-  const int vcol = (n_kv + kh) * d;
-  float va = 0.f, vb = 0.f;
-#pragma unroll 4
-  for (int sp = 0; sp < src.splits; ++sp) {
-    va += row[sp * src.plane + vcol + lane];
-    vb += row[sp * src.plane + vcol + lane + half];
-  }
-  elem<T>::store(vplane, kv_v_offset(off, lane), va);
-  elem<T>::store(vplane, kv_v_offset(off, lane + half), vb);
 }
 
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + expf(-z)); }
@@ -438,17 +470,21 @@ hipError_t rope_kv_write(DType dt, ProjSrc qs, ProjSrc kvs, ProjSrc qt, ProjSrc 
     return hipErrorInvalidValue;
   if (q_done && n_q % 4 != 0) return hipErrorInvalidValue;
   const int G = (n_q + kv.n_kv + 3) / 4, g_lo = q_done ? n_q / 4 : 0;
-  dim3 grid((T - r0) * G + r0 * (G - g_lo));
-  if (dt == DT_BF16)
-    rope_kv_kernel<bf16_t><<<grid, 256, 0, s>>>(qs, kvs, qt, kvt, r0, g_lo, T, (bf16_t*)q_out, (bf16_t*)kv.base,
-                                                kv.n_kv, kv.head_dim, tok_seq, tok_pos, tabs,
-                                                cos_tab, sin_tab, (const bf16_t*)q_gain,
-                                                (const bf16_t*)k_gain, qk_eps, n_q);
-  else
-    rope_kv_kernel<float><<<grid, 256, 0, s>>>(qs, kvs, qt, kvt, r0, g_lo, T, (float*)q_out, (float*)kv.base,
-                                               kv.n_kv, kv.head_dim, tok_seq, tok_pos, tabs,
-                                               cos_tab, sin_tab, (const float*)q_gain,
-                                               (const float*)k_gain, qk_eps, n_q);
+  const int tpw = T >= 512 ? 4 : 1;
+  dim3 grid((T - r0 + tpw - 1) / tpw * G + (r0 + tpw - 1) / tpw * (G - g_lo));
+  auto go = [&](auto elem_tag, auto tpw_c) {
+    using E = decltype(elem_tag);
+    rope_kv_kernel<E, decltype(tpw_c)::value><<<grid, 256, 0, s>>>(
+        qs, kvs, qt, kvt, r0, g_lo, T, (E*)q_out, (E*)kv.base, kv.n_kv, kv.head_dim, tok_seq,
+        tok_pos, tabs, cos_tab, sin_tab, (const E*)q_gain, (const E*)k_gain, qk_eps, n_q);
+  };
+  using One = std::integral_constant<int, 1>;
+  using Four = std::integral_constant<int, 4>;
+  if (dt == DT_BF16) {
+    if (tpw == 4) go(bf16_t{}, Four{}); else go(bf16_t{}, One{});
+  } else {
+    if (tpw == 4) go(float{}, Four{}); else go(float{}, One{});
+  }
   return hipGetLastError();
 }
 
