@@ -11,9 +11,10 @@
 //   partial tile per K split; the consumer kernel sums the splits. With one
 //   split the gate-up GEMM applies SwiGLU in its epilogue.
 // * gemm_tiled_bf16: many rows (prefill, mixed steps), compute-bound.
-//   256 x 256 (8 waves of 64 x 128) or 128 x 128 block tiles; whole fragments
-//   copied HBM -> LDS with direct loads, 64-wide k steps double-buffered;
-//   epilogues: fp32 store, residual add, SwiGLU.
+//   256 x 256 (8 waves of 64 x 128), 192 x 256 or 128 x 128 block tiles;
+//   weight fragments copied HBM -> LDS with direct loads (64-wide k steps,
+//   double-buffered), A fragments loaded straight into registers a stage
+//   ahead; epilogues: fp32 store, residual add, SwiGLU, query RoPE.
 // * gemm_tiled_f32: plain fp32 SIMT tiles for the fp32 mode (row-major).
 #include <algorithm>
 #include <type_traits>
