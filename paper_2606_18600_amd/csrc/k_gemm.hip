@@ -211,7 +211,11 @@ __global__ __launch_bounds__(SK_WAVES * 64) void gemm_skinny_bf16(const bf16_t* 
 // time: an A fragment feeds 4*(BNG/WN) MFMAs of one wave and at most WN waves
 // need it, so staging it in LDS would cost more LDS bandwidth (a write and WN
 // reads) than the global load (two L1/L2 hits) it saves.
-template <int BMT, int BNG, int WM, int WN, int EPI>
+template <int BMT, int BNG, int WM, int WN, int EPI, bool DEEP>
+// DEEP (K ranges of an even number of stages): A is loaded two stages ahead
+// into four half-stage register sets in rotation, with loads and copies past
+// the end clamped to the last stage, so the stage loop (unrolled by two) has
+// no branch and the same wait counts everywhere. Otherwise one stage ahead.
 // blockIdx.z selects a K range of k_len (K for an unsplit product) and, for
 // the fp32 store, an output plane out + blockIdx.z * out_plane floats.
 __global__ __launch_bounds__(WM * WN * 64, 512 / (WM * WN * 64)) void gemm_tiled_bf16(const bf16_t* __restrict__ A,
@@ -306,37 +310,103 @@ __global__ __launch_bounds__(WM * WN * 64, 512 / (WM * WN * 64)) void gemm_tiled
       for (int j = 0; j < TG * 4; ++j) acc[i][j] = mfma16x16x32(a[i], fb[j], acc[i][j]);
   };
 
-  u32x4_t a0[TM], a1[TM];  // A of the current stage, k-tile halves 0 and 1
-  issue(0, 0);
-  aload(a0, 0, 0);
-  aload(a1, 0, 1);
-  await_a(a0, std::integral_constant<int, 0>{});
-  await_a(a1, std::integral_constant<int, 0>{});
-  __syncthreads();
-  int kt = 0;
-  for (; kt + 1 < KTILES; ++kt) {
-    const int buf = kt & 1;
-    // the other buffer was last read in the previous stage, before its barrier
-    issue(kt + 1, buf ^ 1);
-    await_a(a0, in_flight{});  // later: a1's loads, this stage's copies
-    half(buf, 0, a0);
-    aload(a0, kt + 1, 0);
-    await_a(a1, in_flight{});  // later: the copies, the new a0 loads
-    half(buf, 1, a1);
-    aload(a1, kt + 1, 1);
-    // the next stage's copies have landed (only the 2*TM A loads issued
-    // after them may be in flight); then no wave reads this buffer again
-    // (A bare barrier: __syncthreads() would also wait for those A loads.
-    // LDS accesses cannot move across it, since the inline asm next to it
-    // clobbers memory.)
-    __builtin_amdgcn_s_waitcnt(vmcnt_at_most(2 * TM));
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
+  if constexpr (DEEP) {
+    // Four sets: stage kt uses (sa, sb) = A(kt, h0), A(kt, h1) and reloads
+    // them with stage kt + 2. Counts per stage: PER_WAVE copies, 2*TM loads.
+    constexpr int AHEAD = 3 * TM + 2 * PER_WAVE;  // issued after A(kt, h)
+    const int QMAX = 2 * KTILES - 1;
+    auto aload_q = [&](u32x4_t (&a)[TM], int q) {  // half-stage q = 2 kt + h
+      q = q < QMAX ? q : QMAX;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        asm volatile("global_load_dwordx4 %0, %1, off"
+                     : "=v"(a[i])
+                     : "v"(asrc + ((size_t)i * KT + q) * 512)
+                     : "memory");
+    };
+    auto issue_c = [&](int kt, int buf) { issue(kt < KTILES ? kt : KTILES - 1, buf); };
+    // weight fragments read per 64-column group: fewer live registers
+    auto half_b = [&](int buf, int h, const u32x4_t (&a)[TM]) {
+#pragma unroll
+      for (int gi = 0; gi < TG; ++gi) {
+        u32x4_t fb[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          fb[j] = lds[buf][(((wn * TG + gi) * 2 + h) * 4 + j) * 64 + lane];
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[i][gi * 4 + j] = mfma16x16x32(a[i], fb[j], acc[i][gi * 4 + j]);
+      }
+    };
+    auto stage = [&](int kt, u32x4_t (&sa)[TM], u32x4_t (&sb)[TM]) {
+      const int buf = kt & 1;
+      issue_c(kt + 1, buf ^ 1);
+      await_a(sa, std::integral_constant<int, AHEAD>{});
+      half_b(buf, 0, sa);
+      aload_q(sa, 2 * kt + 4);
+      await_a(sb, std::integral_constant<int, AHEAD>{});
+      half_b(buf, 1, sb);
+      aload_q(sb, 2 * kt + 5);
+      // copies of stage kt + 1 landed (the 2*TM A loads after them may not)
+      __builtin_amdgcn_s_waitcnt(vmcnt_at_most(2 * TM));
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+    };
+    u32x4_t s0[TM], s1[TM], s2[TM], s3[TM];
+    issue(0, 0);
+    aload_q(s0, 0);
+    aload_q(s1, 1);
+    aload_q(s2, 2);
+    aload_q(s3, 3);
+    await_a(s0, std::integral_constant<int, 0>{});
+    await_a(s1, std::integral_constant<int, 0>{});
+    await_a(s2, std::integral_constant<int, 0>{});
+    await_a(s3, std::integral_constant<int, 0>{});
+    __syncthreads();
+    for (int kt = 0; kt < KTILES; kt += 2) {
+      stage(kt, s0, s1);
+      stage(kt + 1, s2, s3);
+    }
+    // loads past the end still land in the sets: wait before any reuse
+    await_a(s0, std::integral_constant<int, 0>{});
+    await_a(s1, std::integral_constant<int, 0>{});
+    await_a(s2, std::integral_constant<int, 0>{});
+    await_a(s3, std::integral_constant<int, 0>{});
+  } else {
+    u32x4_t a0[TM], a1[TM];  // A of the current stage, k-tile halves 0 and 1
+    issue(0, 0);
+    aload(a0, 0, 0);
+    aload(a1, 0, 1);
+    await_a(a0, std::integral_constant<int, 0>{});
+    await_a(a1, std::integral_constant<int, 0>{});
+    __syncthreads();
+    int kt = 0;
+    for (; kt + 1 < KTILES; ++kt) {
+      const int buf = kt & 1;
+      // the other buffer was last read in the previous stage, before its barrier
+      issue(kt + 1, buf ^ 1);
+      await_a(a0, in_flight{});  // later: a1's loads, this stage's copies
+      half(buf, 0, a0);
+      aload(a0, kt + 1, 0);
+      await_a(a1, in_flight{});  // later: the copies, the new a0 loads
+      half(buf, 1, a1);
+      aload(a1, kt + 1, 1);
+      // the next stage's copies have landed (only the 2*TM A loads issued
+      // after them may be in flight); then no wave reads this buffer again
+      // (A bare barrier: __syncthreads() would also wait for those A loads.
+      // LDS accesses cannot move across it, since the inline asm next to it
+      // clobbers memory.)
+      __builtin_amdgcn_s_waitcnt(vmcnt_at_most(2 * TM));
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+    }
+    await_a(a0, std::integral_constant<int, TM>{});
+    half(kt & 1, 0, a0);
+    await_a(a1, std::integral_constant<int, 0>{});
+    half(kt & 1, 1, a1);
   }
-  await_a(a0, std::integral_constant<int, TM>{});
-  half(kt & 1, 0, a0);
-  await_a(a1, std::integral_constant<int, 0>{});
-  half(kt & 1, 1, a1);
 
   if (EPI == EPI_STORE_F32 && blockIdx.z != 0) out = (float*)out + blockIdx.z * out_plane;
 
@@ -512,12 +582,25 @@ hipError_t gemm_skinny(const void* A, const void* W, int M, int N, int K, int sp
   }
 }
 
+// Launch a tiled instantiation, taking the two-stages-ahead A path when the
+// K range has an even number of 64-wide stages.
+template <int BMT, int BNG, int WM, int WN, int EPI>
+void launch_tiled(dim3 grid, hipStream_t s, const bf16_t* A, const bf16_t* W, int M, int N, int K,
+                  void* out, int ldo, int k_len, size_t out_plane, RopeRows rope) {
+  if ((k_len / 64) % 2 == 0)
+    gemm_tiled_bf16<BMT, BNG, WM, WN, EPI, true><<<grid, WM * WN * 64, 0, s>>>(
+        A, W, M, N, K, out, ldo, k_len, out_plane, rope);
+  else
+    gemm_tiled_bf16<BMT, BNG, WM, WN, EPI, false><<<grid, WM * WN * 64, 0, s>>>(
+        A, W, M, N, K, out, ldo, k_len, out_plane, rope);
+}
+
 hipError_t gemm_split_k(const void* A, const void* W, int M, int N, int K, int splits, float* out,
                         hipStream_t s) {
   if (M == 0) return hipSuccess;
   if (splits < 1 || N % 256 != 0 || K % (64 * splits) != 0) return hipErrorInvalidValue;
   dim3 grid((M + 255) / 256, N / 256, splits);
-  gemm_tiled_bf16<16, 4, 4, 2, EPI_STORE_F32><<<grid, 512, 0, s>>>(
+  launch_tiled<16, 4, 4, 2, EPI_STORE_F32>(grid, s, 
       (const bf16_t*)A, (const bf16_t*)W, M, N, K, out, N, K / splits, (size_t)M * N, RopeRows{});
   return hipGetLastError();
 }
@@ -531,7 +614,7 @@ hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int
         !rope.sin_tab)
       return hipErrorInvalidValue;
     dim3 grid((M + 255) / 256, N / 256);
-    gemm_tiled_bf16<16, 4, 4, 2, EPI_ROPE_Q><<<grid, 512, 0, s>>>(
+    launch_tiled<16, 4, 4, 2, EPI_ROPE_Q>(grid, s, 
         (const bf16_t*)A, (const bf16_t*)W, M, N, K, out, N, K, 0, rope);
     return hipGetLastError();
   }
@@ -571,25 +654,25 @@ hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int
     if (t == T256) {
       dim3 grid((Ml + 255) / 256, Nl / 256);
       switch (epi) {
-        case EPI_STORE_F32: gemm_tiled_bf16<16, 4, 4, 2, EPI_STORE_F32><<<grid, 512, 0, s>>>(al, wl, Ml, Nl, K, ol, N, K, 0, RopeRows{}); break;
-        case EPI_RESID_ADD: gemm_tiled_bf16<16, 4, 4, 2, EPI_RESID_ADD><<<grid, 512, 0, s>>>(al, wl, Ml, Nl, K, ol, N, K, 0, RopeRows{}); break;
-        case EPI_SWIGLU: gemm_tiled_bf16<16, 4, 4, 2, EPI_SWIGLU><<<grid, 512, 0, s>>>(al, wl, Ml, Nl, K, ol, N, K, 0, RopeRows{}); break;
+        case EPI_STORE_F32: launch_tiled<16, 4, 4, 2, EPI_STORE_F32>(grid, s, al, wl, Ml, Nl, K, ol, N, K, 0, RopeRows{}); break;
+        case EPI_RESID_ADD: launch_tiled<16, 4, 4, 2, EPI_RESID_ADD>(grid, s, al, wl, Ml, Nl, K, ol, N, K, 0, RopeRows{}); break;
+        case EPI_SWIGLU: launch_tiled<16, 4, 4, 2, EPI_SWIGLU>(grid, s, al, wl, Ml, Nl, K, ol, N, K, 0, RopeRows{}); break;
         default: return hipErrorInvalidValue;
       }
     } else if (t == T192) {
       dim3 grid((Ml + 191) / 192, Nl / 256);
       switch (epi) {
-        case EPI_STORE_F32: gemm_tiled_bf16<12, 4, 4, 2, EPI_STORE_F32><<<grid, 512, 0, s>>>(al, wl, Ml, Nl, K, ol, N, K, 0, RopeRows{}); break;
-        case EPI_RESID_ADD: gemm_tiled_bf16<12, 4, 4, 2, EPI_RESID_ADD><<<grid, 512, 0, s>>>(al, wl, Ml, Nl, K, ol, N, K, 0, RopeRows{}); break;
-        case EPI_SWIGLU: gemm_tiled_bf16<12, 4, 4, 2, EPI_SWIGLU><<<grid, 512, 0, s>>>(al, wl, Ml, Nl, K, ol, N, K, 0, RopeRows{}); break;
+        case EPI_STORE_F32: launch_tiled<12, 4, 4, 2, EPI_STORE_F32>(grid, s, al, wl, Ml, Nl, K, ol, N, K, 0, RopeRows{}); break;
+        case EPI_RESID_ADD: launch_tiled<12, 4, 4, 2, EPI_RESID_ADD>(grid, s, al, wl, Ml, Nl, K, ol, N, K, 0, RopeRows{}); break;
+        case EPI_SWIGLU: launch_tiled<12, 4, 4, 2, EPI_SWIGLU>(grid, s, al, wl, Ml, Nl, K, ol, N, K, 0, RopeRows{}); break;
         default: return hipErrorInvalidValue;
       }
     } else {
       dim3 grid((Ml + 127) / 128, Nl / 128);
       switch (epi) {
-        case EPI_STORE_F32: gemm_tiled_bf16<8, 2, 2, 2, EPI_STORE_F32><<<grid, 256, 0, s>>>(al, wl, Ml, Nl, K, ol, N, K, 0, RopeRows{}); break;
-        case EPI_RESID_ADD: gemm_tiled_bf16<8, 2, 2, 2, EPI_RESID_ADD><<<grid, 256, 0, s>>>(al, wl, Ml, Nl, K, ol, N, K, 0, RopeRows{}); break;
-        case EPI_SWIGLU: gemm_tiled_bf16<8, 2, 2, 2, EPI_SWIGLU><<<grid, 256, 0, s>>>(al, wl, Ml, Nl, K, ol, N, K, 0, RopeRows{}); break;
+        case EPI_STORE_F32: launch_tiled<8, 2, 2, 2, EPI_STORE_F32>(grid, s, al, wl, Ml, Nl, K, ol, N, K, 0, RopeRows{}); break;
+        case EPI_RESID_ADD: launch_tiled<8, 2, 2, 2, EPI_RESID_ADD>(grid, s, al, wl, Ml, Nl, K, ol, N, K, 0, RopeRows{}); break;
+        case EPI_SWIGLU: launch_tiled<8, 2, 2, 2, EPI_SWIGLU>(grid, s, al, wl, Ml, Nl, K, ol, N, K, 0, RopeRows{}); break;
         default: return hipErrorInvalidValue;
       }
     }
