@@ -191,6 +191,29 @@ stage_status stage_decode(stage_t* st, const stage_batch* batch, const void* hid
 stage_status stage_step_mixed(stage_t* st, const stage_batch* prefill, const stage_batch* decode,
                               const void* hidden_in, void* hidden_out, void* stream);
 
+/* Decode over the library's static scratch array instead of the bound
+ * workspace: the same forward pass, kernels and results as stage_decode, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc). This call allocates
+ * nothing: no hipMalloc/hipFree, no events; stage_bind_workspace is not
+ * needed for it.
+ *  - The scratch is a file-scope device array of 128 MiB per GPU, held from
+ *    the library's loading until the process ends (each GPU has its own).
+ *    A stage whose stage_workspace_bytes() exceeds it gets
+ *    STAGE_ERR_CAPACITY before anything is enqueued (a Llama-3.1-70B-shaped
+ *    layer range with max_tokens = max_seqs = 128 and max_position = 8192
+ *    fits).
+ *  - Every call on a GPU, from any stage, shares that GPU's array, which
+ *    keeps the last call's contents. Nothing in it must start at zero; the
+ *    rotary table is copied in (from host memory, on `stream`) whenever the
+ *    previous call on that GPU came from another stage. Calls that overlap
+ *    on one GPU (concurrent streams or threads) race on the array and give
+ *    wrong results; serialise them.
+ *  - Validation and error codes are those of stage_decode; op timing is not
+ *    applied to its launches. */
+stage_status stage_decode_noalloc(stage_t* st, const stage_batch* batch, const void* hidden_in,
+                                  void* hidden_out, void* stream);
+
 /* Destroy a stage (does not free any borrowed memory). NULL is allowed. */
 stage_status stage_destroy(stage_t* st);
 

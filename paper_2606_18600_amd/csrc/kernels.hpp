@@ -166,4 +166,12 @@ hipError_t attn_f32(const float* q, KVLayer kv, SegTables tabs, const int32_t* t
 // Positions handled by one prefill work item for a GQA group size.
 int prefill_item_positions(DType dt, int group);
 
+// Bytes of the library's static device scratch array (one copy per GPU, held
+// until the process ends): the workspace of the decode entry point that
+// allocates nothing.
+constexpr size_t kStaticScratchBytes = (size_t)128 << 20;
+// Device address of that array on `device`, which must be the current
+// device. Looked up with hipGetSymbolAddress on the first call per device.
+hipError_t static_scratch(int device, void** ptr);
+
 }  // namespace stage_k

@@ -3,11 +3,13 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -20,6 +22,13 @@ using namespace stage_k;
 namespace {
 
 thread_local std::string g_err;
+std::atomic<uint64_t> g_stage_uid{0};
+
+// Per device: the stage whose call last used the static scratch array (its
+// uid; 0 = none). Only that stage's rotary table is known to be there.
+constexpr int kMaxStaticDevices = 64;
+std::mutex g_static_mu;
+uint64_t g_static_owner[kMaxStaticDevices] = {};
 
 stage_status fail(stage_status code, const char* fmt, ...) {
   char buf[512];
@@ -40,6 +49,16 @@ constexpr int kMaxMidSplits = 8;     // K splits of the products of a small tile
 constexpr int kMidRows = 2048;       // partial-plane rows of such a step (splits x T)
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Decode split items of a step, at most. The plan (build_meta) aims at
+// `attn_waves` waves: with u = sum over sequences of their key blocks, every
+// split covers at least ceil(n_kv u / attn_waves) blocks, so sequence j gets
+// ceil(nb_j / bps) < nb_j / bps + 1 splits and the step fewer than
+// attn_waves / n_kv + (sequences) in total.
+size_t max_decode_items(int max_seqs, int attn_waves, int n_kv) {
+  const size_t by_plan = (size_t)max_seqs + (size_t)((attn_waves + n_kv - 1) / n_kv);
+  return std::min((size_t)max_seqs * kMaxSplits, by_plan);
+}
 
 int env_int(const char* name, int dflt) {
   const char* v = getenv(name);
@@ -78,6 +97,12 @@ struct stage {
   bool row_tail_on = true;  // split-K skinny products for the last rows of large steps
   bool q_rope_fused = true;  // RoPE in the epilogue of a step's query product (when possible)
   bool check_tables = false;  // copy block tables to the host and check ids (STAGE_DEBUG)
+
+  uint64_t uid = 0;        // distinct for every stage created in the process
+  size_t max_ditems = 0;   // decode split items a step may need (bf16)
+  // rotary table (angle p * theta^(-2j/d) in double, rounded once to float),
+  // [max_position][head_dim / 2] cos then sin; uploaded into the workspace
+  std::vector<float> rope_host;
 
   // workspace
   Region r_x, r_h, r_qkv, r_kvpart, r_q, r_attn, r_m, r_gu, r_part_x, r_part_o, r_part_ml, r_meta,
@@ -214,7 +239,7 @@ void plan_workspace(stage* st) {
   take(st->r_part_x, std::max({(size_t)std::max(st->s_o, st->s_down) * R * H, mid_rows * H,
                                c.dtype == STAGE_BF16 && T > R ? (size_t)st->s_qkv * R * qkvw : 0}) *
                          4);
-  const size_t max_items = c.dtype == STAGE_BF16 ? (size_t)st->max_seqs * kMaxSplits : 0;
+  const size_t max_items = st->max_ditems;
   take(st->r_part_o, max_items * qw * 4);
   take(st->r_part_ml, max_items * c.n_q_heads * 2 * 4);
   // metadata: tok_seq, tok_pos [T]; decode items [max_items][4];
@@ -238,7 +263,7 @@ struct StepMeta {
 // Lay out the metadata arrays over a base pointer (host staging or device).
 StepMeta meta_view(const stage* st, int32_t* base) {
   const size_t T = st->max_tokens;
-  const size_t max_items = st->cfg.dtype == STAGE_BF16 ? (size_t)st->max_seqs * kMaxSplits : 0;
+  const size_t max_items = st->max_ditems;
   StepMeta m;
   m.tok_seq = base;
   m.tok_pos = base + T;
@@ -249,7 +274,10 @@ StepMeta meta_view(const stage* st, int32_t* base) {
   return m;
 }
 
-void build_meta(const stage* st, const stage_batch* pf, const stage_batch* dc, StepMeta& m) {
+// Fill the step metadata. Returns false (having written nothing past the
+// item capacity) if the decode split plan would exceed max_ditems, which the
+// bound of max_decode_items rules out.
+bool build_meta(const stage* st, const stage_batch* pf, const stage_batch* dc, StepMeta& m) {
   const int np = pf ? pf->num_seqs : 0, nd = dc ? dc->num_seqs : 0;
   int row = 0;
   const int ppw = prefill_item_positions((DType)st->cfg.dtype,
@@ -292,6 +320,7 @@ void build_meta(const stage* st, const stage_batch* pf, const stage_batch* dc, S
     int splits = std::min(kMaxSplits, std::max(1, (nb + bps_target - 1) / bps_target));
     const int bps = (nb + splits - 1) / splits;
     splits = (nb + bps - 1) / bps;
+    if ((size_t)(m.n_ditems + splits) > st->max_ditems) return false;
     for (int sp = 0; sp < splits; ++sp) {
       const int k0 = sp * bps * kBlock;
       const int k1 = std::min(keys, (sp + 1) * bps * kBlock);
@@ -299,6 +328,7 @@ void build_meta(const stage* st, const stage_batch* pf, const stage_batch* dc, S
     }
   }
   m.item_start[nd] = m.n_ditems;
+  return true;
 }
 
 hipEvent_t take_event(stage* st) {
@@ -475,7 +505,8 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
   int slot = 0;
   if ((vs = take_slot(st, &slot)) != STAGE_OK) return vs;
   StepMeta hm = meta_view(st, st->staging[slot]);
-  build_meta(st, pf, dc, hm);
+  if (!build_meta(st, pf, dc, hm))
+    return fail(STAGE_ERR_CAPACITY, "decode split plan exceeds %zu items", st->max_ditems);
   if ((vs = upload_slot(st, slot, st->meta_ints, s)) != STAGE_OK) return vs;
   StepMeta dm = meta_view(st, st->at<int32_t>(st->r_meta));
 
@@ -737,7 +768,29 @@ stage_status stage_create(const stage_model_config* cfg, int32_t layer_begin, in
     st->q_rope_fused = env_int("STAGE_Q_ROPE", 1) != 0;
     st->check_tables = env_int("STAGE_DEBUG", 0) != 0;
   }
+  st->max_ditems = cfg->dtype == STAGE_BF16
+                       ? max_decode_items(max_seqs, st->attn_waves, cfg->n_kv_heads)
+                       : 0;
+  st->uid = g_stage_uid.fetch_add(1) + 1;
   plan_workspace(st);
+  {
+    const int half = cfg->head_dim / 2;
+    const size_t n = (size_t)cfg->max_position * half;
+    try {
+      st->rope_host.resize(2 * n);
+    } catch (const std::bad_alloc&) {
+      delete st;
+      return fail(STAGE_ERR_OUT_OF_MEMORY, "host allocation of the rotary table failed");
+    }
+    for (int j = 0; j < half; ++j) {
+      const double w = std::pow(cfg->rope_theta, -2.0 * j / cfg->head_dim);
+      for (int p = 0; p < cfg->max_position; ++p) {
+        const double a = (double)p * w;
+        st->rope_host[(size_t)p * half + j] = (float)std::cos(a);
+        st->rope_host[n + (size_t)p * half + j] = (float)std::sin(a);
+      }
+    }
+  }
   for (int i = 0; i < kRing; ++i) {
     void* p = nullptr;
     if ((e = hipHostMalloc(&p, st->meta_ints * 4, hipHostMallocDefault)) != hipSuccess ||
@@ -762,22 +815,11 @@ stage_status stage_bind_workspace(stage_t* st, void* dev, size_t bytes) {
   hipError_t e = hipSetDevice(st->device);
   if (e != hipSuccess) return hip_fail("hipSetDevice", e);
   st->ws = (char*)dev;
-  // rotary table: angle p * theta^(-2j/d) in double, rounded once to float
-  const auto& c = st->cfg;
-  const int half = c.head_dim / 2;
-  std::vector<float> cs((size_t)c.max_position * half), sn((size_t)c.max_position * half);
-  for (int j = 0; j < half; ++j) {
-    const double w = std::pow(c.rope_theta, -2.0 * j / c.head_dim);
-    for (int p = 0; p < c.max_position; ++p) {
-      const double a = (double)p * w;
-      cs[(size_t)p * half + j] = (float)std::cos(a);
-      sn[(size_t)p * half + j] = (float)std::sin(a);
-    }
-  }
-  if ((e = hipMemcpy(st->ws + st->r_cos.off, cs.data(), cs.size() * 4, hipMemcpyHostToDevice)) !=
-          hipSuccess ||
-      (e = hipMemcpy(st->ws + st->r_sin.off, sn.data(), sn.size() * 4, hipMemcpyHostToDevice)) !=
-          hipSuccess) {
+  const size_t n = st->rope_host.size() / 2;
+  if ((e = hipMemcpy(st->ws + st->r_cos.off, st->rope_host.data(), n * 4,
+                     hipMemcpyHostToDevice)) != hipSuccess ||
+      (e = hipMemcpy(st->ws + st->r_sin.off, st->rope_host.data() + n, n * 4,
+                     hipMemcpyHostToDevice)) != hipSuccess) {
     st->ws = nullptr;
     return hip_fail("workspace init", e);
   }
@@ -802,6 +844,56 @@ stage_status stage_step_mixed(stage_t* st, const stage_batch* prefill, const sta
                               const void* hidden_in, void* hidden_out, void* stream) {
   if (!st) return fail(STAGE_ERR_INVALID_ARG, "stage is NULL");
   return run_step(st, prefill, decode, hidden_in, hidden_out, stream);
+}
+
+stage_status stage_decode_noalloc(stage_t* st, const stage_batch* batch, const void* hidden_in,
+                                  void* hidden_out, void* stream) {
+  if (!st) return fail(STAGE_ERR_INVALID_ARG, "stage is NULL");
+  if (!batch) return fail(STAGE_ERR_INVALID_ARG, "batch is NULL");
+  if (st->ws_bytes > kStaticScratchBytes)
+    return fail(STAGE_ERR_CAPACITY,
+                "the stage's workspace (%zu bytes) exceeds the static scratch array (%zu bytes): "
+                "create the stage with smaller max_tokens / max_seqs / max_position",
+                st->ws_bytes, kStaticScratchBytes);
+  if (st->device < 0 || st->device >= kMaxStaticDevices)
+    return fail(STAGE_ERR_UNSUPPORTED, "device %d has no static scratch slot", st->device);
+  // the checks run_step applies, before anything is enqueued here
+  long long T = 0;
+  stage_status vs = check_step(st->cfg, st->max_tokens, st->max_seqs, nullptr, batch, &T);
+  if (vs != STAGE_OK) return vs;
+  if (T == 0) return STAGE_OK;
+  if (!hidden_in || !hidden_out) return fail(STAGE_ERR_INVALID_ARG, "hidden_in/hidden_out is NULL");
+  hipError_t e = hipSetDevice(st->device);
+  if (e != hipSuccess) return hip_fail("hipSetDevice", e);
+  void* scr = nullptr;
+  if ((e = static_scratch(st->device, &scr)) != hipSuccess)
+    return hip_fail("static scratch address", e);
+  hipStream_t s = (hipStream_t)stream;
+  {
+    // the rotary table, unless this stage's last call left it there
+    std::lock_guard<std::mutex> lock(g_static_mu);
+    if (g_static_owner[st->device] != st->uid) {
+      g_static_owner[st->device] = 0;
+      const size_t n = st->rope_host.size() / 2;
+      char* base = (char*)scr;
+      if ((e = hipMemcpyAsync(base + st->r_cos.off, st->rope_host.data(), n * 4,
+                              hipMemcpyHostToDevice, s)) != hipSuccess ||
+          (e = hipMemcpyAsync(base + st->r_sin.off, st->rope_host.data() + n, n * 4,
+                              hipMemcpyHostToDevice, s)) != hipSuccess)
+        return hip_fail("rotary table upload", e);
+      g_static_owner[st->device] = st->uid;
+    }
+  }
+  // the forward pass of stage_decode over the static array; op timing (which
+  // may create events) is not applied to these launches
+  char* bound = st->ws;
+  const bool timing = st->timing;
+  st->ws = (char*)scr;
+  st->timing = false;
+  vs = run_step(st, nullptr, batch, hidden_in, hidden_out, stream);
+  st->ws = bound;
+  st->timing = timing;
+  return vs;
 }
 
 stage_status stage_pack_lm_head(const stage_model_config* cfg, int32_t vocab, const void* src,

@@ -150,6 +150,14 @@ class DeviceStage:
                        hidden_in.data_ptr(), out.data_ptr(), stream)
         return out
 
+    def decode_noalloc(self, ctx_lens, bt, hidden_in, hidden_out=None, stream=0):
+        """stage_decode_noalloc: the decode over the library's static scratch."""
+        out = self._out(hidden_in, hidden_out)
+        S.stage_decode_noalloc(self.handle,
+                               self.batch(np.ones(len(ctx_lens), np.int32), ctx_lens, bt),
+                               hidden_in.data_ptr(), out.data_ptr(), stream)
+        return out
+
     def mixed(self, p_q_lens, p_ctx_lens, p_bt, d_ctx_lens, d_bt, hidden_in, hidden_out=None,
               stream=0):
         out = self._out(hidden_in, hidden_out)

@@ -35,7 +35,8 @@ STAGE_OP_COUNT = len(OP_NAMES)
 EXPORTED = ("stage_create", "stage_workspace_bytes", "stage_bind_workspace", "stage_prefill",
             "stage_decode", "stage_step_mixed", "stage_destroy", "stage_last_error",
             "stage_validate_step", "stage_set_op_timing", "stage_read_op_times",
-            "stage_pack_weight", "stage_copy_probe", "stage_lm_head", "stage_pack_lm_head")
+            "stage_pack_weight", "stage_copy_probe", "stage_lm_head", "stage_pack_lm_head",
+            "stage_decode_noalloc")
 
 STAGE_W_QKV = 0
 STAGE_W_O = 1
@@ -93,6 +94,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.stage_bind_workspace.argtypes = [P, P, ctypes.c_size_t]
     lib.stage_prefill.argtypes = [P, ctypes.POINTER(stage_batch), P, P, P]
     lib.stage_decode.argtypes = [P, ctypes.POINTER(stage_batch), P, P, P]
+    lib.stage_decode_noalloc.argtypes = [P, ctypes.POINTER(stage_batch), P, P, P]
     lib.stage_step_mixed.argtypes = [P, ctypes.POINTER(stage_batch),
                                      ctypes.POINTER(stage_batch), P, P, P]
     lib.stage_destroy.argtypes = [P]
@@ -107,6 +109,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.stage_read_op_times.argtypes = [P, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_int64)]
     for name in ("stage_create", "stage_bind_workspace", "stage_prefill", "stage_decode",
+                 "stage_decode_noalloc",
                  "stage_step_mixed", "stage_destroy", "stage_validate_step",
                  "stage_set_op_timing", "stage_read_op_times", "stage_pack_weight",
                  "stage_copy_probe", "stage_lm_head", "stage_pack_lm_head"):
@@ -168,6 +171,11 @@ def stage_prefill(st: int, batch: stage_batch, hidden_in: int, hidden_out: int,
 def stage_decode(st: int, batch: stage_batch, hidden_in: int, hidden_out: int,
                  stream: int = 0) -> None:
     _check(load_library().stage_decode(st, _bp(batch), hidden_in, hidden_out, stream))
+
+
+def stage_decode_noalloc(st: int, batch: stage_batch, hidden_in: int, hidden_out: int,
+                         stream: int = 0) -> None:
+    _check(load_library().stage_decode_noalloc(st, _bp(batch), hidden_in, hidden_out, stream))
 
 
 def stage_step_mixed(st: int, prefill: Optional[stage_batch], decode: Optional[stage_batch],
