@@ -255,9 +255,10 @@ def test_qwen_small_long_context_decode(dtype):
 
 @pytest.mark.parametrize("lens", [[20, 9], [150, 61]], ids=["split-k", "tiled"])
 def test_hidden_out_may_alias_hidden_in(lens):
-    """Writing the output over the input gives the same result. The tiled
-    GEMMs are deterministic (bitwise equal); the split-K GEMMs sum partial
-    products with atomics, whose order varies from run to run."""
+    """Writing the output over the input gives the same result, bitwise: the
+    input is read (by the first RMSNorm) before anything is written to the
+    output, and every kernel is deterministic (the split-K GEMMs write
+    partial planes that the next kernel sums in a fixed order; no atomics)."""
     seed = 71
     shape = synth.TINY
     lens = np.array(lens, np.int32)
@@ -272,10 +273,7 @@ def test_hidden_out_may_alias_hidden_in(lens):
         out = pair.gpu.prefill(lens, [0, 0], torch.from_numpy(bt).cuda(), xin, hidden_out=xin)
         torch.cuda.synchronize()
         assert out.data_ptr() == xin.data_ptr()
-        if T > 128:
-            assert torch.equal(out, ref)
-        else:
-            assert rel_l2(out.double().cpu().numpy(), ref.double().cpu().numpy()) < 1e-2
+        assert torch.equal(out, ref)
     finally:
         pair.close()
 

@@ -1,0 +1,303 @@
+"""Parity of the HIP stage with strong random weights (GPU), where every
+branch of a layer moves the residual stream by O(1).
+
+With the workloads' N(0, 0.02^2) projections the attention and FFN branches
+are a few percent of a layer's output, so an output-level relative L2 of
+2e-2 would let a branch be wrong by a third. Here the projections are
+N(0, 1/fan-in) and the norm gains U[0.5, 1.5] (tests.helpers.strong_weights),
+and each call asserts, next to the output bar, the same bar on the branch
+y - x (output minus input) against the oracle's branch. Every KV entry the
+calls write is compared with the oracle's as well.
+
+The cases are the edge cases of the path: both GEMM paths and the boundary
+between them, 1-token prompts, prompts of 15/16/17 tokens, continuation
+chunks that start mid-block, a decode at position 0, decodes over contexts
+long enough for many key splits, the last rows of large steps on the split-K
+kernels, mixed steps, and every GQA group size the library accepts (1, 2, 4,
+8, 16) at head_dim 64 and 128, in bf16 and fp32.
+
+Tolerances (relative L2, outputs, branches and KV alike): 2e-2 in bf16,
+1e-4 in fp32.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from paper_2606_18600_amd import synth
+from tests.gpu_pair import Pair, log
+from tests.helpers import rel_l2, strong_weights
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+QWEN_SMALL = synth.ModelShape("qwen-small", hidden=512, n_q_heads=8, n_kv_heads=1, head_dim=128,
+                              ffn=768, rms_eps=1e-6, rope_theta=1e6, qk_norm=True,
+                              qk_rms_eps=1e-6)
+
+# GQA group sizes 1, 4 and 16 at both head dims (2 and 8 are the tiny and
+# the qwen-small shapes); q/k-norm on two of them.
+GROUP_SHAPES = [
+    synth.ModelShape("g1-d64", hidden=256, n_q_heads=4, n_kv_heads=4, head_dim=64, ffn=512,
+                     rms_eps=1e-5, rope_theta=5e5),
+    synth.ModelShape("g4-d64", hidden=256, n_q_heads=8, n_kv_heads=2, head_dim=64, ffn=512,
+                     rms_eps=1e-5, rope_theta=5e5),
+    synth.ModelShape("g16-d64", hidden=256, n_q_heads=16, n_kv_heads=1, head_dim=64, ffn=512,
+                     rms_eps=1e-5, rope_theta=5e5),
+    synth.ModelShape("g1-d128-qk", hidden=512, n_q_heads=4, n_kv_heads=4, head_dim=128, ffn=768,
+                     rms_eps=1e-6, rope_theta=1e6, qk_norm=True, qk_rms_eps=1e-6),
+    synth.ModelShape("g4-d128", hidden=512, n_q_heads=8, n_kv_heads=2, head_dim=128, ffn=768,
+                     rms_eps=1e-5, rope_theta=5e5),
+    synth.ModelShape("g16-d128-qk", hidden=512, n_q_heads=16, n_kv_heads=1, head_dim=128,
+                     ffn=768, rms_eps=1e-6, rope_theta=1e6, qk_norm=True, qk_rms_eps=1e-6),
+]
+
+
+def strong_pair(shape, dtype, n_layers, num_blocks, max_tokens, max_seqs, seed) -> Pair:
+    w = [strong_weights(shape, seed, l) for l in range(n_layers)]
+    return Pair(shape, dtype, n_layers, num_blocks, max_tokens, max_seqs, seed, host_weights=w)
+
+
+def check(tag, y, yr, x, dtype):
+    """Output and branch (y - x) against the oracle, both at the dtype's bar."""
+    tol = TOL[dtype]
+    e = rel_l2(y, yr)
+    eb = rel_l2(y - x, yr - x)
+    share = np.linalg.norm(yr - x) / max(np.linalg.norm(yr), 1e-30)
+    log(f"  {tag}: rel_l2={e:.3e} branch_rel_l2={eb:.3e} (branch/output norm {share:.2f})")
+    assert np.isfinite(y).all(), tag
+    assert e <= tol, f"{tag}: output rel_l2 {e:.3e} > {tol}"
+    assert eb <= tol, f"{tag}: branch rel_l2 {eb:.3e} > {tol}"
+    return max(e, eb)
+
+
+def check_kv(pair, dtype, tag=""):
+    kv = pair.kv_errors()
+    log(f"  {tag} kv rel_l2={kv:.3e} over {len(pair.written)} written slots")
+    assert kv <= TOL[dtype], f"{tag}: kv rel_l2 {kv:.3e}"
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_strong_tiny_prefill_then_decodes(dtype):
+    """The tiny flow (4 prompts of 16-64 tokens, then 16 decodes) with strong
+    weights; the branch is about as large as the output here."""
+    seed, shape = 2620, synth.TINY
+    log(f"[test] strong tiny flow dtype={dtype}")
+    lens = synth.uniform_lengths(seed, 0, 4, 16, 64)
+    bt = synth.make_block_tables(lens + 16, 8, synth.BlockAllocator(64, seed))
+    pair = strong_pair(shape, dtype, 2, 64, 256, 8, seed)
+    try:
+        y, yr, x = pair.prefill(lens, np.zeros(4, np.int32), bt,
+                                synth.hidden_states(seed, 1, int(lens.sum()), shape.hidden))
+        check("prefill", y, yr, x, dtype)
+        ctx = lens.copy()
+        for step in range(16):
+            y, yr, x = pair.decode(ctx, bt, synth.hidden_states(seed, 100 + step, 4, shape.hidden))
+            check(f"decode {step}", y, yr, x, dtype)
+            ctx += 1
+        check_kv(pair, dtype)
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("T", [1, 100, 128, 129, 300])
+def test_strong_prefill_token_counts(T):
+    """T <= 128 runs the split-K GEMMs, T > 128 the tiled ones; T = 1 is a
+    single one-token prompt."""
+    seed, shape, dtype = 2621 + T, synth.TINY, "bf16"
+    log(f"[test] strong prefill T={T}")
+    if T == 1:
+        lens = np.array([1], np.int32)
+    else:
+        r = np.random.default_rng(seed)
+        cuts = np.sort(r.choice(np.arange(1, T), size=2, replace=False))
+        lens = np.diff(np.concatenate([[0], cuts, [T]])).astype(np.int32)
+    bt = synth.make_block_tables(lens + 1, 32, synth.BlockAllocator(96, seed))
+    pair = strong_pair(shape, dtype, 2, 96, 512, 8, seed)
+    try:
+        y, yr, x = pair.prefill(lens, np.zeros(len(lens), np.int32), bt,
+                                synth.hidden_states(seed, 1, T, shape.hidden))
+        check("prefill", y, yr, x, dtype)
+        y, yr, x = pair.decode(lens, bt, synth.hidden_states(seed, 2, len(lens), shape.hidden))
+        check("decode", y, yr, x, dtype)
+        check_kv(pair, dtype)
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("shape", [synth.TINY, QWEN_SMALL], ids=["tiny", "qwen-small"])
+def test_strong_ragged_and_midblock(dtype, shape):
+    """Prompts of 1, 15, 16, 17, 33 tokens, continuation chunks that start
+    mid-block (3, 1, 16, 15, 2 tokens), then decodes."""
+    seed = 2630
+    log(f"[test] strong ragged {shape.name} dtype={dtype}")
+    lens = np.array([1, 15, 16, 17, 33], np.int32)
+    bt = synth.make_block_tables(lens + 20, 8, synth.BlockAllocator(64, seed))
+    pair = strong_pair(shape, dtype, 2, 64, 256, 8, seed)
+    try:
+        y, yr, x = pair.prefill(lens, np.zeros(5, np.int32), bt,
+                                synth.hidden_states(seed, 1, int(lens.sum()), shape.hidden))
+        check("prefill", y, yr, x, dtype)
+        q2 = np.array([3, 1, 16, 15, 2], np.int32)
+        y, yr, x = pair.prefill(q2, lens, bt, synth.hidden_states(seed, 2, int(q2.sum()),
+                                                                  shape.hidden))
+        check("chunk", y, yr, x, dtype)
+        ctx = lens + q2
+        for step in range(3):
+            y, yr, x = pair.decode(ctx, bt, synth.hidden_states(seed, 10 + step, 5, shape.hidden))
+            check(f"decode {step}", y, yr, x, dtype)
+            ctx += 1
+        check_kv(pair, dtype)
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("shape", [synth.TINY, QWEN_SMALL], ids=["tiny", "qwen-small"])
+def test_strong_decode_at_position_zero(dtype, shape):
+    """Decode tokens with no context attend only to themselves: the output
+    and the K/V they write are checked; a second decode then reads them."""
+    seed = 2640
+    log(f"[test] strong decode@0 {shape.name} dtype={dtype}")
+    bt = synth.make_block_tables([5, 5, 5], 2, synth.BlockAllocator(8, seed))
+    pair = strong_pair(shape, dtype, 2, 8, 16, 4, seed)
+    try:
+        y, yr, x = pair.decode(np.zeros(3, np.int32), bt,
+                               synth.hidden_states(seed, 1, 3, shape.hidden))
+        check("decode@0", y, yr, x, dtype)
+        check_kv(pair, dtype, "after decode@0")
+        y, yr, x = pair.decode(np.ones(3, np.int32), bt,
+                               synth.hidden_states(seed, 2, 3, shape.hidden))
+        check("decode@1", y, yr, x, dtype)
+        check_kv(pair, dtype, "after decode@1")
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("shape", [synth.TINY, QWEN_SMALL], ids=["tiny", "qwen-small"])
+def test_strong_mixed_step(dtype, shape):
+    seed = 2650
+    log(f"[test] strong mixed {shape.name} dtype={dtype}")
+    d_ctx0 = np.array([40, 3, 100, 17], np.int32)
+    p_total = np.array([70, 48], np.int32)
+    alloc = synth.BlockAllocator(128, seed)
+    dbt = synth.make_block_tables(d_ctx0 + 4, 16, alloc)
+    pbt = synth.make_block_tables(p_total, 16, alloc)
+    pair = strong_pair(shape, dtype, 2, 128, 256, 8, seed)
+    try:
+        y, yr, x = pair.prefill(d_ctx0, np.zeros(4, np.int32), dbt,
+                                synth.hidden_states(seed, 1, int(d_ctx0.sum()), shape.hidden))
+        check("context prefill", y, yr, x, dtype)
+        pq, pc = np.array([30, 48], np.int32), np.array([0, 0], np.int32)
+        y, yr, x = pair.mixed(pq, pc, pbt, d_ctx0, dbt,
+                              synth.hidden_states(seed, 2, int(pq.sum()) + 4, shape.hidden))
+        check("mixed 1", y, yr, x, dtype)
+        pq2, pc2 = np.array([40], np.int32), np.array([30], np.int32)
+        y, yr, x = pair.mixed(pq2, pc2, pbt[:1], d_ctx0 + 1, dbt,
+                              synth.hidden_states(seed, 3, 44, shape.hidden))
+        check("mixed 2", y, yr, x, dtype)
+        check_kv(pair, dtype)
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("shape", [synth.TINY, QWEN_SMALL], ids=["tiny", "qwen-small"])
+def test_strong_last_rows_on_split_k(shape):
+    """Steps of 256 k + r rows whose last r rows run on the split-K kernels
+    (r = 128 prefill-only, r = 40 decodes of a mixed step), and r = 129."""
+    seed, dtype = 2660, "bf16"
+    log(f"[test] strong row tail {shape.name}")
+    d_ctx0 = synth.uniform_lengths(seed, 1, 40, 5, 60).astype(np.int32)
+    totals = np.array([1100, 1160, 1580, 257], np.int32)
+    alloc = synth.BlockAllocator(512, seed)
+    dbt = synth.make_block_tables(d_ctx0 + 4, 8, alloc)
+    pbt = synth.make_block_tables(totals, 100, alloc)
+    pair = strong_pair(shape, dtype, 2, 512, 1536, 48, seed)
+    try:
+        y, yr, x = pair.prefill(d_ctx0, np.zeros(40, np.int32), dbt,
+                                synth.hidden_states(seed, 2, int(d_ctx0.sum()), shape.hidden))
+        check("context prefill", y, yr, x, dtype)
+        q1 = np.array([500, 480, 300, 128], np.int32)
+        y, yr, x = pair.prefill(q1, np.zeros(4, np.int32), pbt,
+                                synth.hidden_states(seed, 3, int(q1.sum()), shape.hidden))
+        check("prefill 1408", y, yr, x, dtype)
+        pq = np.array([600, 680], np.int32)
+        y, yr, x = pair.mixed(pq, q1[:2], pbt[:2].copy(), d_ctx0, dbt,
+                              synth.hidden_states(seed, 4, 1320, shape.hidden))
+        check("mixed 1320", y, yr, x, dtype)
+        q3 = np.array([1280, 129], np.int32)
+        y, yr, x = pair.prefill(q3, q1[2:], pbt[2:].copy(),
+                                synth.hidden_states(seed, 5, 1409, shape.hidden))
+        check("prefill 1409", y, yr, x, dtype)
+        check_kv(pair, dtype)
+    finally:
+        pair.close()
+
+
+def test_strong_long_context_decode_splits():
+    """Contexts of 2500, 700 and 129 tokens (many decode key splits, an
+    uneven last split) on the head_dim-128 / group-8 / q-k-norm shape."""
+    seed, shape, dtype = 2670, QWEN_SMALL, "bf16"
+    log("[test] strong long-context decode")
+    ctx = np.array([2500, 700, 129], np.int32)
+    alloc = synth.BlockAllocator(300, seed)
+    bt = synth.make_block_tables(ctx + 3, 160, alloc)
+    pair = strong_pair(shape, dtype, 1, 300, 1024, 4, seed)
+    try:
+        done = np.zeros(3, np.int32)
+        i = 0
+        while (done < ctx).any():
+            q = np.minimum(ctx - done, 400).astype(np.int32)
+            live = q > 0
+            y, yr, x = pair.prefill(q[live], done[live], bt[live],
+                                    synth.hidden_states(seed, 10 + i, int(q.sum()), shape.hidden))
+            check(f"chunk {i}", y, yr, x, dtype)
+            done += q
+            i += 1
+        for step in range(3):
+            y, yr, x = pair.decode(ctx + step, bt,
+                                   synth.hidden_states(seed, 100 + step, 3, shape.hidden))
+            check(f"decode {step}", y, yr, x, dtype)
+        check_kv(pair, dtype)
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("shape", GROUP_SHAPES, ids=[s.name for s in GROUP_SHAPES])
+def test_strong_gqa_group_sizes(dtype, shape):
+    """Every accepted GQA group size at both head dims: a ragged prefill
+    (1..150-token prompts, some past one prefill work item), continuation
+    chunks, decodes (one with a context long enough for several key splits)
+    and a mixed step."""
+    seed = 2680
+    log(f"[test] strong GQA {shape.name} dtype={dtype}")
+    lens = np.array([1, 16, 17, 150, 40], np.int32)
+    q2 = np.array([130, 3, 15, 1, 500], np.int32)
+    alloc = synth.BlockAllocator(96, seed)
+    bt = synth.make_block_tables(lens + q2 + 4, 48, alloc)
+    pbt = synth.make_block_tables([90], 8, alloc)
+    pair = strong_pair(shape, dtype, 2, 96, 1024, 8, seed)
+    try:
+        y, yr, x = pair.prefill(lens, np.zeros(5, np.int32), bt,
+                                synth.hidden_states(seed, 1, int(lens.sum()), shape.hidden))
+        check("prefill", y, yr, x, dtype)
+        y, yr, x = pair.prefill(q2, lens, bt, synth.hidden_states(seed, 2, int(q2.sum()),
+                                                                  shape.hidden))
+        check("chunk", y, yr, x, dtype)
+        ctx = lens + q2
+        for step in range(2):
+            y, yr, x = pair.decode(ctx, bt, synth.hidden_states(seed, 10 + step, 5, shape.hidden))
+            check(f"decode {step}", y, yr, x, dtype)
+            ctx += 1
+        pq, pc = np.array([90], np.int32), np.array([0], np.int32)
+        y, yr, x = pair.mixed(pq, pc, pbt, ctx, bt,
+                              synth.hidden_states(seed, 20, 95, shape.hidden))
+        check("mixed", y, yr, x, dtype)
+        check_kv(pair, dtype)
+    finally:
+        pair.close()
