@@ -72,6 +72,7 @@ __all__ = [
     "round_to_bf16",
     "slot_of",
     "attention_one_sequence",
+    "project_qkv",
     "layer_forward",
     "stage_forward",
 ]
@@ -200,6 +201,29 @@ def attention_one_sequence(q: np.ndarray, k_all: np.ndarray, v_all: np.ndarray,
     return out
 
 
+def project_qkv(cfg: OracleConfig, w: Dict[str, np.ndarray], x: np.ndarray,
+                pos: np.ndarray, rounding=None):
+    """The attention inputs of a layer for rows ``x`` ``[T, H]`` at positions
+    ``pos`` ``[T]``: RMSNorm, the QKV projection, (Qwen3) per-head RMSNorm of
+    q and k, and RoPE of q and k. Returns ``q`` ``[T, n_q, d]`` and the keys
+    and values the layer writes to its cache, ``k``, ``v`` ``[T, n_kv, d]``."""
+    rnd = rounding if rounding is not None else (lambda a: a)
+    nq, nkv, d = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    T = x.shape[0]
+    h = rnd(rms_norm(x, w["attn_norm"], cfg.rms_eps))
+    qkv = h @ w["w_qkv"].T                                 # [T, (nq+2nkv)d]
+    q = qkv[:, :nq * d].reshape(T, nq, d)
+    k = qkv[:, nq * d:(nq + nkv) * d].reshape(T, nkv, d)
+    v = qkv[:, (nq + nkv) * d:].reshape(T, nkv, d)
+    if cfg.qk_norm:
+        q = rms_norm(q, w["q_norm"], cfg.qk_rms_eps)
+        k = rms_norm(k, w["k_norm"], cfg.qk_rms_eps)
+    q = rnd(rope(q, pos, cfg.rope_theta))
+    k = rnd(rope(k, pos, cfg.rope_theta))
+    v = rnd(v)
+    return q, k, v
+
+
 def layer_forward(cfg: OracleConfig, w: Dict[str, np.ndarray], x: np.ndarray,
                   seqs: Sequence[SeqSpec], kv: Dict[str, np.ndarray],
                   rounding=None) -> np.ndarray:
@@ -217,20 +241,9 @@ def layer_forward(cfg: OracleConfig, w: Dict[str, np.ndarray], x: np.ndarray,
     assert T == sum(s.q_len for s in seqs)
 
     # attention branch
-    h = rnd(rms_norm(x, w["attn_norm"], cfg.rms_eps))
-    qkv = h @ w["w_qkv"].T                                 # [T, (nq+2nkv)d]
-    q = qkv[:, :nq * d].reshape(T, nq, d)
-    k = qkv[:, nq * d:(nq + nkv) * d].reshape(T, nkv, d)
-    v = qkv[:, (nq + nkv) * d:].reshape(T, nkv, d)
-    if cfg.qk_norm:
-        q = rms_norm(q, w["q_norm"], cfg.qk_rms_eps)
-        k = rms_norm(k, w["k_norm"], cfg.qk_rms_eps)
-
     pos = np.concatenate([np.arange(s.ctx_len, s.ctx_len + s.q_len) for s in seqs]) \
         if T else np.zeros(0, np.int64)
-    q = rnd(rope(q, pos, cfg.rope_theta))
-    k = rnd(rope(k, pos, cfg.rope_theta))
-    v = rnd(v)
+    q, k, v = project_qkv(cfg, w, x, pos, rounding)
 
     attn = np.empty((T, nq, d), dt)
     row = 0
