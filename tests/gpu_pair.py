@@ -12,9 +12,34 @@ import torch
 
 from oracle import stage_oracle as O
 from paper_2606_18600_amd import synth
-from paper_2606_18600_amd.harness import (DeviceStage, gpu_kv_to_oracle_layout, to_host64,
-                                          torch_dtype, upload_weights)
+from paper_2606_18600_amd.harness import DeviceStage, to_host64, torch_dtype, upload_weights
 from tests.helpers import ocfg, rel_l2, seqs_from
+
+
+def kv_plane_index(block: int, d: int):
+    """Index arrays (o, dd) -> flat position of K[o][dd] and V[o][dd] inside
+    one (block, kv head) plane (the fragment layouts of the KV pool)."""
+    o = np.arange(block)[:, None]
+    dd = np.arange(d)[None, :]
+    k = (dd // 32) * 512 + (o + 16 * ((dd % 32) // 8)) * 8 + dd % 8
+    v = (dd // 32) * 512 + (dd % 16 + 16 * (o // 4)) * 8 + ((dd // 16) % 2) * 4 + o % 4
+    return k, v
+
+
+def gpu_kv_to_oracle_layout(kv6: torch.Tensor) -> List[Dict[str, np.ndarray]]:
+    """Convert the GPU pool [L][nb][nkv][2][16][d] (planes in fragment order)
+    into per-layer {'k','v'} arrays [nb][16][nkv][d] in float64."""
+    a = kv6.detach().to(torch.float64).cpu().numpy()
+    L, nb, nkv, _, blk, d = a.shape
+    ki, vi = kv_plane_index(blk, d)
+    out = []
+    for l in range(L):
+        flat = a[l].reshape(nb, nkv, 2, blk * d)
+        k = flat[:, :, 0, :][:, :, ki]          # [nb][nkv][16][d]
+        v = flat[:, :, 1, :][:, :, vi]
+        out.append({"k": np.ascontiguousarray(k.transpose(0, 2, 1, 3)),
+                    "v": np.ascontiguousarray(v.transpose(0, 2, 1, 3))})
+    return out
 
 
 def log(msg: str) -> None:

@@ -28,8 +28,8 @@ import torch
 from oracle import stage_oracle as O
 from paper_2606_18600_amd import synth
 from paper_2606_18600_amd.harness import (DeviceStage, device_layer_weights,
-                                          gpu_kv_to_oracle_layout, model_config, pack_layer)
-from tests.gpu_pair import log
+                                          model_config, pack_layer)
+from tests.gpu_pair import gpu_kv_to_oracle_layout, kv_plane_index, log
 from tests.helpers import ocfg, rel_l2
 
 pytestmark = pytest.mark.gpu
@@ -57,6 +57,44 @@ def _seq_cache(st, bt_row, n_tok):
 
 def _kv_at(cache, table, p):
     return cache["k"][table[p // 16], p % 16], cache["v"][table[p // 16], p % 16]
+
+
+def _check_all_written_kv(shape, st, w64, tables, ctx_lens, q_lens, x_in, tag, chunk=2048):
+    """Every K/V entry a one-layer call wrote (all of its rows), against the
+    oracle's own projection of the call's input rows (O.project_qkv: RMSNorm,
+    QKV projection, q/k-norm, RoPE, from the stored weights). Checked row by
+    row, so one wrong token cannot hide in a large call."""
+    oc = ocfg(shape)
+    nkv, d = shape.n_kv_heads, shape.head_dim
+    pos = np.concatenate([np.arange(c, c + q) for c, q in zip(ctx_lens, q_lens)]).astype(np.int64)
+    blk = np.concatenate([np.asarray(tables[i])[np.arange(c, c + q) // 16]
+                          for i, (c, q) in enumerate(zip(ctx_lens, q_lens))]).astype(np.int64)
+    assert len(pos) == x_in.shape[0]
+    ki, vi = kv_plane_index(16, d)
+    ki_t, vi_t = torch.from_numpy(ki).cuda(), torch.from_numpy(vi).cuda()
+    planes = st.kv_view()[0].reshape(st.num_blocks, nkv, 2, 16 * d)
+    worst_k = worst_v = 0.0
+    for r0 in range(0, len(pos), chunk):
+        r1 = min(len(pos), r0 + chunk)
+        _, k_ref, v_ref = O.project_qkv(oc, w64, x_in[r0:r1], pos[r0:r1])
+        b_t = torch.from_numpy(blk[r0:r1]).cuda()
+        o_t = torch.from_numpy(pos[r0:r1] % 16).cuda()
+        sel = planes[b_t]                                  # [n, nkv, 2, 16 d]
+        gk = torch.gather(sel[:, :, 0, :], 2, ki_t[o_t][:, None, :].expand(-1, nkv, -1))
+        gv = torch.gather(sel[:, :, 1, :], 2, vi_t[o_t][:, None, :].expand(-1, nkv, -1))
+        gk, gv = gk.double().cpu().numpy(), gv.double().cpu().numpy()
+        for g, ref, name in ((gk, k_ref, "K"), (gv, v_ref, "V")):
+            err = np.linalg.norm((g - ref).reshape(len(g), -1), axis=1) / \
+                np.linalg.norm(ref.reshape(len(ref), -1), axis=1)
+            i = int(np.argmax(err))
+            assert err[i] <= TOL, f"{tag}: {name} of row {r0 + i} (position {pos[r0 + i]}) " \
+                                  f"rel_l2 {err[i]:.3e}"
+            if name == "K":
+                worst_k = max(worst_k, float(err.max()))
+            else:
+                worst_v = max(worst_v, float(err.max()))
+    log(f"  {tag}: all {len(pos)} written K/V rows, worst per-row rel_l2 K {worst_k:.3e} "
+        f"V {worst_v:.3e}")
 
 
 def test_l70_decode_20_layers_sampled():
@@ -132,6 +170,51 @@ def test_l70_decode_20_layers_sampled():
         log(f"  seq {s} ctx {int(ctx[s])}: output rel_l2 vs exact {e_ex:.3e}, vs bf16-emulated "
             f"{e_em:.3e}; emulated vs exact (bf16 floor) {floor:.3e}")
         assert e_ex <= max(TOL, 1.25 * floor), (s, e_ex, floor)
+        assert e_em <= max(TOL, 1.25 * floor), (s, e_em, floor)
+
+
+def test_l70_first_positions_and_one_token_prompts():
+    """One L70 layer. A decode batch of 64 whose first sequences sit at
+    positions 0, 1, 15 and 16 (the rest at U[512, 2048]); then one prefill
+    call of 2048 rows made of prompts of 1, 1, 17 and 2029 tokens (the
+    2048-row path: split query / key-value QKV, RoPE in the query product's
+    epilogue). Every edge row against the oracle, and every K/V entry both
+    calls wrote."""
+    seed, shape, layer, B = 2613, synth.LLAMA70B, 33, 64
+    log("l70 first positions and one-token prompts, one layer")
+    cfg = model_config(shape, "bf16")
+    w = device_layer_weights(shape, seed, layer, "bf16")
+    w64 = _host64(w)
+    ctx = synth.uniform_lengths(seed, 1, B, 512, 2048)
+    ctx[:4] = [0, 1, 15, 16]
+    pq = np.array([1, 1, 17, 2029], np.int32)
+    pc = np.zeros(4, np.int32)
+    alloc = synth.BlockAllocator(int(((ctx + 16) // 16).sum() + ((pq + 15) // 16).sum()) + 8, seed)
+    dbt_np = synth.make_block_tables(ctx + 1, int((ctx.max() + 16) // 16), alloc)
+    pbt_np = synth.make_block_tables(pq, int((pq.max() + 15) // 16), alloc)
+    nb = int(max(dbt_np.max(), pbt_np.max())) + 1
+    st = DeviceStage(shape, "bf16", layer, [pack_layer(cfg, w)], nb, 2048, B, packed=True)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    try:
+        st.kv_pool.normal_(0.0, 1.0, generator=g)
+        x = torch.randn((B, shape.hidden), generator=g, device="cuda").to(torch.bfloat16)
+        y = st.decode(ctx, torch.from_numpy(dbt_np).cuda(), x)
+        torch.cuda.synchronize()
+        x64, y64 = x.double().cpu().numpy(), y.double().cpu().numpy()
+        rows = [(j, int(ctx[j]), j) for j in (0, 1, 2, 3, 40)]
+        _check_rows_one_layer(shape, st, w64, dbt_np, rows, x64, y64, "decode rows at 0/1/15/16")
+        _check_all_written_kv(shape, st, w64, dbt_np, ctx, np.ones(B, np.int32), x64, "decode")
+        x = torch.randn((2048, shape.hidden), generator=g, device="cuda").to(torch.bfloat16)
+        y = st.prefill(pq, pc, torch.from_numpy(pbt_np).cuda(), x)
+        torch.cuda.synchronize()
+        x64, y64 = x.double().cpu().numpy(), y.double().cpu().numpy()
+        rows = [(0, 0, 0), (1, 0, 1)] + [(2, p, 2 + p) for p in range(17)] + \
+            _sample_rows(np.random.default_rng(seed), pq, pc, 6)
+        _check_rows_one_layer(shape, st, w64, pbt_np, rows, x64, y64, "prefill rows")
+        _check_all_written_kv(shape, st, w64, pbt_np, pc, pq, x64, "prefill 1+1+17+2029")
+    finally:
+        st.close()
 
 
 def test_l70_decode_one_layer_sampled():
@@ -160,6 +243,8 @@ def test_l70_decode_one_layer_sampled():
         rows = [(j, int(ctx[j]), j) for j in pick]
         _check_rows_one_layer(shape, st, w64, bt_np, rows, x.double().cpu().numpy(),
                               y.double().cpu().numpy(), "decode rows")
+        _check_all_written_kv(shape, st, w64, bt_np, ctx, np.ones(B, np.int32),
+                              x.double().cpu().numpy(), "decode")
     finally:
         st.close()
 
@@ -218,6 +303,8 @@ def test_l70_prefill_chunks_sampled():
             rows = _sample_rows(rng, [q], [ctx0], 10)
             _check_rows_one_layer(shape, st, w64, bt_np, rows, x.double().cpu().numpy(),
                                   y.double().cpu().numpy(), f"chunk ctx={ctx0} q={q}")
+            _check_all_written_kv(shape, st, w64, bt_np, [ctx0], [q], x.double().cpu().numpy(),
+                                  f"chunk ctx={ctx0} q={q}")
     finally:
         st.close()
 
@@ -253,6 +340,8 @@ def test_l70_bench_prefill_schedule_sampled():
             rows = _sample_rows(rng, q, ctx, 4)
             _check_rows_one_layer(shape, st, w64, bt_np[idx], rows, x.double().cpu().numpy(),
                                   y.double().cpu().numpy(), f"step {k} {list(zip(ctx, q))}")
+            _check_all_written_kv(shape, st, w64, bt_np[idx], ctx, q, x.double().cpu().numpy(),
+                                  f"step {k}")
     finally:
         st.close()
 
@@ -288,6 +377,9 @@ def test_q32_mixed_step_sampled():
                 for j in sorted({0, 127, int(np.argmax(dctx)), int(np.argmin(dctx))} |
                                 set(rng.choice(128, 6, replace=False).tolist()))]
         _check_rows_one_layer(shape, st, w64, dbt_np, drow, x64, y64, "decode rows")
+        _check_all_written_kv(shape, st, w64, list(pbt_np) + list(dbt_np),
+                              list(pc) + list(dctx), list(pq) + [1] * len(dctx), x64,
+                              "mixed step")
     finally:
         st.close()
 
@@ -318,6 +410,8 @@ def test_l70_decode_batch128_one_layer_sampled():
         rows = [(j, int(ctx[j]), j) for j in pick]
         _check_rows_one_layer(shape, st, w64, bt_np, rows, x.double().cpu().numpy(),
                               y.double().cpu().numpy(), "decode rows (batch 128)")
+        _check_all_written_kv(shape, st, w64, bt_np, ctx, np.ones(B, np.int32),
+                              x.double().cpu().numpy(), "decode (batch 128)")
     finally:
         st.close()
 
@@ -356,6 +450,9 @@ def test_l70_mixed_step_sampled():
                 for j in sorted({0, 127, int(np.argmax(dctx)), int(np.argmin(dctx))} |
                                 set(rng.choice(128, 6, replace=False).tolist()))]
         _check_rows_one_layer(shape, st, w64, dbt_np, drow, x64, y64, "decode rows")
+        _check_all_written_kv(shape, st, w64, list(pbt_np) + list(dbt_np),
+                              list(pc) + list(dctx), list(pq) + [1] * len(dctx), x64,
+                              "mixed step")
     finally:
         st.close()
 
@@ -385,5 +482,7 @@ def test_l70_one_call_prefill_of_8192_tokens_sampled():
         rng = np.random.default_rng(seed)
         _check_rows_one_layer(shape, st, w64, bt_np, _sample_rows(rng, pq, pc, 8),
                               x.double().cpu().numpy(), y.double().cpu().numpy(), "rows")
+        _check_all_written_kv(shape, st, w64, bt_np, pc, pq, x.double().cpu().numpy(),
+                              "8192-token call")
     finally:
         st.close()

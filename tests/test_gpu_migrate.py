@@ -11,11 +11,11 @@ import torch
 
 from oracle import stage_oracle as O
 from paper_2606_18600_amd import synth
-from paper_2606_18600_amd.harness import (DeviceStage, device_layer_weights, gpu_kv_to_oracle_layout,
+from paper_2606_18600_amd.harness import (DeviceStage, device_layer_weights,
                                           model_config, pack_layer, to_host64, torch_dtype,
                                           upload_weights)
 from paper_2606_18600_amd.migrate import recompute_kv
-from tests.gpu_pair import log
+from tests.gpu_pair import gpu_kv_to_oracle_layout, log
 from tests.helpers import ocfg, rel_l2
 
 pytestmark = pytest.mark.gpu

@@ -7,7 +7,7 @@ import pytest
 def test_kv_plane_layouts_are_permutations(d):
     """Every (token, d) of a KV block plane has its own slot in the fragment
     layouts the attention kernels read (K and V planes)."""
-    from paper_2606_18600_amd.harness import kv_plane_index
+    from tests.gpu_pair import kv_plane_index
     k, v = kv_plane_index(16, d)
     for idx in (k, v):
         assert sorted(idx.ravel().tolist()) == list(range(16 * d))
