@@ -80,34 +80,224 @@ def bench_q32_mixed(args):
         st.mixed(pq, pc, pbt, dctx0 + i, dbt, x, out, stream=sp)
         i += 1
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
     ctx_timed = []
-    e0.record(stream)
-    for _ in range(K):
+    ev[0].record(stream)
+    for k in range(K):
         st.mixed(pq, pc, pbt, dctx0 + i, dbt, x, out, stream=sp)
+        ev[k + 1].record(stream)
         ctx_timed.append(dctx0 + i)
         i += 1
-    e1.record(stream)
     torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / K
+    ms = ev[0].elapsed_time(ev[K]) / K
+    step_ms = [ev[k].elapsed_time(ev[k + 1]) for k in range(K)]
+    assert torch.isfinite(out.float()).all(), "non-finite stage output"
     S.stage_set_op_timing(st.handle, True)
     for _ in range(K):
         st.mixed(pq, pc, pbt, dctx0 + i, dbt, x, out, stream=sp)
         i += 1
     op_ms, op_n = S.stage_read_op_times(st.handle)
     st.close()
+    del weights, st
+    torch.cuda.empty_cache()
     chunks = list(zip(pc.tolist(), pq.tolist()))
     roof = float(np.mean([step_roofline_ms(shape, nL, chunks, c) for c in ctx_timed]))
+    # dominant kernel: the gate-up + SwiGLU product of the 2176-row step
+    j = S.OP_NAMES.index("gate_up")
+    gu_us = op_ms[j] / op_n[j] * 1e3
+    gu_fl = 2.0 * 2176 * 2 * shape.ffn * shape.hidden
+    gu_tfs = gu_fl / (gu_us / 1e6) / 1e12
     res = {"workload": "q32-mixed: Qwen3-32B-shaped stage, layers [24,40); per step 4 x 512 "
                        "prefill chunks (prefixes 0/512/1024/1536) + 128 decodes, contexts "
                        "uniform 256-4096",
-           "ms_per_step": round(ms, 3), "prefill_tok_s": round(2048 / (ms / 1e3), 1),
+           "steps": K, "warmup": W,
+           "ms_per_step": round(ms, 3),
+           "step_ms_p50": round(float(np.percentile(step_ms, 50)), 3),
+           "step_ms_p90": round(float(np.percentile(step_ms, 90)), 3),
+           "prefill_tok_s": round(2048 / (ms / 1e3), 1),
            "decode_tok_s": round(128 / (ms / 1e3), 1),
            "roofline_ms": round(roof, 3), "roofline_frac": round(roof / ms, 4),
+           "roofline": {"bound": "mfma", "kernel": "gemm_tiled_bf16 (gate-up + SwiGLU, 2176 rows)",
+                        "achieved": round(gu_tfs, 1), "peak": BF16_PEAK_TFLOPS,
+                        "unit": "TFLOP/s", "frac": round(gu_tfs / BF16_PEAK_TFLOPS, 4),
+                        "traffic": None, "flop_per_launch": gu_fl,
+                        "us_per_launch": round(gu_us, 1)},
            "ops_ms_per_step": {S.OP_NAMES[j]: round(op_ms[j] / K, 4) for j in range(len(op_ms))}}
     log(f"[bench] q32-mixed {ms:.3f} ms/step (roofline {roof:.3f} ms, {roof / ms:.1%}); "
-        f"{2048 / (ms / 1e3):.0f} prefill + {128 / (ms / 1e3):.0f} decode tok/s")
+        f"{2048 / (ms / 1e3):.0f} prefill + {128 / (ms / 1e3):.0f} decode tok/s; "
+        f"gate-up {gu_tfs:.0f} TFLOP/s")
+    if not getattr(args, "no_cpu", False):
+        log("[bench] timing the CPU oracle: one mixed step of one Qwen3-32B-shaped layer")
+        sec, reps, spent = oracle_layer_step(shape, chunks + [(int(c), 1) for c in dctx0], seed)
+        res["cpu_baseline"] = cpu_block(2048 + 128, nL, sec, reps, spent,
+                                        "one mixed step (4 x 512 prefill + 128 decode tokens; "
+                                        "value counts both)")
     return res
+
+
+def bench_tiny(args):
+    """The tiny configuration end to end: 2 layers (hidden 256, 4/2 heads,
+    head_dim 64, ffn 704), fp32 weights N(0, 0.02^2) from the seed, 4 prompts
+    of 16..64 tokens prefilled in one call, then 16 decode steps; whole-run
+    times in the fp32 and bf16 modes (launch-bound: neither roofline
+    applies), and the oracle over the same run on the host."""
+    import torch
+    from paper_2606_18600_amd import synth
+    from paper_2606_18600_amd.harness import DeviceStage, upload_weights
+    dev = torch.device("cuda:0")
+    shape, seed = synth.TINY, args.seed
+    host = [synth.host_layer_weights(shape, seed, l) for l in range(2)]
+    lens = synth.uniform_lengths(seed, 0, 4, 16, 64)
+    bt_np = synth.make_block_tables(lens + 16, 8, synth.BlockAllocator(64, seed))
+    bt = torch.from_numpy(bt_np).to(dev)
+    xp = synth.hidden_states(seed, 1, int(lens.sum()), shape.hidden)
+    xd = [synth.hidden_states(seed, 100 + k, 4, shape.hidden) for k in range(16)]
+    n_tok = int(lens.sum()) + 64
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    res = {"workload": "tiny: 2 layers, hidden 256, 4 q / 2 kv heads, head_dim 64, ffn 704; "
+                       "4 prompts uniform 16-64 prefilled, then 16 decode steps",
+           "prompt_tokens": int(lens.sum()), "decode_tokens": 64}
+    for dt in ("f32", "bf16"):
+        td = torch.float32 if dt == "f32" else torch.bfloat16
+        st = DeviceStage(shape, dt, 0, [upload_weights(h, dt) for h in host], 64, 256, 8)
+        xpt = torch.from_numpy(xp).to(dev, td)
+        xdt = [torch.from_numpy(a).to(dev, td) for a in xd]
+        out = torch.empty_like(xpt)
+
+        def run():
+            st.prefill(lens, np.zeros(4, np.int32), bt, xpt, out, stream=sp)
+            for k in range(16):
+                st.decode(lens + k, bt, xdt[k], out[:4], stream=sp)
+
+        for _ in range(3):
+            run()
+        torch.cuda.synchronize()
+        reps = max(5, args.steps)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        st.close()
+        res[dt] = {"ms_per_run": round(ms, 4), "tok_s": round(n_tok / (ms / 1e3), 1),
+                   "runs": reps}
+        log(f"[bench] tiny {dt}: {ms:.3f} ms per run (prefill + 16 decodes), "
+            f"{n_tok / (ms / 1e3):.0f} tok/s")
+    if not getattr(args, "no_cpu", False):
+        from oracle import stage_oracle as O
+        cfg = O.OracleConfig(shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
+                             shape.ffn, shape.rms_eps, shape.rope_theta)
+
+        def oracle_run():
+            kv = O.new_kv_cache(cfg, 2, 64, np.float32)
+            O.stage_forward(cfg, host, xp, [O.SeqSpec(0, int(q), list(r))
+                                            for q, r in zip(lens, bt_np)], kv, dtype=np.float32)
+            for k in range(16):
+                O.stage_forward(cfg, host, xd[k], [O.SeqSpec(int(c) + k, 1, list(r))
+                                                   for c, r in zip(lens, bt_np)], kv,
+                                dtype=np.float32)
+
+        sec, reps, spent = time_oracle(oracle_run, 5.0)
+        res["cpu_baseline"] = {"value": round(n_tok / sec, 1), "unit": "tok/s",
+                               "cores": blas_threads(), "kind": "oracle",
+                               "sample": f"the whole run (prefill + 16 decode steps, 2 layers) "
+                                         f"in float32, {reps} run(s) in {spent:.1f} s"}
+    return res
+
+
+def bench_full_model(args):
+    """The 80-layer model as one stage under continuous batching, with the
+    roofline of its dominant kernels and the oracle baseline."""
+    import torch
+    from paper_2606_18600_amd import stage as S
+    from paper_2606_18600_amd import synth
+    from paper_2606_18600_amd.batcher import bench_l70_full
+    shape, nL = synth.LLAMA70B, 80
+    res = bench_l70_full(args, log)
+    j = S.OP_NAMES.index("gate_up")
+    for name in ("decode_only", "offline", "poisson"):
+        r = res[name]
+        op_ms, op_n = r.pop("_op_ms", None), r.pop("_op_n", None)
+        if op_ms is not None and op_n[j]:
+            r["ops_ms_per_step"] = {S.OP_NAMES[k]: round(op_ms[k] / 3, 3)
+                                    for k in range(len(op_ms))}
+    # dominant kernels: the decode-only step's gate-up (HBM) and the mixed
+    # step's gate-up (MFMA), from the per-op timing of the steps after the
+    # timed ones
+    d = res["decode_only"]
+    if "ops_ms_per_step" in d:
+        gu_us = d["ops_ms_per_step"]["gate_up"] / nL * 1e3
+        B = 128
+        byts = 2 * shape.ffn * shape.hidden * 2 + B * shape.hidden * 2 + B * shape.ffn * 2
+        gbs = byts / (gu_us / 1e6) / 1e9
+        res["roofline"] = {"bound": "hbm", "kernel": "gemm_skinny_bf16 (gate-up + SwiGLU, "
+                                                     "decode-only steps, up to 128 rows)",
+                           "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                           "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                           "bytes_per_launch": byts, "us_per_launch": round(gu_us, 1),
+                           "note": "bytes at batch 128; the batch shrinks as requests finish"}
+    m = res["offline"]
+    if "ops_ms_per_step" in m:
+        gu_us = m["ops_ms_per_step"]["gate_up"] / nL * 1e3
+        fl = 2.0 * 2176 * 2 * shape.ffn * shape.hidden
+        res["roofline_mixed"] = {"bound": "mfma", "kernel": "gemm_tiled_bf16 (gate-up + SwiGLU, "
+                                                            "2176-row mixed steps)",
+                                 "achieved": round(fl / (gu_us / 1e6) / 1e12, 1),
+                                 "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                 "frac": round(fl / (gu_us / 1e6) / 1e12 / BF16_PEAK_TFLOPS, 4),
+                                 "traffic": None, "us_per_launch": round(gu_us, 1),
+                                 "note": "FLOPs at 2176 rows (2048 prefill + 128 decode)"}
+    if not getattr(args, "no_cpu", False):
+        log("[bench] timing the CPU oracle: one decode step (batch 128) of one layer")
+        ctx = synth.uniform_lengths(args.seed, 10, 128, 1024, 4096)
+        sec, reps, spent = oracle_layer_step(shape, [(int(c), 1) for c in ctx], args.seed)
+        res["cpu_baseline"] = cpu_block(128, nL, sec, reps, spent,
+                                        "one decode step, batch 128, contexts uniform 1024-4096")
+    return res
+
+
+def bench_default(args):
+    """One line for all five configurations: the metric's workload (the
+    20-layer Llama-3.1-70B-shaped decode, batch 64) as `value`, the chunked
+    prefill of the same stage, the tiny stage, the Qwen3-32B-shaped mixed step
+    and the 80-layer model under continuous batching, each with its roofline
+    and the oracle's time on the host."""
+    import torch
+    from paper_2606_18600_amd import stage as S
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    only = set(args.only.split(",")) if args.only else {"c1", "c2", "c4", "c5"}
+    configs = {}
+    result = None
+    if "c1" in only:
+        configs["c1_tiny"] = bench_tiny(args)
+    if "c2" in only:
+        result, ms, step_bytes, gu_gbs = bench_l70_stage(args)
+    if "c4" in only:
+        configs["c4_q32_mixed"] = bench_q32_mixed(args)
+    if "c5" in only:
+        configs["c5_l70_full"] = bench_full_model(args)
+    if result is None:
+        result = {"metric": METRIC, "value": None, "unit": "tok/s", "n_gpus": 1,
+                  "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
+                  "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+                  "config": {"workload": "partial run (--only)"}}
+    cal = calibrate(torch, S, stream)
+    if "c2" in only:
+        cal["gate_up_frac_of_copy"] = round(gu_gbs / cal["copy_GBs"], 4)
+        cal["decode_step_frac_of_copy"] = round(step_bytes / (ms / 1e3) / 1e9 / cal["copy_GBs"],
+                                                4)
+        if "prefill" in result:
+            cal["prefill_frac_of_gemm_probe"] = round(
+                result["prefill"]["tflops"] / cal["gemm_TFLOPs"], 4)
+    result["calibrated"] = cal
+    log(f"[bench] calibration: {cal}")
+    result["host"] = host_info()
+    result["configs"] = configs
+    return result
 
 
 # Context lengths of the migration sweep, and the links a migrated
@@ -515,109 +705,82 @@ def summarize_pmc(fetch_dir, write_dir, title, cmds, algorithmic, top=12):
     return "\n".join(out)
 
 
-def cpu_baseline(shape, ctx_lens, seed):
-    """The oracle (float32) on the host: one decode step of one layer for the
-    whole batch, scaled by the stage's 20 layers (every layer costs the same)."""
-    import torch
-    from oracle import stage_oracle as O
-    from paper_2606_18600_amd import synth
-    cfg = O.OracleConfig(shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
-                         shape.ffn, shape.rms_eps, shape.rope_theta)
-    w = synth.host_layer_weights(shape, seed, 20, dtype=np.float32)
-    B = len(ctx_lens)
-    nbps = (ctx_lens + 1 + 15) // 16
-    nb = int(nbps.sum())
-    kv = O.new_kv_cache(cfg, 1, nb, np.float32)
-    r = np.random.default_rng(seed)
-    kv[0]["k"][:] = r.standard_normal(kv[0]["k"].shape, dtype=np.float32)
-    kv[0]["v"][:] = r.standard_normal(kv[0]["v"].shape, dtype=np.float32)
-    starts = np.concatenate([[0], np.cumsum(nbps)])
-    seqs = [O.SeqSpec(int(c), 1, list(range(starts[i], starts[i + 1])))
-            for i, c in enumerate(ctx_lens)]
-    x = synth.hidden_states(seed, 9, B, shape.hidden)
-    O.stage_forward(cfg, [w], x[:2], seqs[:2], kv, dtype=np.float32)  # warm caches
-    reps, t0 = 0, time.perf_counter()
-    while reps < 40 and (reps == 0 or time.perf_counter() - t0 < 10.0):
-        O.stage_forward(cfg, [w], x, seqs, kv, dtype=np.float32)
-        reps += 1
-    total = time.perf_counter() - t0
-    dt = total / reps
+def host_info():
+    """The host the oracle baselines run on."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "nproc": os.cpu_count(), "oracle_threads": blas_threads()}
+
+
+def blas_threads():
     try:
         from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        return int(max([i.get("num_threads", 1) for i in threadpool_info()] + [1]))
     except Exception:
-        cores = os.cpu_count()
-    step_s = dt * 20
-    return {"value": B / step_s, "unit": "tok/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"one decode step of one layer, batch {B} (contexts as the workload), "
-                      f"float32, repeated {reps}x ({total:.1f} s, {dt:.2f} s each), "
-                      f"scaled x20 layers"}
+        return int(os.cpu_count() or 1)
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--seed", type=int, default=2606)
-    ap.add_argument("--no-prefill", action="store_true")
-    ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--requests", type=int, default=512,
-                    help="l70-full: new requests queued behind the 128 running ones")
-    ap.add_argument("--arrival-rate", type=float, default=0.0,
-                    help="l70-full: Poisson arrivals per second (0: all at t=0)")
-    ap.add_argument("--workload", default="l70-decode",
-                    choices=["l70-decode", "q32-mixed", "l70-full", "migrate", "estimator",
-                             "lm-head"],
-                    help="l70-decode (default: the metric's workload, plus the chunked prefill "
-                         "of the same stage); the others print their own line")
-    ap.add_argument("--summarize-trace", metavar="DIR",
-                    help="print a summary of a rocprofv3 kernel trace under DIR and exit")
-    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
-                    help="print HBM traffic per launch from FETCH_SIZE / WRITE_SIZE runs and exit")
-    ap.add_argument("--summary-title", default="")
-    ap.add_argument("--summary-cmd", action="append", default=[])
-    args = ap.parse_args()
-    if args.summarize_trace:
-        print(summarize_trace(args.summarize_trace, args.summary_title,
-                              " ; ".join(args.summary_cmd)))
-        return
-    if args.summarize_pmc:
-        from paper_2606_18600_amd import synth
-        sh = synth.LLAMA70B
-        alg = (f"decode gate-up + SwiGLU (M=64, N={2 * sh.ffn}, K={sh.hidden}) "
-               f"{gate_up_swiglu_bytes(sh, 64)} bytes")
-        print(summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.summary_title,
-                            args.summary_cmd, alg))
-        return
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU: the stage runs on a single MI355X and the library "
-              f"has no multi-GPU path (asked for --gpus {args.gpus}).", file=sys.stderr)
-        sys.exit(2)
+def time_oracle(fn, budget_s=10.0, max_reps=40):
+    """Seconds per call of fn: calls repeated until about budget_s have
+    passed (at least once; the first call is dropped when there are more)."""
+    ts = []
+    t_start = time.perf_counter()
+    while len(ts) < max_reps and (not ts or time.perf_counter() - t_start < budget_s):
+        t0 = time.perf_counter()
+        fn()
+        ts.append(time.perf_counter() - t0)
+    body = ts[1:] if len(ts) > 2 else ts
+    return float(np.mean(body)), len(ts), time.perf_counter() - t_start
 
-    if args.workload == "q32-mixed":
-        print(json.dumps({"metric": METRIC, "n_gpus": 1, "steps": args.steps,
-                          "warmup": args.warmup, "dtype": "bf16", "data": "synthetic",
-                          **bench_q32_mixed(args)}), flush=True)
-        return
-    if args.workload == "lm-head":
-        print(json.dumps({"metric": METRIC, "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
-                          **bench_lm_head(args)}), flush=True)
-        return
-    if args.workload == "estimator":
-        print(json.dumps({"metric": METRIC, "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
-                          **bench_estimator(args)}), flush=True)
-        return
-    if args.workload == "migrate":
-        print(json.dumps({"metric": METRIC, "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
-                          **bench_migrate(args)}), flush=True)
-        return
-    if args.workload == "l70-full":
-        from paper_2606_18600_amd.batcher import bench_l70_full
-        print(json.dumps({"metric": METRIC, "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
-                          **bench_l70_full(args, log)}), flush=True)
-        return
 
+def oracle_layer_step(shape, seqs, seed, budget_s=10.0):
+    """The oracle (float32) for one step of one layer: sequences given as
+    (ctx, q) pairs, their context KV present in a paged cache (values do not
+    change the cost), random weights of the layer's shape. Returns (seconds
+    per step and layer, repetitions, seconds spent)."""
+    from oracle import stage_oracle as O
+    from paper_2606_18600_amd.synth import GAIN_NAMES
+    cfg = O.OracleConfig(shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
+                         shape.ffn, shape.rms_eps, shape.rope_theta, shape.qk_norm,
+                         shape.qk_rms_eps)
+    r = np.random.default_rng(seed)
+    w = {}
+    for name, shp in shape.weight_shapes().items():
+        a = r.standard_normal(shp, dtype=np.float32)
+        w[name] = (1.0 + 0.02 * a) if name in GAIN_NAMES else 0.02 * a
+    nbps = [(int(c) + int(q) + 15) // 16 for c, q in seqs]
+    kv = O.new_kv_cache(cfg, 1, int(sum(nbps)), np.float32)
+    kv[0]["k"].fill(0.01)
+    kv[0]["v"].fill(0.01)
+    starts = np.concatenate([[0], np.cumsum(nbps)]).astype(int)
+    specs = [O.SeqSpec(int(c), int(q), list(range(starts[i], starts[i + 1])))
+             for i, (c, q) in enumerate(seqs)]
+    x = r.standard_normal((int(sum(q for _, q in seqs)), shape.hidden), dtype=np.float32)
+    return time_oracle(lambda: O.stage_forward(cfg, [w], x, specs, kv, dtype=np.float32),
+                       budget_s)
+
+
+def cpu_block(tokens_per_step, n_layers, sec_layer, reps, spent, what, unit="tok/s"):
+    """A cpu_baseline entry: one step of one layer timed, scaled by the
+    stage's layers (every layer of a stage costs the same)."""
+    step_s = sec_layer * n_layers
+    return {"value": round(tokens_per_step / step_s, 3), "unit": unit, "cores": blas_threads(),
+            "kind": "oracle",
+            "sample": f"{what}; one layer in float32, {reps} run(s) in {spent:.1f} s, "
+                      f"{sec_layer:.3f} s each, scaled x{n_layers} layers"}
+
+
+def bench_l70_stage(args):
+    """The metric's workload: the 20-layer Llama-3.1-70B-shaped stage, decode
+    batch 64 (C2), then the chunked prefill of 8 prompts on the same stage
+    (C3)."""
     import torch
     from paper_2606_18600_amd import stage as S
     from paper_2606_18600_amd import synth
@@ -724,6 +887,7 @@ def main():
     }
     result["roofline"]["traffic_note"] = traffic_note
 
+    steps = []
     if not args.no_prefill:
         pf_bt = torch.from_numpy(pf_bt_np).to(dev)
         steps = synth.chunk_schedule(p_lens, 2048)
@@ -772,20 +936,90 @@ def main():
             f"{pfl / (pms / 1e3) / 1e12:.0f} TFLOP/s; gate_up {gu_tfs:.0f} TFLOP/s")
 
     st.close()
-    del weights
+    del weights, st
     torch.cuda.empty_cache()
-
-    cal = calibrate(torch, S, stream)
-    cal["gate_up_frac_of_copy"] = round(gu_gbs / cal["copy_GBs"], 4)
-    cal["decode_step_frac_of_copy"] = round(step_bytes / (ms / 1e3) / 1e9 / cal["copy_GBs"], 4)
-    if "prefill" in result:
-        cal["prefill_frac_of_gemm_probe"] = round(result["prefill"]["tflops"] / cal["gemm_TFLOPs"], 4)
-    result["calibrated"] = cal
-    log(f"[bench] calibration: {cal}")
-
     if not args.no_cpu:
-        log("[bench] timing the CPU oracle on a bounded sample")
-        result["cpu_baseline"] = cpu_baseline(shape, ctx0, seed)
+        log("[bench] timing the CPU oracle: one decode step and one 2048-token chunk of one layer")
+        sec, reps, spent = oracle_layer_step(shape, [(int(c), 1) for c in ctx0], seed)
+        result["cpu_baseline"] = cpu_block(B, nL, sec, reps, spent,
+                                           f"one decode step, batch {B} (contexts as the workload)")
+        if "prefill" in result:
+            first = steps[0]
+            sec, reps, spent = oracle_layer_step(shape, [(c, q) for _, c, q in first], seed)
+            result["prefill"]["cpu_baseline"] = cpu_block(
+                sum(q for _, _, q in first), nL, sec, reps, spent,
+                f"one 2048-token prefill step (the schedule's first: {len(first)} prompt chunk(s))")
+    return result, ms, step_bytes, gu_gbs
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--seed", type=int, default=2606)
+    ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--only", default="",
+                    help="default run: comma-separated subset of c1,c2,c4,c5 (c2 includes the "
+                         "prefill, c3)")
+    ap.add_argument("--requests", type=int, default=512,
+                    help="l70-full: new requests queued behind the 128 running ones")
+    ap.add_argument("--arrival-rate", type=float, default=0.0,
+                    help="l70-full: Poisson arrivals per second (0: all at t=0)")
+    ap.add_argument("--workload", default="l70-decode",
+                    choices=["l70-decode", "q32-mixed", "l70-full", "migrate", "estimator",
+                             "lm-head"],
+                    help="l70-decode (default: the metric's workload, plus the chunked prefill "
+                         "of the same stage); the others print their own line")
+    ap.add_argument("--summarize-trace", metavar="DIR",
+                    help="print a summary of a rocprofv3 kernel trace under DIR and exit")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="print HBM traffic per launch from FETCH_SIZE / WRITE_SIZE runs and exit")
+    ap.add_argument("--summary-title", default="")
+    ap.add_argument("--summary-cmd", action="append", default=[])
+    args = ap.parse_args()
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace, args.summary_title,
+                              " ; ".join(args.summary_cmd)))
+        return
+    if args.summarize_pmc:
+        from paper_2606_18600_amd import synth
+        sh = synth.LLAMA70B
+        alg = (f"decode gate-up + SwiGLU (M=64, N={2 * sh.ffn}, K={sh.hidden}) "
+               f"{gate_up_swiglu_bytes(sh, 64)} bytes")
+        print(summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.summary_title,
+                            args.summary_cmd, alg))
+        return
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: the stage runs on a single MI355X and the library "
+              f"has no multi-GPU path (asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    if args.workload == "q32-mixed":
+        print(json.dumps({"metric": METRIC, "n_gpus": 1, "steps": args.steps,
+                          "warmup": args.warmup, "dtype": "bf16", "data": "synthetic",
+                          **bench_q32_mixed(args)}), flush=True)
+        return
+    if args.workload == "lm-head":
+        print(json.dumps({"metric": METRIC, "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
+                          **bench_lm_head(args)}), flush=True)
+        return
+    if args.workload == "estimator":
+        print(json.dumps({"metric": METRIC, "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
+                          **bench_estimator(args)}), flush=True)
+        return
+    if args.workload == "migrate":
+        print(json.dumps({"metric": METRIC, "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
+                          **bench_migrate(args)}), flush=True)
+        return
+    if args.workload == "l70-full":
+        from paper_2606_18600_amd.batcher import bench_l70_full
+        print(json.dumps({"metric": METRIC, "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
+                          **bench_l70_full(args, log)}), flush=True)
+        return
+
+    result = bench_default(args)
     print(json.dumps(result), flush=True)
 
 

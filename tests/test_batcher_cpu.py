@@ -99,3 +99,26 @@ def test_simulation_runs_every_request_to_completion(seed):
     assert b.finished == len(reqs)
     assert all(r.prefilled == r.prompt and r.decoded == r.out for r in reqs)
     assert sorted(b.alloc.free) == list(range(nb))
+
+
+def test_sustainable_rate_balances_prefill_with_decode():
+    """At the roofline-sustainable rate the prefill tokens of a step keep pace
+    with its decodes: P / mean_prompt requests start per step while
+    max_decodes / mean_out finish, and the rate is that count over the
+    step's Eq. 1 time."""
+    from paper_2606_18600_amd import synth
+    from paper_2606_18600_amd.batcher import lognormal_mean, sustainable_rate
+    from paper_2606_18600_amd.roofline import step_roofline_ms
+    mean_out = lognormal_mean(256, 0.8)
+    assert mean_out == pytest.approx(256 * np.exp(0.32))
+    rate, ms, P = sustainable_rate(synth.LLAMA70B, 80, 2560.0, mean_out)
+    assert P == round(128 * 2560.0 / mean_out)
+    assert P / 2560.0 == pytest.approx(128 / mean_out, rel=1e-3)
+    expect = step_roofline_ms(synth.LLAMA70B, 80, [((2560.0 - P) / 2, P)],
+                              np.full(128, 2560.0 + mean_out / 2))
+    assert ms == pytest.approx(expect)
+    assert rate == pytest.approx(128 / mean_out / (ms / 1e3), rel=1e-3)
+    # prompts so long that the budget binds: prefill-limited
+    rate2, _, P2 = sustainable_rate(synth.LLAMA70B, 80, 40000.0, 100.0)
+    assert P2 == 2048
+    assert rate2 < 128 / 100.0 / (ms / 1e3)

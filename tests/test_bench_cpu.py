@@ -64,3 +64,17 @@ def test_gpus_above_one_exit_with_a_message():
     r = subprocess.run([sys.executable, os.path.join(bench.ROOT, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, timeout=120)
     assert r.returncode != 0 and "one GPU" in r.stderr
+
+
+def test_oracle_step_timing_and_cpu_block():
+    """The CPU-baseline helpers: one step of one layer of the oracle, timed,
+    and its scaling to the stage's layers."""
+    from paper_2606_18600_amd import synth
+    sec, reps, spent = bench.oracle_layer_step(synth.TINY, [(20, 1), (0, 7), (33, 1)], 1,
+                                               budget_s=0.2)
+    assert sec > 0 and reps >= 1 and spent >= sec
+    blk = bench.cpu_block(9, 20, 0.5, 3, 1.5, "a sample")
+    assert blk["value"] == pytest.approx(9 / 10.0)
+    assert blk["kind"] == "oracle" and blk["cores"] >= 1 and "x20 layers" in blk["sample"]
+    info = bench.host_info()
+    assert info["nproc"] >= 1 and "cpu_model" in info
