@@ -257,6 +257,58 @@ stage_status stage_lm_head(stage_t* st, const void* final_norm, const void* w_lm
 stage_status stage_pack_lm_head(const stage_model_config* cfg, int32_t vocab, const void* src,
                                 void* dst, void* stream);
 
+/* ---- shared tensor store ---------------------------------------------- */
+/* The paper keeps model weights and KV-cache space in a store process that
+ * loads them once and hands them to engine processes zero-copy, so that an
+ * engine (re)starts without reloading anything (Sec. 5.2, "Shared Tensor
+ * Store"; Sec. 5.3 overlaps this with the rest of engine start-up). These
+ * calls are that hand-over on one GPU: the store allocates and exports, an
+ * engine in another process attaches and passes the pointers it gets to
+ * stage_create like any other device memory.
+ *  - Each allocation is one device allocation below STAGE_STORE_MAX_BYTES,
+ *    exported whole: a handle maps exactly one allocation from its base.
+ *    Larger tensors are split by the caller (a layer's weights are several
+ *    allocations, a KV pool can be one per layer range).
+ *  - The store owns its allocations and must keep them alive (and not free
+ *    them) while any engine is attached; engines only read weights and
+ *    write the KV blocks their own block tables name. Nothing orders work
+ *    between processes: callers synchronise (e.g. the store finishes
+ *    writing before it publishes the handles).
+ *  - Both processes need the same GPU, and the engine must be a process of
+ *    its own (a handle cannot be opened in the process that exported it). */
+#define STAGE_STORE_MAX_BYTES ((size_t)1 << 31)
+
+/* An exported allocation: opaque bytes, safe to copy between processes
+ * (e.g. hex-encoded through a pipe). */
+typedef struct {
+  unsigned char bytes[64];
+} stage_ipc_handle;
+
+/* Store side: allocate `bytes` (0 < bytes < STAGE_STORE_MAX_BYTES, else
+ * STAGE_ERR_INVALID_ARG / STAGE_ERR_CAPACITY) of zero-filled device memory on
+ * the current device and export it. *dev receives the pointer in this
+ * process, *handle what another process attaches with. Synchronous. */
+stage_status stage_store_alloc(size_t bytes, void** dev, stage_ipc_handle* handle);
+
+/* Store side: free an allocation of stage_store_alloc (NULL is allowed).
+ * Engines must have detached. */
+stage_status stage_store_free(void* dev);
+
+/* Copy `bytes` from src (device or host memory) into store memory dst,
+ * enqueued on `stream`: how a store loads tensors that need no packing
+ * (norm gains; packed projections are written by stage_pack_weight straight
+ * into store memory). */
+stage_status stage_store_write(void* dst, const void* src, size_t bytes, void* stream);
+
+/* Engine side: map an exported allocation into this process; *dev receives
+ * its address here (the base of the allocation). STAGE_ERR_DEVICE if the
+ * handle cannot be opened (wrong GPU, store gone, same process). */
+stage_status stage_store_attach(const stage_ipc_handle* handle, void** dev);
+
+/* Engine side: unmap what stage_store_attach mapped (NULL is allowed).
+ * Stages created over it must have been destroyed and their work finished. */
+stage_status stage_store_detach(void* dev);
+
 /* ---- measurement hooks ------------------------------------------------ */
 
 /* Operation classes timed by the op-timing hook. */

@@ -174,4 +174,7 @@ constexpr size_t kStaticScratchBytes = (size_t)128 << 20;
 // device. Looked up with hipGetSymbolAddress on the first call per device.
 hipError_t static_scratch(int device, void** ptr);
 
+// Set the calling thread's message for stage_last_error().
+void set_error(const char* msg);
+
 }  // namespace stage_k

@@ -76,6 +76,8 @@ struct PendingTiming {
 
 }  // namespace
 
+void stage_k::set_error(const char* msg) { g_err = msg ? msg : ""; }
+
 struct stage {
   stage_model_config cfg{};
   int32_t layer_begin = 0, n_layers = 0;

@@ -117,14 +117,19 @@ class DeviceStage:
         assert kv_pool.numel() >= numel and kv_pool.dtype == td
         self.kv_pool = kv_pool
         self.weights = list(weights)
-        layers = []
         for w in self.weights:
             for k, v in w.items():
                 assert v.is_contiguous() and v.dtype == td, k
-            layers.append(S.stage_layer_weights(
-                *[w[f].data_ptr() if f in w else None for f in WEIGHT_FIELDS]))
-        self.handle = S.stage_create(self.cfg, layer_begin, layer_begin + self.n_layers, layers,
-                                     kv_pool.data_ptr(), num_blocks, max_tokens, max_seqs)
+        ptrs = [{f: w[f].data_ptr() for f in WEIGHT_FIELDS if f in w} for w in self.weights]
+        self._create(layer_begin, ptrs, kv_pool.data_ptr(), max_tokens, max_seqs, device)
+
+    def _create(self, layer_begin: int, layer_ptrs: Sequence[Dict[str, int]], kv_ptr: int,
+                max_tokens: int, max_seqs: int, device) -> None:
+        """stage_create over device pointers, then a workspace of the size
+        the stage asks for."""
+        layers = [S.stage_layer_weights(*[w.get(f) for f in WEIGHT_FIELDS]) for w in layer_ptrs]
+        self.handle = S.stage_create(self.cfg, layer_begin, layer_begin + len(layers), layers,
+                                     kv_ptr, self.num_blocks, max_tokens, max_seqs)
         nbytes = S.stage_workspace_bytes(self.handle)
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
         S.stage_bind_workspace(self.handle, self.workspace.data_ptr(), nbytes)
@@ -195,3 +200,23 @@ class DeviceStage:
             self.close()
         except Exception:
             pass
+
+
+class PointerStage(DeviceStage):
+    """A stage over packed weights and a KV pool given as raw device
+    pointers (e.g. memory mapped from a tensor store); only the workspace is
+    allocated here."""
+
+    def __init__(self, shape: ModelShape, dtype: str, layer_begin: int,
+                 layer_ptrs: Sequence[Dict[str, int]], kv_ptr: int, num_blocks: int,
+                 max_tokens: int, max_seqs: int, max_position: int = 8192, device="cuda"):
+        self.shape, self.dtype = shape, dtype
+        self.n_layers = len(layer_ptrs)
+        self.num_blocks = num_blocks
+        self.cfg = model_config(shape, dtype, max_position)
+        self.kv_pool = None
+        self.weights = []
+        self._create(layer_begin, layer_ptrs, kv_ptr, max_tokens, max_seqs, device)
+
+    def kv_view(self) -> torch.Tensor:
+        raise RuntimeError("a stage over raw pointers has no KV tensor to view")

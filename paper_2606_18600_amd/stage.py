@@ -36,7 +36,10 @@ EXPORTED = ("stage_create", "stage_workspace_bytes", "stage_bind_workspace", "st
             "stage_decode", "stage_step_mixed", "stage_destroy", "stage_last_error",
             "stage_validate_step", "stage_set_op_timing", "stage_read_op_times",
             "stage_pack_weight", "stage_copy_probe", "stage_lm_head", "stage_pack_lm_head",
-            "stage_decode_noalloc")
+            "stage_decode_noalloc", "stage_store_alloc", "stage_store_free", "stage_store_write",
+            "stage_store_attach", "stage_store_detach")
+
+STAGE_STORE_MAX_BYTES = 1 << 31
 
 STAGE_W_QKV = 0
 STAGE_W_O = 1
@@ -64,6 +67,10 @@ class stage_layer_weights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
                 ("attn_norm", "w_qkv", "q_norm", "k_norm", "w_o", "ffn_norm", "w_gate_up",
                  "w_down")]
+
+
+class stage_ipc_handle(ctypes.Structure):
+    _fields_ = [("bytes", ctypes.c_ubyte * 64)]
 
 
 class stage_batch(ctypes.Structure):
@@ -105,6 +112,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.stage_copy_probe.argtypes = [P, P, ctypes.c_size_t, P]
     lib.stage_lm_head.argtypes = [P, P, P, i32, P, i32, ctypes.POINTER(ctypes.c_int32), i32, P, P]
     lib.stage_pack_lm_head.argtypes = [ctypes.POINTER(stage_model_config), i32, P, P, P]
+    lib.stage_store_alloc.argtypes = [ctypes.c_size_t, ctypes.POINTER(P),
+                                      ctypes.POINTER(stage_ipc_handle)]
+    lib.stage_store_free.argtypes = [P]
+    lib.stage_store_write.argtypes = [P, P, ctypes.c_size_t, P]
+    lib.stage_store_attach.argtypes = [ctypes.POINTER(stage_ipc_handle), ctypes.POINTER(P)]
+    lib.stage_store_detach.argtypes = [P]
     lib.stage_set_op_timing.argtypes = [P, i32]
     lib.stage_read_op_times.argtypes = [P, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_int64)]
@@ -112,7 +125,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                  "stage_decode_noalloc",
                  "stage_step_mixed", "stage_destroy", "stage_validate_step",
                  "stage_set_op_timing", "stage_read_op_times", "stage_pack_weight",
-                 "stage_copy_probe", "stage_lm_head", "stage_pack_lm_head"):
+                 "stage_copy_probe", "stage_lm_head", "stage_pack_lm_head", "stage_store_alloc",
+                 "stage_store_free", "stage_store_write", "stage_store_attach",
+                 "stage_store_detach"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -232,3 +247,34 @@ def stage_read_op_times(st: int) -> Tuple[list, list]:
     n = (ctypes.c_int64 * STAGE_OP_COUNT)()
     _check(load_library().stage_read_op_times(st, ms, n))
     return list(ms), list(n)
+
+
+def stage_store_alloc(nbytes: int) -> Tuple[int, bytes]:
+    """(device pointer, 64-byte IPC handle) of a new zero-filled store
+    allocation."""
+    p = ctypes.c_void_p()
+    h = stage_ipc_handle()
+    _check(load_library().stage_store_alloc(nbytes, ctypes.byref(p), ctypes.byref(h)))
+    return p.value, bytes(h.bytes)
+
+
+def stage_store_free(ptr: int) -> None:
+    _check(load_library().stage_store_free(ptr))
+
+
+def stage_store_write(dst: int, src: int, nbytes: int, stream: int = 0) -> None:
+    _check(load_library().stage_store_write(dst, src, nbytes, stream))
+
+
+def stage_store_attach(handle: bytes) -> int:
+    if len(handle) != 64:
+        raise StageError(STAGE_ERR_INVALID_ARG, f"an IPC handle has 64 bytes, got {len(handle)}")
+    h = stage_ipc_handle()
+    ctypes.memmove(h.bytes, handle, 64)
+    p = ctypes.c_void_p()
+    _check(load_library().stage_store_attach(ctypes.byref(h), ctypes.byref(p)))
+    return p.value
+
+
+def stage_store_detach(ptr: int) -> None:
+    _check(load_library().stage_store_detach(ptr))

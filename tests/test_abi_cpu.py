@@ -172,3 +172,23 @@ def test_lm_head_rejects_a_null_stage():
     lib = _lib()
     assert lib.stage_lm_head(None, 0x1000, 0x2000, 1024, 0x3000, 4, None, 4, 0x4000,
                              None) == S.STAGE_ERR_INVALID_ARG
+
+
+def test_store_host_checks():
+    """The store's argument checks need no device: empty and 2 GiB
+    allocations are refused before anything is allocated; freeing or
+    detaching NULL is a no-op."""
+    lib = _lib()
+    import ctypes
+    p = ctypes.c_void_p()
+    h = S.stage_ipc_handle()
+    assert lib.stage_store_alloc(0, ctypes.byref(p), ctypes.byref(h)) == S.STAGE_ERR_INVALID_ARG
+    assert lib.stage_store_alloc(1 << 31, ctypes.byref(p), ctypes.byref(h)) == \
+        S.STAGE_ERR_CAPACITY
+    assert "below" in S.stage_last_error()
+    assert lib.stage_store_alloc(16, None, ctypes.byref(h)) == S.STAGE_ERR_INVALID_ARG
+    assert lib.stage_store_attach(None, ctypes.byref(p)) == S.STAGE_ERR_INVALID_ARG
+    assert lib.stage_store_free(None) == S.STAGE_OK
+    assert lib.stage_store_detach(None) == S.STAGE_OK
+    with pytest.raises(S.StageError):
+        S.stage_store_attach(b"short")
