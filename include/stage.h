@@ -106,8 +106,12 @@ typedef struct {
 } stage_model_config;
 
 /* Device pointers to one layer's weights (q_norm/k_norm may be NULL unless
- * qk_norm is set). The four projections must be in the stage_pack_weight()
- * layout. */
+ * qk_norm is set). The four projections w_qkv, w_o, w_gate_up and w_down
+ * must be in the stage_pack_weight() layout (bf16 mode), not row-major:
+ * the stage cannot tell the two apart, so row-major bf16 matrices give
+ * wrong outputs without an error. Pack each matrix once, when it is loaded
+ * (stage_pack_weight can write straight into store memory). In fp32 mode
+ * the packed layout is the row-major one. Gains are plain arrays. */
 typedef struct {
   const void* attn_norm; /* [hidden] */
   const void* w_qkv;     /* [(n_q + 2 n_kv) * head_dim, hidden] */
@@ -151,7 +155,11 @@ typedef enum {
 stage_status stage_pack_weight(const stage_model_config* cfg, stage_weight_kind kind,
                                const void* src, void* dst, void* stream);
 
-/* Create a stage over layers [layer_begin, layer_end) of a model.
+/* Create a stage over layers [layer_begin, layer_end) of a model: the
+ * contiguous layer range that the paper's placement assigns to one device
+ * (Sec. 2.3, "Uneven Layer Partitioning in PP"; Algorithm 1 adds stages of
+ * l - l' consecutive layers), over weights and KV space that a store owns
+ * and the engine only references (Sec. 5.2, "Shared Tensor Store").
  *  layers:   host array of layer_end - layer_begin weight sets (device
  *            pointers, borrowed: they must outlive the stage).
  *  kv_pool:  device pointer to the KV pool (layout above), borrowed.
@@ -176,18 +184,27 @@ size_t stage_workspace_bytes(const stage_t* st);
 stage_status stage_bind_workspace(stage_t* st, void* dev, size_t bytes);
 
 /* Prefill (or chunked prefill / recomputation): every sequence has
- * q_lens >= 1 new tokens. */
+ * q_lens >= 1 new tokens. One pass of the stage's layers over the batch's
+ * rows: hidden states in, hidden states out for the next stage (Sec. 4.1.2,
+ * Eq. 2 prices exactly this B*S*H*E transfer); the compute-bound phase of
+ * Sec. 2.3 and Table 2's prefill rows. Rebuilding a migrated request's KV
+ * cache is a chunked call of this kind (Sec. 5.1, "Output-Preserving Request
+ * Migration"). */
 stage_status stage_prefill(stage_t* st, const stage_batch* batch, const void* hidden_in,
                            void* hidden_out, void* stream);
 
-/* Decode: every sequence has exactly one new token (q_lens[i] == 1). */
+/* Decode: every sequence has exactly one new token (q_lens[i] == 1): the
+ * memory-bound phase of Sec. 2.3 and Table 2's decode rows, one token per
+ * running request and step, hidden states in and out (Sec. 4.1.2, Eq. 2). */
 stage_status stage_decode(stage_t* st, const stage_batch* batch, const void* hidden_in,
                           void* hidden_out, void* stream);
 
 /* One continuous-batching step: a prefill batch (may be NULL or empty) and a
  * decode batch (may be NULL or empty) in one pass over the layers. Rows of
  * hidden_in: prefill rows first, then decode rows. A sequence must not
- * appear in both batches. */
+ * appear in both batches. This is the request mix of one engine step, whose
+ * latency the paper's estimator sums over Table 2's operations (Sec. 4.1.1,
+ * Eq. 1) and whose batch the scheduler forms (Sec. 4.2.2). */
 stage_status stage_step_mixed(stage_t* st, const stage_batch* prefill, const stage_batch* decode,
                               const void* hidden_in, void* hidden_out, void* stream);
 
