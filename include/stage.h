@@ -204,7 +204,8 @@ stage_status stage_decode(stage_t* st, const stage_batch* batch, const void* hid
  * hidden_in: prefill rows first, then decode rows. A sequence must not
  * appear in both batches. This is the request mix of one engine step, whose
  * latency the paper's estimator sums over Table 2's operations (Sec. 4.1.1,
- * Eq. 1) and whose batch the scheduler forms (Sec. 4.2.2). */
+ * Eq. 1) and whose batch size the placement optimizer bounds by memory
+ * (Sec. 4.2.2, "Batch Size Determination"). */
 stage_status stage_step_mixed(stage_t* st, const stage_batch* prefill, const stage_batch* decode,
                               const void* hidden_in, void* hidden_out, void* stream);
 
@@ -278,7 +279,8 @@ stage_status stage_pack_lm_head(const stage_model_config* cfg, int32_t vocab, co
 /* The paper keeps model weights and KV-cache space in a store process that
  * loads them once and hands them to engine processes zero-copy, so that an
  * engine (re)starts without reloading anything (Sec. 5.2, "Shared Tensor
- * Store"; Sec. 5.3 overlaps this with the rest of engine start-up). These
+ * Store"; the same section overlaps the store's loading with engine start-up,
+ * its concurrent initialization). These
  * calls are that hand-over on one GPU: the store allocates and exports, an
  * engine in another process attaches and passes the pointers it gets to
  * stage_create like any other device memory.
