@@ -18,7 +18,7 @@ OUT_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libstage.so")
 ARCH = os.environ.get("STAGE_OFFLOAD_ARCH", "gfx950")
 
-SOURCES = ["k_elem.hip", "k_gemm.hip", "k_attn.hip", "scratch.hip", "stage.cpp", "store.cpp"]
+SOURCES = ["k_elem.hip", "k_gemm.hip", "k_attn.hip", "scratch.hip", "stage.cpp", "store.cpp", "plan.cpp"]
 
 HIPCC_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17", "-Wall",

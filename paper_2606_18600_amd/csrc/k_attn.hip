@@ -335,6 +335,7 @@ constexpr int kPfBPS = 4;
 // Row tiles per wave. Four tiles per wave do not fit the register budget of
 // two waves per SIMD and measured slower, so only two are built.
 constexpr int kPfRowTiles = 2;
+static_assert(kPfWaves * kPfRowTiles * 16 == kPrefillRows, "rows of a prefill work item");
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
@@ -597,11 +598,6 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__
 
 }  // namespace
 
-int prefill_item_positions(DType dt, int group) {
-  (void)dt;
-  return kPfWaves * kPfRowTiles * 16 / group;
-}
-
 hipError_t attn_decode(DType dt, const void* q, KVLayer kv, SegTables tabs,
                        const DecodeItem* items, int n_items, int n_q, float* part_o,
                        float* part_ml, hipStream_t s) {
@@ -661,7 +657,7 @@ hipError_t attn_prefill(DType dt, const void* q, KVLayer kv, SegTables tabs,
                         hipStream_t s) {
   if (n_items == 0) return hipSuccess;
   if (dt != DT_BF16) return hipErrorInvalidValue;
-  if ((kPfWaves * kPfRowTiles * 16) % (n_q / kv.n_kv) != 0) return hipErrorInvalidValue;
+  if (kPrefillRows % (n_q / kv.n_kv) != 0) return hipErrorInvalidValue;
   dim3 grid(n_items, kv.n_kv);
   if (kv.head_dim == 128)
     launch_prefill<128, kPfRowTiles>(grid, s, q, kv, tabs, items, n_q, out);

@@ -53,7 +53,7 @@ __global__ void pack_weight_kernel(const bf16_t* __restrict__ src, bf16_t* __res
 // ---------------------------------------------------------------------------
 // bf16 split-K GEMM for decode-sized M
 // ---------------------------------------------------------------------------
-constexpr int SK_WAVES = 4;
+constexpr int SK_WAVES = kSkinnyWaves;
 
 enum SkinnyEpi { SK_PARTIAL = 0, SK_SWIGLU = 1 };
 
@@ -545,20 +545,6 @@ hipError_t pack_weight(const void* src, void* dst, int N, int K, int gate_up_ffn
   pack_weight_kernel<<<(int)blocks, 256, 0, s>>>((const bf16_t*)src, (bf16_t*)dst, N, K,
                                                  gate_up_ffn);
   return hipGetLastError();
-}
-
-int skinny_kb_len(int K, int splits) {
-  int kb = (K + splits - 1) / splits;
-  return (kb + 63) / 64 * 64;
-}
-
-int skinny_splits(int N, int K, int target_blocks, int max_splits) {
-  const int col_blocks = (N / 64 + SK_WAVES - 1) / SK_WAVES;
-  int s = std::max(1, target_blocks / col_blocks);
-  s = std::min(s, std::min(max_splits, K / 64));
-  // the number of K ranges actually launched after rounding the range up
-  const int kb = skinny_kb_len(K, s);
-  return (K + kb - 1) / kb;
 }
 
 hipError_t gemm_skinny(const void* A, const void* W, int M, int N, int K, int splits,

@@ -130,6 +130,8 @@ hipError_t copy_probe(const void* src, void* dst, size_t bytes, hipStream_t s);
 // kernel sums in a loop: a narrow QKV projection (one tensor-parallel
 // rank's heads) needs many K ranges to occupy the chip.
 constexpr int kSkinnyMaxSplits = 8;
+// Waves of a split-K decode GEMM workgroup (one 64-row weight group each).
+constexpr int kSkinnyWaves = 4;
 constexpr int kSkinnyMaxQkvSplits = 32;
 // K splits for an [M <= 128] x [N, K] decode GEMM: as many as keep the launch
 // at <= target_blocks blocks of 4 waves (at most max_splits).
@@ -163,6 +165,9 @@ hipError_t attn_f32(const float* q, KVLayer kv, SegTables tabs, const int32_t* t
                     const int32_t* tok_pos, int t_begin, int n_tok, int n_q, float* out,
                     hipStream_t s);
 
+// (position, head) rows of one prefill attention work item: 4 waves of two
+// 16-row tiles.
+constexpr int kPrefillRows = 128;
 // Positions handled by one prefill work item for a GQA group size.
 int prefill_item_positions(DType dt, int group);
 

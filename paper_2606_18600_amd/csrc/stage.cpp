@@ -143,8 +143,12 @@ stage_status check_config(const stage_model_config* c) {
     return fail(STAGE_ERR_INVALID_ARG, "config sizes must be positive");
   if (!(c->rms_eps >= 0.f) || !(c->qk_rms_eps >= 0.f) || !(c->rope_theta > 0.0))
     return fail(STAGE_ERR_INVALID_ARG, "eps must be >= 0 and rope_theta > 0");
-  if (c->dtype != STAGE_F32 && c->dtype != STAGE_BF16)
-    return fail(STAGE_ERR_UNSUPPORTED, "dtype %d not supported", (int)c->dtype);
+  // A C caller can store any integer in the enum field: read it as one.
+  static_assert(sizeof(stage_dtype) == sizeof(int32_t), "stage_dtype is a 32-bit enum");
+  int32_t dtype_raw;
+  std::memcpy(&dtype_raw, &c->dtype, sizeof dtype_raw);
+  if (dtype_raw != STAGE_F32 && dtype_raw != STAGE_BF16)
+    return fail(STAGE_ERR_UNSUPPORTED, "dtype %d not supported", (int)dtype_raw);
   if (c->block_size != kBlock)
     return fail(STAGE_ERR_UNSUPPORTED, "block_size must be %d (got %d)", kBlock, c->block_size);
   if (c->head_dim != 64 && c->head_dim != 128)
@@ -1008,12 +1012,15 @@ stage_status stage_pack_weight(const stage_model_config* cfg, stage_weight_kind 
   const int H = cfg->hidden, F = cfg->ffn, qw = cfg->n_q_heads * cfg->head_dim;
   const int qkvw = (cfg->n_q_heads + 2 * cfg->n_kv_heads) * cfg->head_dim;
   int N = 0, K = 0, ffn = 0;
-  switch (kind) {
+  static_assert(sizeof(stage_weight_kind) == sizeof(int32_t), "stage_weight_kind is 32-bit");
+  int32_t kind_raw;
+  std::memcpy(&kind_raw, &kind, sizeof kind_raw);
+  switch (kind_raw) {
     case STAGE_W_QKV: N = qkvw; K = H; break;
     case STAGE_W_O: N = H; K = qw; break;
     case STAGE_W_GATE_UP: N = 2 * F; K = H; ffn = F; break;
     case STAGE_W_DOWN: N = H; K = F; break;
-    default: return fail(STAGE_ERR_INVALID_ARG, "unknown weight kind %d", (int)kind);
+    default: return fail(STAGE_ERR_INVALID_ARG, "unknown weight kind %d", (int)kind_raw);
   }
   hipStream_t s = (hipStream_t)stream;
   hipError_t e;

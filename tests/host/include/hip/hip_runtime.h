@@ -1,0 +1,64 @@
+// Host-only stand-in for the HIP runtime header, for the sanitizer build of
+// the library's host code (tests/host/stage_host_check.cpp). It declares only
+// what stage.cpp, store.cpp and kernels.hpp use; the definitions live in the
+// check program and treat "device" memory as host memory, so AddressSanitizer
+// sees every host-side write into workspaces, staging buffers and tables.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+typedef enum hipError_t {
+  hipSuccess = 0,
+  hipErrorInvalidValue = 1,
+  hipErrorOutOfMemory = 2,
+  hipErrorInvalidDevice = 101,
+  hipErrorInvalidSymbol = 13,
+  hipErrorNoDevice = 100,
+  hipErrorUnknown = 999
+} hipError_t;
+
+typedef struct ihipStream_t* hipStream_t;
+typedef struct ihipEvent_t* hipEvent_t;
+
+typedef enum hipMemcpyKind {
+  hipMemcpyHostToHost = 0,
+  hipMemcpyHostToDevice = 1,
+  hipMemcpyDeviceToHost = 2,
+  hipMemcpyDeviceToDevice = 3,
+  hipMemcpyDefault = 4
+} hipMemcpyKind;
+
+typedef enum hipDeviceAttribute_t { hipDeviceAttributeMultiprocessorCount = 63 } hipDeviceAttribute_t;
+
+typedef struct hipIpcMemHandle_st {
+  char reserved[64];
+} hipIpcMemHandle_t;
+
+#define hipHostMallocDefault 0x0
+#define hipEventDisableTiming 0x2
+#define hipIpcMemLazyEnablePeerAccess 0x01
+
+hipError_t hipGetDeviceCount(int* count);
+hipError_t hipGetDevice(int* device);
+hipError_t hipSetDevice(int device);
+hipError_t hipDeviceGetAttribute(int* value, hipDeviceAttribute_t attr, int device);
+const char* hipGetErrorString(hipError_t e);
+hipError_t hipMalloc(void** p, size_t bytes);
+hipError_t hipFree(void* p);
+hipError_t hipHostMalloc(void** p, size_t bytes, unsigned flags);
+hipError_t hipHostFree(void* p);
+hipError_t hipMemset(void* p, int v, size_t bytes);
+hipError_t hipMemcpy(void* dst, const void* src, size_t bytes, hipMemcpyKind kind);
+hipError_t hipMemcpyAsync(void* dst, const void* src, size_t bytes, hipMemcpyKind kind,
+                          hipStream_t s);
+hipError_t hipStreamSynchronize(hipStream_t s);
+hipError_t hipEventCreate(hipEvent_t* e);
+hipError_t hipEventCreateWithFlags(hipEvent_t* e, unsigned flags);
+hipError_t hipEventRecord(hipEvent_t e, hipStream_t s);
+hipError_t hipEventSynchronize(hipEvent_t e);
+hipError_t hipEventDestroy(hipEvent_t e);
+hipError_t hipEventElapsedTime(float* ms, hipEvent_t a, hipEvent_t b);
+hipError_t hipIpcGetMemHandle(hipIpcMemHandle_t* h, void* p);
+hipError_t hipIpcOpenMemHandle(void** p, hipIpcMemHandle_t h, unsigned flags);
+hipError_t hipIpcCloseMemHandle(void* p);
