@@ -34,7 +34,30 @@ def _seq_kv(st, bt_row, n_tok):
     return out
 
 
-def _run(shape, dtype, weights, prompt, n_dec, seed, chunk, max_tokens, layer_begin=0):
+def _oracle_check(shape, dtype, w64, xs64, n, ya, yb, zb, kv_b, layer_begin):
+    """The receiver's recomputation against the oracle: one oracle prefill of
+    all n tokens from the same hidden states (its outputs and every K/V
+    entry), then the next decode step."""
+    oc = ocfg(shape)
+    L = len(w64)
+    nb = (n + 1 + 15) // 16
+    okv = O.new_kv_cache(oc, L, nb)
+    table = list(range(nb))
+    y_or = O.stage_forward(oc, w64, xs64[:n], [O.SeqSpec(0, n, table)], okv)
+    z_or = O.stage_forward(oc, w64, xs64[n:n + 1], [O.SeqSpec(n, 1, table)], okv)
+    eo = rel_l2(yb.double().cpu().numpy(), y_or)
+    ez = rel_l2(zb.double().cpu().numpy(), z_or)
+    worst = 0.0
+    for l, (kb, vb) in enumerate(kv_b):
+        k_or = okv[l]["k"].reshape(-1, *okv[l]["k"].shape[2:])[:n]
+        v_or = okv[l]["v"].reshape(-1, *okv[l]["v"].shape[2:])[:n]
+        worst = max(worst, rel_l2(kb, k_or), rel_l2(vb, v_or))
+    log(f"  against the oracle: recomputed outputs {eo:.3e}, K/V {worst:.3e}, next decode {ez:.3e}")
+    assert max(eo, ez, worst) <= TOL[dtype], (eo, ez, worst)
+
+
+def _run(shape, dtype, weights, prompt, n_dec, seed, chunk, max_tokens, layer_begin=0,
+         w64=None):
     td = torch_dtype(dtype)
     H = shape.hidden
     total = prompt + n_dec + 1
@@ -81,6 +104,26 @@ def _run(shape, dtype, weights, prompt, n_dec, seed, chunk, max_tokens, layer_be
         assert en <= TOL[dtype], ("next decode", en)
         log(f"  {shape.name} {dtype}: prompt {prompt} + {n_dec} decodes, chunk {chunk}: KV worst "
             f"{worst:.3e}, outputs {eo:.3e}, next decode {en:.3e}")
+        if w64 is not None and len(w64) == 1 and n > 1024:
+            # one model-sized layer: every rebuilt K/V row against the
+            # oracle's own projection of the hidden states (the input of
+            # the stage's only layer), row by row
+            kb, vb = _seq_kv(b, btb[0], n)[0]
+            pos = np.arange(n)
+            xs64 = xs[:n].double().cpu().numpy()
+            worst = 0.0
+            for r0 in range(0, n, 1024):
+                _, k_or, v_or = O.project_qkv(ocfg(shape), w64[0], xs64[r0:r0 + 1024],
+                                              pos[r0:r0 + 1024])
+                for g_, o_ in ((kb[r0:r0 + 1024], k_or), (vb[r0:r0 + 1024], v_or)):
+                    err = np.linalg.norm((g_ - o_).reshape(len(o_), -1), axis=1) / \
+                        np.linalg.norm(o_.reshape(len(o_), -1), axis=1)
+                    worst = max(worst, float(err.max()))
+            log(f"  against the oracle: all {n} rebuilt K/V rows, worst per-row {worst:.3e}")
+            assert worst <= TOL[dtype]
+        elif w64 is not None:
+            _oracle_check(shape, dtype, w64, xs.double().cpu().numpy(), n, ya, yb, zb,
+                          _seq_kv(b, btb[0], n), layer_begin)
     finally:
         a.close()
         b.close()
@@ -90,17 +133,21 @@ def _run(shape, dtype, weights, prompt, n_dec, seed, chunk, max_tokens, layer_be
 def test_migration_by_recomputation_tiny(dtype):
     shape, seed = synth.TINY, 2611
     w = [upload_weights(synth.host_layer_weights(shape, seed, l), dtype) for l in range(2)]
+    w64 = [to_host64(x) for x in w]
     cfg = model_config(shape, dtype)
     w = [pack_layer(cfg, x) for x in w]
-    _run(shape, dtype, w, prompt=70, n_dec=23, seed=seed, chunk=37, max_tokens=64)
+    _run(shape, dtype, w, prompt=70, n_dec=23, seed=seed, chunk=37, max_tokens=64, w64=w64)
 
 
 def test_migration_by_recomputation_l70_layer():
     shape, seed, layer = synth.LLAMA70B, 2612, 40
     cfg = model_config(shape, "bf16")
-    w = [pack_layer(cfg, device_layer_weights(shape, seed, layer, "bf16"))]
+    rm = device_layer_weights(shape, seed, layer, "bf16")
+    w64 = [to_host64(rm)]
+    w = [pack_layer(cfg, rm)]
+    del rm
     _run(shape, "bf16", w, prompt=3000, n_dec=24, seed=seed, chunk=2048, max_tokens=2048,
-         layer_begin=layer)
+         layer_begin=layer, w64=w64)
 
 
 def test_long_context_chunk_sampled():
