@@ -159,12 +159,14 @@ __global__ __launch_bounds__(256) void attn_decode_bf16(const bf16_t* __restrict
                                                         const bf16_t* __restrict__ kv, int n_kv,
                                                         SegTables tabs,
                                                         const DecodeItem* __restrict__ items,
+                                                        const int32_t* __restrict__ order,
                                                         int n_q, float* __restrict__ part_o,
                                                         float* __restrict__ part_ml) {
   const int lane = threadIdx.x & 63;
   const int kvh = blockIdx.y * 4 + (threadIdx.x >> 6);
   if (kvh >= n_kv) return;
-  const DecodeItem it = items[blockIdx.x];
+  const int idx = order[blockIdx.x];
+  const DecodeItem it = items[idx];
   const int G = n_q / n_kv;
   const int row = lane & 15;  // query head within the group
   const bool row_ok = row < G;
@@ -234,7 +236,7 @@ __global__ __launch_bounds__(256) void attn_decode_bf16(const bf16_t* __restrict
   }
 
   if (!row_ok) return;
-  const size_t ob = ((size_t)blockIdx.x * n_q + kvh * G + row);
+  const size_t ob = ((size_t)idx * n_q + kvh * G + row);
   float* po = part_o + ob * D;
 #pragma unroll
   for (int t = 0; t < D / 16; ++t)
@@ -599,17 +601,17 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__
 }  // namespace
 
 hipError_t attn_decode(DType dt, const void* q, KVLayer kv, SegTables tabs,
-                       const DecodeItem* items, int n_items, int n_q, float* part_o,
-                       float* part_ml, hipStream_t s) {
+                       const DecodeItem* items, const int32_t* order, int n_items, int n_q,
+                       float* part_o, float* part_ml, hipStream_t s) {
   if (n_items == 0) return hipSuccess;
   if (dt != DT_BF16) return hipErrorInvalidValue;
   dim3 grid(n_items, (kv.n_kv + 3) / 4);
   if (kv.head_dim == 128)
     attn_decode_bf16<128><<<grid, 256, 0, s>>>((const bf16_t*)q, (const bf16_t*)kv.base, kv.n_kv,
-                                               tabs, items, n_q, part_o, part_ml);
+                                               tabs, items, order, n_q, part_o, part_ml);
   else if (kv.head_dim == 64)
     attn_decode_bf16<64><<<grid, 256, 0, s>>>((const bf16_t*)q, (const bf16_t*)kv.base, kv.n_kv,
-                                              tabs, items, n_q, part_o, part_ml);
+                                              tabs, items, order, n_q, part_o, part_ml);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

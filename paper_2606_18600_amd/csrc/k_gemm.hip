@@ -17,6 +17,7 @@
 //   ahead; epilogues: fp32 store, residual add, SwiGLU, query RoPE.
 // * gemm_tiled_f32: plain fp32 SIMT tiles for the fp32 mode (row-major).
 #include <algorithm>
+#include <cstdlib>
 #include <type_traits>
 
 #include "common.hpp"
@@ -194,6 +195,176 @@ __global__ __launch_bounds__(SK_WAVES * 64) void gemm_skinny_bf16(const bf16_t* 
           mo[packed_a_offset(m, c, F)] = f32_to_bf16(silu_f(acc[i][j][r]) * acc[i][j + 2][r]);
         }
       }
+  }
+}
+
+// The same product for 65..128 rows with 8 waves per block: wave w streams
+// weight group w % 4 and only k tile 2t + w / 4 of each 64-wide step (4 W
+// fragments), multiplying it with all MT m-tiles of A from the shared LDS
+// ring; the two waves of a group add their sums through LDS at the end and
+// each writes half of the m-tiles. A wave's MFMA work per step is then that
+// of the 4-wave kernel at 64 rows, and a block runs two waves per SIMD. With
+// 128 rows on 4 waves (one per SIMD) the MFMAs of a step took about as long
+// as the step's loads, so the two no longer overlapped.
+constexpr int SK8_WAVES = 8;
+
+template <int MT, int EPI>
+__global__ __launch_bounds__(SK8_WAVES * 64) __attribute__((amdgpu_waves_per_eu(2)))
+void gemm_skinny8_bf16(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, int M, int N,
+                       int K, int kb_len, void* __restrict__ out) {
+  constexpr int NA = (2 * MT + SK8_WAVES - 1) / SK8_WAVES;  // A copies per wave and step
+  constexpr int SLOT = SK8_WAVES * NA;                      // fragments per ring slot
+  constexpr int WAIT = vmcnt_at_most(4 + NA);               // all but the newest step's loads
+  constexpr int H0 = MT < 4 ? MT : 4;                       // m-tiles [0, H0) end in k half 0
+  constexpr int RING = 3 * SLOT * 64;                       // u32x4 of the A ring
+  constexpr int RED = 4 * 4 * 4 * 64;                       // u32x4 of one reduction round
+  __shared__ u32x4_t lds[RING > RED ? RING : RED];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int gw = wave & 3, kh = wave >> 2;
+  const int G = N / 64;
+  const int g_raw = blockIdx.x * 4 + gw;
+  const bool live = g_raw < G;
+  const int g = live ? g_raw : G - 1;
+  const int kbeg = blockIdx.y * kb_len;
+  const int iters = (min(kb_len, K - kbeg)) / 64;  // >= 1: the grid covers K exactly
+  const int r16 = lane & 15;
+  const int KT = K / 32;
+  const bf16_t* wp = W + ((size_t)g * KT + kbeg / 32 + kh) * 4 * 512 + lane * 8;
+  const bf16_t* asrc[NA];
+#pragma unroll
+  for (int u = 0; u < NA; ++u) {
+    const int f = min(wave + SK8_WAVES * u, 2 * MT - 1);
+    asrc[u] = A + ((size_t)(f / 2) * KT + kbeg / 32 + f % 2) * 512 + lane * 8;
+  }
+
+  f32x4_t acc[MT][4];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  u32x4_t wx[4], wy[4];
+  auto load = [&](u32x4_t (&w)[4], int t) {
+    t = t < iters ? t : iters - 1;
+    const int slot = t % 3;
+#pragma unroll
+    for (int u = 0; u < NA; ++u)
+      __builtin_amdgcn_global_load_lds((const void*)(asrc[u] + (size_t)t * 2 * 512),
+                                       (lds_ptr_t)&lds[(slot * SLOT + wave + SK8_WAVES * u) * 64],
+                                       16, 0, 0);
+    const bf16_t* q = wp + (size_t)t * 8 * 512;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      w[j] = __builtin_nontemporal_load((const u32x4_t*)(q + j * 512));
+  };
+  auto compute = [&](const u32x4_t (&w)[4], int t) {
+    const int slot = t % 3;
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const u32x4_t a = lds[(slot * SLOT + i * 2 + kh) * 64 + lane];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = mfma16x16x32(a, w[j], acc[i][j]);
+    }
+  };
+  // the step loop of gemm_skinny_bf16: step t's loads are complete once only
+  // step t+1's are outstanding, and the barrier publishes the A copies
+  load(wx, 0);
+  int t = 0;
+  for (; t + 1 < iters; t += 2) {
+    load(wy, t + 1);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(WAIT);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    compute(wx, t);
+    __builtin_amdgcn_sched_barrier(0);
+    load(wx, t + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(WAIT);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    compute(wy, t + 1);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if (t < iters) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_s_barrier();
+    compute(wx, t);
+  }
+  // The ring becomes the reduction buffer: every load (the clamped ones past
+  // the end included) has landed and every wave has read its last A.
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  // round 1: k half 1 hands m-tiles [0, H0) to k half 0
+  if (kh == 1) {
+#pragma unroll
+    for (int i = 0; i < H0; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        lds[((gw * 4 + i) * 4 + j) * 64 + lane] = __builtin_bit_cast(u32x4_t, acc[i][j]);
+  }
+  __syncthreads();
+  if (kh == 0) {
+#pragma unroll
+    for (int i = 0; i < H0; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] += __builtin_bit_cast(f32x4_t, lds[((gw * 4 + i) * 4 + j) * 64 + lane]);
+  }
+  if constexpr (MT > H0) {
+    __syncthreads();
+    // round 2: k half 0 hands m-tiles [H0, MT) to k half 1
+    if (kh == 0) {
+#pragma unroll
+      for (int i = H0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          lds[((gw * 4 + i - H0) * 4 + j) * 64 + lane] = __builtin_bit_cast(u32x4_t, acc[i][j]);
+    }
+    __syncthreads();
+    if (kh == 1) {
+#pragma unroll
+      for (int i = H0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] += __builtin_bit_cast(f32x4_t, lds[((gw * 4 + i - H0) * 4 + j) * 64 + lane]);
+    }
+  }
+  if (!live) return;
+
+  // epilogue of m-tiles [0, H0) (k half 0) or [H0, MT) (k half 1), as in
+  // gemm_skinny_bf16
+  const int i0 = kh == 0 ? 0 : H0, i1 = kh == 0 ? H0 : MT;
+  if (EPI == SK_PARTIAL) {
+    float* part = (float*)out + (size_t)blockIdx.y * M * N;
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      if (i < i0 || i >= i1) continue;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = i * 16 + (lane >> 4) * 4 + r;
+        if (m >= M) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) part[(size_t)m * N + g * 64 + j * 16 + r16] = acc[i][j][r];
+      }
+    }
+  } else {
+    const int F = N / 2;
+    bf16_t* mo = (bf16_t*)out;
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      if (i < i0 || i >= i1) continue;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = i * 16 + (lane >> 4) * 4 + r;
+        if (m >= M) continue;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int c = g * 32 + j * 16 + r16;
+          mo[packed_a_offset(m, c, F)] = f32_to_bf16(silu_f(acc[i][j][r]) * acc[i][j + 2][r]);
+        }
+      }
+    }
   }
 }
 
@@ -523,11 +694,31 @@ __global__ __launch_bounds__(256) void gemm_tiled_f32(const float* __restrict__ 
   }
 }
 
+// 65..128 rows run on the 8-wave kernel unless STAGE_SKINNY8=0 (read once).
+bool skinny8_enabled() {
+  static const bool on = [] {
+    const char* v = getenv("STAGE_SKINNY8");
+    return !(v && *v && atoi(v) == 0);
+  }();
+  return on;
+}
+
 template <int MT>
 hipError_t launch_skinny(const bf16_t* a, const bf16_t* w, int M, int N, int K, int kb_len,
                          bool swiglu, void* out, hipStream_t s) {
   const int groups = N / 64;
   dim3 grid((groups + SK_WAVES - 1) / SK_WAVES, (K + kb_len - 1) / kb_len);
+  if constexpr (MT > 4) {
+    if (skinny8_enabled()) {
+      if (swiglu)
+        gemm_skinny8_bf16<MT, SK_SWIGLU><<<grid, SK8_WAVES * 64, 0, s>>>(a, w, M, N, K, kb_len,
+                                                                         out);
+      else
+        gemm_skinny8_bf16<MT, SK_PARTIAL><<<grid, SK8_WAVES * 64, 0, s>>>(a, w, M, N, K, kb_len,
+                                                                          out);
+      return hipGetLastError();
+    }
+  }
   if (swiglu)
     gemm_skinny_bf16<MT, SK_SWIGLU><<<grid, SK_WAVES * 64, 0, s>>>(a, w, M, N, K, kb_len, out);
   else

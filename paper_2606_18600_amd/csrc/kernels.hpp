@@ -148,9 +148,11 @@ hipError_t gemm_split_k(const void* A, const void* W, int M, int N, int K, int s
 hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int N, int K,
                 void* out, hipStream_t s, RopeRows rope = RopeRows{});
 
+// Decode attention: workgroup b takes item order[b] (the host's dispatch
+// order); partials are written at the item's own index.
 hipError_t attn_decode(DType dt, const void* q, KVLayer kv, SegTables tabs,
-                       const DecodeItem* items, int n_items, int n_q, float* part_o,
-                       float* part_ml, hipStream_t s);
+                       const DecodeItem* items, const int32_t* order, int n_items, int n_q,
+                       float* part_o, float* part_ml, hipStream_t s);
 hipError_t attn_merge(DType dt, const float* part_o, const float* part_ml,
                       const int32_t* tok_item_start, const int32_t* tok_rows, int n_tok, int n_q,
                       int n_kv, int head_dim, void* out, hipStream_t s);

@@ -249,9 +249,10 @@ void plan_workspace(stage* st) {
   take(st->r_part_o, max_items * qw * 4);
   take(st->r_part_ml, max_items * c.n_q_heads * 2 * 4);
   // metadata: tok_seq, tok_pos [T]; decode items [max_items][4];
-  // item_start [max_seqs + 1]; tok_rows [max_seqs]; prefill items [T + max_seqs][4]
+  // item_start [max_seqs + 1]; tok_rows [max_seqs]; prefill items [T + max_seqs][4];
+  // decode item dispatch order [max_items]
   st->meta_ints = 2 * T + 4 * max_items + 2 * (size_t)st->max_seqs + 1 +
-                  4 * (T + (size_t)st->max_seqs);
+                  4 * (T + (size_t)st->max_seqs) + max_items;
   take(st->r_meta, st->meta_ints * 4);
   take(st->r_cos, (size_t)c.max_position * (D / 2) * 4);
   take(st->r_sin, (size_t)c.max_position * (D / 2) * 4);
@@ -262,6 +263,7 @@ struct StepMeta {
   int32_t *tok_seq, *tok_pos;
   DecodeItem* ditems;
   int32_t *item_start, *tok_rows;
+  int32_t* ditem_order;  // decode items in dispatch order (longest key range first)
   PrefillItem* pitems;
   int n_ditems = 0, n_pitems = 0;
 };
@@ -277,6 +279,7 @@ StepMeta meta_view(const stage* st, int32_t* base) {
   m.item_start = base + 2 * T + 4 * max_items;
   m.tok_rows = m.item_start + st->max_seqs + 1;
   m.pitems = reinterpret_cast<PrefillItem*>(m.tok_rows + st->max_seqs);
+  m.ditem_order = reinterpret_cast<int32_t*>(m.pitems + T + st->max_seqs);
   return m;
 }
 
@@ -334,6 +337,13 @@ bool build_meta(const stage* st, const stage_batch* pf, const stage_batch* dc, S
     }
   }
   m.item_start[nd] = m.n_ditems;
+  // Dispatch the longest key ranges first (the splits of one sequence
+  // differ by at most one block, those of different sequences by up to 2x),
+  // so that the short ones fill the tail of the launch.
+  for (int i = 0; i < m.n_ditems; ++i) m.ditem_order[i] = i;
+  std::stable_sort(m.ditem_order, m.ditem_order + m.n_ditems, [&](int32_t a, int32_t b) {
+    return m.ditems[a].k1 - m.ditems[a].k0 > m.ditems[b].k1 - m.ditems[b].k0;
+  });
   return true;
 }
 
@@ -622,7 +632,7 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
           });
         if (nd > 0) {
           L(STAGE_OP_ATTN, [&] {
-            return attn_decode(dt, q, kvl, tabs, dm.ditems, hm.n_ditems, nq,
+            return attn_decode(dt, q, kvl, tabs, dm.ditems, dm.ditem_order, hm.n_ditems, nq,
                                st->at<float>(st->r_part_o), st->at<float>(st->r_part_ml), ls);
           });
           L(STAGE_OP_ATTN, [&] {

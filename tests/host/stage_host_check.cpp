@@ -176,10 +176,20 @@ hipError_t gemm(DType, Epilogue, const void*, const void*, int M, int N, int K, 
   CHECK(M >= 1 && N >= 1 && K >= 1);
   return hipSuccess;
 }
-hipError_t attn_decode(DType, const void*, KVLayer, SegTables, const DecodeItem* items, int n,
-                       int, float*, float*, hipStream_t) {
+hipError_t attn_decode(DType, const void*, KVLayer, SegTables, const DecodeItem* items,
+                       const int32_t* order, int n, int, float*, float*, hipStream_t) {
   ++g_launches;
   CHECK(n >= 1 && inside(items, (size_t)n * sizeof(DecodeItem)));
+  // the dispatch order is a permutation of the items, longest key range first
+  CHECK(inside(order, (size_t)n * 4));
+  std::vector<char> hit(n, 0);
+  for (int b = 0; b < n; ++b) {
+    CHECK(order[b] >= 0 && order[b] < n && !hit[order[b]]);
+    hit[order[b]] = 1;
+    if (b > 0)
+      CHECK(items[order[b - 1]].k1 - items[order[b - 1]].k0 >=
+            items[order[b]].k1 - items[order[b]].k0);
+  }
   for (int i = 0; i < n; ++i) {
     const DecodeItem& it = items[i];
     CHECK(it.tok >= 0 && it.tok < g_T);
