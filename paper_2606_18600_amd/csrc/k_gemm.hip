@@ -782,6 +782,16 @@ hipError_t gemm_split_k(const void* A, const void* W, int M, int N, int K, int s
   return hipGetLastError();
 }
 
+// The split-K tail of SwiGLU products (below) unless STAGE_SWIGLU_TAIL_SKINNY=0
+// (read once).
+bool swiglu_tail_skinny() {
+  static const bool on = [] {
+    const char* v = getenv("STAGE_SWIGLU_TAIL_SKINNY");
+    return !(v && *v && atoi(v) == 0);
+  }();
+  return on;
+}
+
 hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int N, int K,
                 void* out, hipStream_t s, RopeRows rope) {
   if (M == 0) return hipSuccess;
@@ -866,14 +876,27 @@ hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int
     const double c256 = cost_of(T256, M), c192 = cost_of(T192, M);
     if (c192 < cost) best = T192, cost = c192;
     if (c256 <= cost) best = T256, cost = c256;
-    // Rows past the last multiple of 256 as a launch of their own on 128 x 128
-    // tiles, when the rows before them fill whole rounds of 256-row tiles and
-    // the split beats the product on one tiling, e.g. gate-up of 2048 + 128
-    // rows at N = 57344: 7 whole rounds and a half-size one instead of 7.9
-    // rounds (-1.3% per 80-layer mixed step, A/B on one box). Where the
-    // first rows would end in a partial round of their own (2048 x 51200:
-    // 6.25 rounds) the split measured slower and is not taken.
     const int m1 = M / 256 * 256;
+    // A SwiGLU product's rows past the last multiple of 256 (at most 128 of
+    // them) on the split-K kernel with one K range and SwiGLU in its
+    // epilogue: one more pass over the weights at ~6.3 TB/s, which costs
+    // about N / 78000 rounds of 256 x 256 tiles (~5.3 TFLOP/s per CU). Taken
+    // when that beats the tilings above, e.g. gate-up at 2048 + 128 rows:
+    // -3% at N = 57344 (against the 128 x 128 tail below) and at N = 51200
+    // (against 9 partly idle m-blocks), A/B on one box.
+    if (epi == EPI_SWIGLU && m1 > 0 && m1 < M && M - m1 <= 128 && swiglu_tail_skinny() &&
+        cost_of(T256, m1) + N / 78000.0 < cost) {
+      const hipError_t e = launch(T256, 0, m1, 0, N);
+      if (e != hipSuccess) return e;
+      return gemm_skinny(a + (size_t)(m1 / 16) * (K / 32) * 512, W, M - m1, N, K, 1, true,
+                         (bf16_t*)out + (size_t)(m1 / 16) * (N / 64) * 512, s);
+    }
+    // Otherwise such rows as a launch of their own on 128 x 128 tiles, when
+    // the rows before them fill whole rounds of 256-row tiles and the split
+    // beats the product on one tiling (-1.3% per 80-layer mixed step before
+    // the split-K tail above). Where the first rows would end in a partial
+    // round of their own (2048 x 51200: 6.25 rounds) this split measured
+    // slower and is not taken.
     if (m1 > 0 && m1 < M && (long)(m1 / 256) * (N / 256) % 256 == 0) {
       const double c_split = cost_of(T256, m1) + cost_of(T128, M - m1);
       if (c_split < cost) {
