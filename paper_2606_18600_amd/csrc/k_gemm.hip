@@ -9,7 +9,10 @@
 //   streams its group's fragments (contiguous in the packed layout) with
 //   non-temporal loads, two 64-wide k steps in flight, and writes an fp32
 //   partial tile per K split; the consumer kernel sums the splits. With one
-//   split the gate-up GEMM applies SwiGLU in its epilogue.
+//   split the gate-up GEMM applies SwiGLU in its epilogue. 65-128 rows run
+//   on 8 waves (gemm_skinny8_bf16); products split over K run on 8 waves
+//   over two weight groups and four k parts (gemm_skinny_kp_bf16), which
+//   halves the number of partial planes for the same number of blocks.
 // * gemm_tiled_bf16: many rows (prefill, mixed steps), compute-bound.
 //   256 x 256 (8 waves of 64 x 128), 192 x 256 or 128 x 128 block tiles;
 //   weight fragments copied HBM -> LDS with direct loads (64-wide k steps,
@@ -368,6 +371,155 @@ void gemm_skinny8_bf16(const bf16_t* __restrict__ A, const bf16_t* __restrict__ 
   }
 }
 
+// Products split over K (splits > 1) on 8 waves as KP = 8 / GW k parts of
+// GW adjacent weight groups: wave w streams group w % GW and k tile
+// KP t + w / GW of each step t (a step covers 32 KP of K: 4 W fragments per
+// wave), multiplying it with all MT m-tiles of A from the shared LDS ring;
+// the KP waves of a group add their sums through LDS at the end, each
+// finishing MR = ceil(MT / KP) m-tiles. With two groups per block a launch
+// needs half the K ranges of the four-group kernels for the same number of
+// blocks, so the fp32 partial planes it writes, and its consumer reads,
+// halve too.
+template <int MT, int GW>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2)))
+void gemm_skinny_kp_bf16(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, int M, int N,
+                         int K, int kb_len, float* __restrict__ out) {
+  constexpr int KP = 8 / GW;
+  constexpr int AF = MT * KP;                        // A fragments per step
+  constexpr int NA = (AF + 7) / 8;                   // A copies per wave and step
+  constexpr int SLOT = 8 * NA;                       // fragments per ring slot
+  constexpr int WAIT = vmcnt_at_most(4 + NA);        // all but the newest step's loads
+  constexpr int MR = (MT + KP - 1) / KP;             // m-tiles each wave finishes
+  constexpr int RING = 3 * SLOT * 64;                // u32x4 of the A ring
+  constexpr int RED = (KP - 1) * GW * MR * 4 * 64;   // u32x4 of one reduction round
+  static_assert(GW * KP == 8, "8 waves");
+  __shared__ u32x4_t lds[RING > RED ? RING : RED];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int gw = wave % GW, kp = wave / GW;
+  const int G = N / 64;
+  const int g_raw = blockIdx.x * GW + gw;
+  const bool live = g_raw < G;
+  const int g = live ? g_raw : G - 1;
+  const int kbeg = blockIdx.y * kb_len;
+  const int iters = (min(kb_len, K - kbeg)) / (32 * KP);  // >= 1: the grid covers K exactly
+  const int r16 = lane & 15;
+  const int KT = K / 32;
+  const bf16_t* wp = W + ((size_t)g * KT + kbeg / 32 + kp) * 4 * 512 + lane * 8;
+  // A fragment f of a step is (m-tile f / KP, k tile f % KP); copies past AF
+  // re-read the last fragment into slots nobody reads
+  const bf16_t* asrc[NA];
+#pragma unroll
+  for (int u = 0; u < NA; ++u) {
+    const int f = min(wave + 8 * u, AF - 1);
+    asrc[u] = A + ((size_t)(f / KP) * KT + kbeg / 32 + f % KP) * 512 + lane * 8;
+  }
+
+  f32x4_t acc[MT][4];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  u32x4_t wx[4], wy[4];
+  // loads of step t, clamped to the last step past the end (as above)
+  auto load = [&](u32x4_t (&w)[4], int t) {
+    t = t < iters ? t : iters - 1;
+    const int slot = t % 3;
+#pragma unroll
+    for (int u = 0; u < NA; ++u)
+      __builtin_amdgcn_global_load_lds((const void*)(asrc[u] + (size_t)t * KP * 512),
+                                       (lds_ptr_t)&lds[(slot * SLOT + wave + 8 * u) * 64], 16, 0,
+                                       0);
+    const bf16_t* q = wp + (size_t)t * KP * 4 * 512;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      w[j] = __builtin_nontemporal_load((const u32x4_t*)(q + j * 512));
+  };
+  auto compute = [&](const u32x4_t (&w)[4], int t) {
+    const int slot = t % 3;
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const u32x4_t a = lds[(slot * SLOT + i * KP + kp) * 64 + lane];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = mfma16x16x32(a, w[j], acc[i][j]);
+    }
+  };
+  // the step loop of gemm_skinny_bf16
+  load(wx, 0);
+  int t = 0;
+  for (; t + 1 < iters; t += 2) {
+    load(wy, t + 1);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(WAIT);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    compute(wx, t);
+    __builtin_amdgcn_sched_barrier(0);
+    load(wx, t + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(WAIT);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    compute(wy, t + 1);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if (t < iters) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_s_barrier();
+    compute(wx, t);
+  }
+  // The ring becomes the reduction buffer once every load has landed and
+  // every wave has read its last A. Round r: the waves of k parts other than
+  // r hand m-tiles [r MR, (r + 1) MR) to the wave of k part r, which adds
+  // them in k-part order.
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < KP; ++r) {
+    if (r > 0) __syncthreads();
+    if (kp != r) {
+      const int wr = (kp < r ? kp : kp - 1) * GW + gw;
+#pragma unroll
+      for (int ii = 0; ii < MR; ++ii) {
+        if (r * MR + ii >= MT) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          lds[((wr * MR + ii) * 4 + j) * 64 + lane] = __builtin_bit_cast(u32x4_t, acc[r * MR + ii][j]);
+      }
+    }
+    __syncthreads();
+    if (kp == r) {
+#pragma unroll
+      for (int q = 0; q < KP - 1; ++q) {
+        const int wr = q * GW + gw;
+#pragma unroll
+        for (int ii = 0; ii < MR; ++ii) {
+          if (r * MR + ii >= MT) continue;
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[r * MR + ii][j] +=
+                __builtin_bit_cast(f32x4_t, lds[((wr * MR + ii) * 4 + j) * 64 + lane]);
+        }
+      }
+    }
+  }
+  if (!live) return;
+
+  // each wave stores the m-tiles it finished, as in gemm_skinny_bf16
+  float* part = out + (size_t)blockIdx.y * M * N;
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    if (i / MR != kp) continue;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = i * 16 + (lane >> 4) * 4 + r;
+      if (m >= M) continue;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) part[(size_t)m * N + g * 64 + j * 16 + r16] = acc[i][j][r];
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // bf16 tiled GEMM (prefill / mixed)
 // ---------------------------------------------------------------------------
@@ -704,6 +856,16 @@ bool skinny8_enabled() {
 }
 
 template <int MT>
+hipError_t launch_skinny_kp(const bf16_t* a, const bf16_t* w, int M, int N, int K, int kb_len,
+                            int splits, void* out, hipStream_t s) {
+  const int groups = N / 64;
+  dim3 grid((groups + kSkinnyKpGroups - 1) / kSkinnyKpGroups, splits);
+  gemm_skinny_kp_bf16<MT, kSkinnyKpGroups><<<grid, 512, 0, s>>>(a, w, M, N, K, kb_len,
+                                                                 (float*)out);
+  return hipGetLastError();
+}
+
+template <int MT>
 hipError_t launch_skinny(const bf16_t* a, const bf16_t* w, int M, int N, int K, int kb_len,
                          bool swiglu, void* out, hipStream_t s) {
   const int groups = N / 64;
@@ -743,10 +905,24 @@ hipError_t gemm_skinny(const void* A, const void* W, int M, int N, int K, int sp
   if (M == 0) return hipSuccess;
   if (M > 128 || N % 64 != 0 || K % 64 != 0 || splits < 1 || (swiglu && splits != 1))
     return hipErrorInvalidValue;
-  const int kb = skinny_kb_len(K, splits);
-  if ((K + kb - 1) / kb != splits) return hipErrorInvalidValue;  // every split must be non-empty
   const bf16_t* a = (const bf16_t*)A;
   const bf16_t* w = (const bf16_t*)W;
+  if (skinny_kp_used(K, splits, swiglu)) {
+    const int kb = skinny_kp_kb_len(K, splits);
+    if ((K + kb - 1) / kb != splits) return hipErrorInvalidValue;  // every split non-empty
+    switch ((M + 15) / 16) {
+      case 1: return launch_skinny_kp<1>(a, w, M, N, K, kb, splits, out, s);
+      case 2: return launch_skinny_kp<2>(a, w, M, N, K, kb, splits, out, s);
+      case 3: return launch_skinny_kp<3>(a, w, M, N, K, kb, splits, out, s);
+      case 4: return launch_skinny_kp<4>(a, w, M, N, K, kb, splits, out, s);
+      case 5: return launch_skinny_kp<5>(a, w, M, N, K, kb, splits, out, s);
+      case 6: return launch_skinny_kp<6>(a, w, M, N, K, kb, splits, out, s);
+      case 7: return launch_skinny_kp<7>(a, w, M, N, K, kb, splits, out, s);
+      default: return launch_skinny_kp<8>(a, w, M, N, K, kb, splits, out, s);
+    }
+  }
+  const int kb = skinny_kb_len(K, splits);
+  if ((K + kb - 1) / kb != splits) return hipErrorInvalidValue;  // every split must be non-empty
   switch ((M + 15) / 16) {
     case 1: return launch_skinny<1>(a, w, M, N, K, kb, swiglu, out, s);
     case 2: return launch_skinny<2>(a, w, M, N, K, kb, swiglu, out, s);

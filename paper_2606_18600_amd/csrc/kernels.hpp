@@ -137,6 +137,18 @@ constexpr int kSkinnyMaxQkvSplits = 32;
 // at <= target_blocks blocks of 4 waves (at most max_splits).
 int skinny_splits(int N, int K, int target_blocks, int max_splits = kSkinnyMaxSplits);
 int skinny_kb_len(int K, int splits);
+// Products split over K (splits > 1, K % 128 == 0, no SwiGLU) run on the
+// k-part kernel: 8 waves on kSkinnyKpGroups weight groups, K ranges a
+// multiple of 128, so a launch has half the K ranges of the four-group
+// kernels for the same number of blocks. STAGE_SKINNY_KP=0 turns it off
+// (read once).
+constexpr int kSkinnyKpGroups = 2;
+bool skinny_kp_enabled();
+bool skinny_kp_used(int K, int splits, bool swiglu);
+int skinny_kp_kb_len(int K, int splits);
+// K splits for the k-part kernel: as many as keep the launch at
+// <= target_blocks blocks (at most max_splits).
+int skinny_kp_splits(int N, int K, int target_blocks, int max_splits = kSkinnyMaxSplits);
 hipError_t gemm_skinny(const void* A, const void* W, int M, int N, int K, int splits, bool swiglu,
                        void* out, hipStream_t s);
 // bf16 LDS-tiled product split over K: `splits` fp32 partial planes

@@ -775,10 +775,17 @@ stage_status stage_create(const stage_model_config* cfg, int32_t layer_begin, in
     const int blocks = std::max(1, env_int("STAGE_SKINNY_BLOCKS", cus * 9 / 10));
     const int H = cfg->hidden, F = cfg->ffn, qw = cfg->n_q_heads * cfg->head_dim;
     const int qkvw = (cfg->n_q_heads + 2 * cfg->n_kv_heads) * cfg->head_dim;
-    st->s_qkv = skinny_splits(qkvw, H, blocks, kSkinnyMaxQkvSplits);
-    st->s_o = skinny_splits(H, qw, blocks);
-    st->s_gu = skinny_splits(2 * F, H, blocks);
-    st->s_down = skinny_splits(H, F, blocks);
+    // products the k-part kernel takes (K % 128 == 0) are planned for it:
+    // one block per CU
+    const int kp_blocks = std::max(1, env_int("STAGE_SKINNY_KP_BLOCKS", cus));
+    auto splits_for = [&](int N, int K, int max_splits) {
+      return skinny_kp_enabled() && K % 128 == 0 ? skinny_kp_splits(N, K, kp_blocks, max_splits)
+                                                 : skinny_splits(N, K, blocks, max_splits);
+    };
+    st->s_qkv = splits_for(qkvw, H, kSkinnyMaxQkvSplits);
+    st->s_o = splits_for(H, qw, kSkinnyMaxSplits);
+    st->s_gu = splits_for(2 * F, H, kSkinnyMaxSplits);
+    st->s_down = splits_for(H, F, kSkinnyMaxSplits);
     st->attn_waves = std::max(64, env_int("STAGE_ATTN_WAVES", 1600));
     st->row_tail_on = env_int("STAGE_ROW_TAIL", 1) != 0;
     st->q_rope_fused = env_int("STAGE_Q_ROPE", 1) != 0;

@@ -160,7 +160,8 @@ hipError_t gemm_skinny(const void*, const void*, int M, int N, int K, int splits
   ++g_launches;
   CHECK(M >= 1 && M <= 128 && N % 64 == 0 && K % 64 == 0 && splits >= 1);
   CHECK(!swiglu || splits == 1);
-  const int kb = skinny_kb_len(K, splits);
+  const int kb = skinny_kp_used(K, splits, swiglu) ? skinny_kp_kb_len(K, splits)
+                                                   : skinny_kb_len(K, splits);
   CHECK((K + kb - 1) / kb == splits);
   return hipSuccess;
 }
