@@ -771,8 +771,10 @@ __global__ __launch_bounds__(WM * WN * 64, 512 / (WM * WN * 64)) void gemm_tiled
       for (int gi = 0; gi < TG; ++gi) {
         const int g = g0 + wn * TG + gi;
         if (EPI == EPI_SWIGLU) {
-          // tiles 0,1: gate columns 32g..32g+31; tiles 2,3: the matching up columns
-          const int F = N / 2;
+          // tiles 0,1: gate columns 32g..32g+31; tiles 2,3: the matching up columns;
+          // F from ldo, the whole product's width (so a launch may also cover
+          // only its first columns)
+          const int F = ldo / 2;
 #pragma unroll
           for (int j = 0; j < 2; ++j) {
             const int c = g * 32 + j * 16 + r16;
