@@ -27,7 +27,7 @@ import pytest
 
 from paper_2606_18600_amd import synth
 from tests.gpu_pair import Pair, log
-from tests.helpers import rel_l2, strong_weights
+from tests.helpers import rel_l2, seqs_from, strong_weights
 
 pytestmark = pytest.mark.gpu
 
@@ -58,6 +58,13 @@ GROUP_SHAPES = [
 def strong_pair(shape, dtype, n_layers, num_blocks, max_tokens, max_seqs, seed) -> Pair:
     w = [strong_weights(shape, seed, l) for l in range(n_layers)]
     return Pair(shape, dtype, n_layers, num_blocks, max_tokens, max_seqs, seed, host_weights=w)
+
+
+def strong_pair_pos(shape, dtype, n_layers, num_blocks, max_tokens, max_seqs, seed,
+                    max_position) -> Pair:
+    w = [strong_weights(shape, seed, l) for l in range(n_layers)]
+    return Pair(shape, dtype, n_layers, num_blocks, max_tokens, max_seqs, seed, host_weights=w,
+                max_position=max_position)
 
 
 def check(tag, y, yr, x, dtype):
@@ -263,6 +270,79 @@ def test_strong_long_context_decode_splits():
                                    synth.hidden_states(seed, 100 + step, 3, shape.hidden))
             check(f"decode {step}", y, yr, x, dtype)
         check_kv(pair, dtype)
+    finally:
+        pair.close()
+
+
+def test_strong_decode_at_the_split_cap_and_far_positions():
+    """Decodes at positions 200000 and 131071 (rotary table of 200064
+    positions) and 5: the two long contexts take the most key splits a
+    sequence may have (32, each over ~390 blocks), which the merge combines
+    in eight chunks of four.
+
+    The contexts are written into the pool directly and copied into the
+    oracle's cache, so the oracle runs only the decode tokens: keys
+    N(0, 0.5^2) and values N(0, 1), except six keys per long context, spread
+    over its splits, set along the direction of the token's own queries (the
+    oracle's, from the same input) with scores of 11 to 15 against a
+    background summing to ~e^12, and values of +-4. The attention output is
+    then a specific mix of those six values and the background, which a
+    dropped or mis-weighted split, or a wrong position, would change."""
+    import torch
+    from oracle import stage_oracle as O
+    from tests.gpu_pair import gpu_kv_to_oracle_layout, kv_plane_index
+    seed, shape, dtype = 2690, QWEN_SMALL, "bf16"
+    log("[test] strong decode at the split cap, positions up to 200000")
+    ctx = np.array([200000, 131071, 5], np.int32)
+    nb = (ctx + 1 + 15) // 16
+    nblocks = int(nb.sum()) + 8
+    alloc = synth.BlockAllocator(nblocks, seed)
+    bt = synth.make_block_tables(ctx + 1, int(nb.max()), alloc)
+    pair = strong_pair_pos(shape, dtype, 1, nblocks, 16, 4, seed, max_position=200064)
+    try:
+        d = shape.head_dim
+        pool = pair.gpu.kv_view()                       # [L][nb][nkv][2][16][d]
+        flat = pool.view(pool.shape[0], pool.shape[1], pool.shape[2], 2, -1)
+        g = torch.Generator(device="cuda")
+        g.manual_seed(seed)
+        flat[:, :, :, 0].normal_(0.0, 0.5, generator=g)
+        flat[:, :, :, 1].normal_(0.0, 1.0, generator=g)
+        # the decode tokens' queries, as the oracle forms them
+        xin = synth.hidden_states(seed, 1, 3, shape.hidden)
+        x64 = torch.from_numpy(xin).to(torch.bfloat16).to(torch.float64).numpy()
+        q, _, _ = O.project_qkv(pair.cfg, pair.w64[0], x64, ctx.astype(np.int64))
+        ki, vi = kv_plane_index(16, d)
+        rng = np.random.default_rng(seed)
+        for s in range(2):
+            u = q[s].mean(axis=0)
+            u /= np.linalg.norm(u)
+            proj = float(np.mean(q[s] @ u)) / np.sqrt(d)  # mean score per unit of key length
+            for f, t in zip((0.03, 0.2, 0.41, 0.6, 0.79, 0.97), (14.0, 13.0, 12.0, 15.0, 11.0, 13.5)):
+                p = int(f * ctx[s])
+                blk, o = int(bt[s][p // 16]), p % 16
+                kvec = torch.tensor(u * (t / proj), dtype=torch.bfloat16, device="cuda")
+                vvec = torch.tensor(4.0 * rng.choice([-1.0, 1.0], d), dtype=torch.bfloat16,
+                                    device="cuda")
+                flat[0, blk, 0, 0, torch.from_numpy(ki[o]).cuda()] = kvec
+                flat[0, blk, 0, 1, torch.from_numpy(vi[o]).cuda()] = vvec
+        torch.cuda.synchronize()
+        cache = gpu_kv_to_oracle_layout(pool)
+        for l, c in enumerate(cache):
+            pair.okv[l]["k"][...] = c["k"]
+            pair.okv[l]["v"][...] = c["v"]
+        del cache
+        y, yr, x = pair.decode(ctx, bt, xin)
+        check("decode", y, yr, x, dtype)
+        check_kv(pair, dtype)
+        # the bar sees a single key: with the strongest planted key of the
+        # first sequence (in its 20th of 32 splits) zeroed in the oracle's
+        # cache, the oracle's output moves far past the tolerance
+        p = int(0.6 * ctx[0])
+        pair.okv[0]["k"][int(bt[0][p // 16]), p % 16] = 0.0
+        yr2 = O.stage_forward(pair.cfg, pair.w64, x, seqs_from(ctx, [1, 1, 1], bt), pair.okv)
+        moved = rel_l2(yr2[0], yr[0])
+        log(f"  oracle output with one planted key removed moves by {moved:.3e}")
+        assert moved > 10 * TOL[dtype], moved
     finally:
         pair.close()
 
