@@ -348,6 +348,73 @@ def test_strong_decode_at_the_split_cap_and_far_positions():
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_strong_prefill_chunk_behind_a_long_planted_context(dtype):
+    """A 300-token chunk behind 29995 cached tokens (prefill items of 16
+    positions, key stages over the whole context, the causal boundary inside
+    the chunk) next to a 40-token chunk behind 7 tokens, in one call. The
+    cached context is written into the pool directly (keys N(0, 0.5^2),
+    values N(0, 1)) and copied into the oracle's cache; eight keys spread
+    over it are set along the mean direction of the long chunk's queries with
+    scores of 6 to 13 (values +-4), so every query row weighs them
+    differently against the background and a key range read wrongly shows."""
+    import torch
+    from oracle import stage_oracle as O
+    from tests.gpu_pair import gpu_kv_to_oracle_layout, kv_plane_index
+    seed, shape = 2700, QWEN_SMALL
+    log(f"[test] strong prefill chunk behind a long planted context dtype={dtype}")
+    pc = np.array([29995, 7], np.int32)
+    pq = np.array([300, 40], np.int32)
+    nb = (pc + pq + 15) // 16
+    nblocks = int(nb.sum()) + 8
+    alloc = synth.BlockAllocator(nblocks, seed)
+    bt = synth.make_block_tables(pc + pq, int(nb.max()), alloc)
+    pair = strong_pair_pos(shape, dtype, 1, nblocks, 512, 4, seed, max_position=32768)
+    try:
+        d = shape.head_dim
+        pool = pair.gpu.kv_view()
+        flat = pool.view(pool.shape[0], pool.shape[1], pool.shape[2], 2, -1)
+        g = torch.Generator(device="cuda")
+        g.manual_seed(seed)
+        flat[:, :, :, 0].normal_(0.0, 0.5, generator=g)
+        flat[:, :, :, 1].normal_(0.0, 1.0, generator=g)
+        xin = synth.hidden_states(seed, 1, int(pq.sum()), shape.hidden)
+        x64 = torch.from_numpy(xin).to(pair.td).to(torch.float64).numpy()
+        pos = np.arange(pc[0], pc[0] + pq[0], dtype=np.int64)
+        q, _, _ = O.project_qkv(pair.cfg, pair.w64[0], x64[:pq[0]], pos)
+        u = q.reshape(-1, d).mean(axis=0)
+        u /= np.linalg.norm(u)
+        proj = float(np.mean(q.reshape(-1, d) @ u)) / np.sqrt(d)
+        ki, vi = kv_plane_index(16, d)
+        rng = np.random.default_rng(seed)
+        for f, t in zip(np.linspace(0.02, 0.98, 8), (6.0, 13.0, 8.0, 11.0, 7.0, 12.0, 9.0, 10.0)):
+            p = int(f * pc[0])
+            blk, o = int(bt[0][p // 16]), p % 16
+            flat[0, blk, 0, 0, torch.from_numpy(ki[o]).cuda()] = torch.tensor(
+                u * (t / proj), dtype=flat.dtype, device="cuda")
+            flat[0, blk, 0, 1, torch.from_numpy(vi[o]).cuda()] = torch.tensor(
+                4.0 * rng.choice([-1.0, 1.0], d), dtype=flat.dtype, device="cuda")
+        torch.cuda.synchronize()
+        cache = gpu_kv_to_oracle_layout(pool)
+        for l, c in enumerate(cache):
+            pair.okv[l]["k"][...] = c["k"]
+            pair.okv[l]["v"][...] = c["v"]
+        del cache
+        y, yr, x = pair.prefill(pq, pc, bt, xin)
+        check("chunk", y, yr, x, dtype)
+        check_kv(pair, dtype)
+        # the bar sees a single key: with the strongest planted key zeroed in
+        # the oracle's cache, the long chunk's rows move far past it
+        p = int(np.linspace(0.02, 0.98, 8)[1] * pc[0])
+        pair.okv[0]["k"][int(bt[0][p // 16]), p % 16] = 0.0
+        yr2 = O.stage_forward(pair.cfg, pair.w64, x, seqs_from(pc, pq, bt), pair.okv)
+        moved = rel_l2(yr2[:pq[0]], yr[:pq[0]])
+        log(f"  oracle output with one planted key removed moves by {moved:.3e}")
+        assert moved > 10 * TOL[dtype], moved
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("shape", GROUP_SHAPES, ids=[s.name for s in GROUP_SHAPES])
 def test_strong_gqa_group_sizes(dtype, shape):
     """Every accepted GQA group size at both head dims: a ragged prefill
