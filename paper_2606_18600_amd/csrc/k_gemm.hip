@@ -739,13 +739,31 @@ __global__ __launch_bounds__(WM * WN * 64, 512 / (WM * WN * 64)) void gemm_tiled
   if constexpr (EPI == EPI_ROPE_Q) {
     // The wave's two groups are the 128 columns of one head, so both members
     // of each rotate-half pair (jj, jj + 64) are in this lane: tile j of the
-    // first group and tile j of the second.
+    // first group and tile j of the second. With a gain (Qwen3's q RMSNorm)
+    // each row is first normalised over the head: the lane's 8 values of the
+    // row, then the 16 lanes holding the same rows (lanes 16 q .. 16 q + 15).
     static_assert(TG == 2, "one 128-column head per wave");
     const int hc = (g0 + wn * TG) * 64;  // the head's first column
+    const bf16_t* qg = (const bf16_t*)rope.gain;
+    float ga[4], gb[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      ga[j] = qg ? bf16_to_f32(qg[j * 16 + r16]) : 1.f;
+      gb[j] = qg ? bf16_to_f32(qg[64 + j * 16 + r16]) : 1.f;
+    }
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
+        float rs = 1.f;
+        if (qg) {  // every lane takes part in the shuffles, padding rows too
+          float ss = 0.f;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) ss += acc[i][j][r] * acc[i][j][r];
+#pragma unroll
+          for (int o = 1; o < 16; o <<= 1) ss += __shfl_xor(ss, o, 64);
+          rs = 1.0f / sqrtf(ss / 128.0f + rope.eps);
+        }
         const int m = (mt0 + wm * TM + i) * 16 + (lane >> 4) * 4 + r;
         if (m >= M) continue;
         const size_t pr = (size_t)rope.pos[m] * 64;
@@ -753,7 +771,7 @@ __global__ __launch_bounds__(WM * WN * 64, 512 / (WM * WN * 64)) void gemm_tiled
         for (int j = 0; j < 4; ++j) {
           const int jj = j * 16 + r16;
           const float c = rope.cos_tab[pr + jj], sn = rope.sin_tab[pr + jj];
-          const float a = acc[i][j][r], b = acc[i][4 + j][r];
+          const float a = acc[i][j][r] * rs * ga[j], b = acc[i][4 + j][r] * rs * gb[j];
           bf16_t* o = (bf16_t*)out + (size_t)m * ldo + hc + jj;
           o[0] = f32_to_bf16(a * c - b * sn);
           o[64] = f32_to_bf16(a * sn + b * c);

@@ -26,6 +26,8 @@ struct RopeRows {
   const int32_t* pos = nullptr;
   const float* cos_tab = nullptr;
   const float* sin_tab = nullptr;
+  const void* gain = nullptr;  // q RMSNorm gain [d] (bf16) before RoPE, or none
+  float eps = 0.f;
 };
 
 // Block tables of the (at most) two segments of a step: sequences

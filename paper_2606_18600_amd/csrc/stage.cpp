@@ -108,6 +108,7 @@ struct stage {
   bool attn_scale = true;  // more decode attention waves for batches above 64
   bool row_tail_on = true;  // split-K skinny products for the last rows of large steps
   bool q_rope_fused = true;  // RoPE in the epilogue of a step's query product (when possible)
+  bool q_norm_fused = true;  // ... also after a q RMSNorm (q/k-norm models)
   bool check_tables = false;  // copy block tables to the host and check ids (STAGE_DEBUG)
 
   uint64_t uid = 0;        // distinct for every stage created in the process
@@ -565,9 +566,11 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
   const int ro = row_tail_for(st, T, rt, H) ? rt : 0, rd = ro;
   const int Tq = T - rq, To = T - ro, Td = T - rd;  // rows of each product on tiles
   const int kv_splits = skinny ? 0 : qkv_kv_splits(st, Tq);
-  // with split key/value columns the query product applies RoPE in its
-  // epilogue (one 128-column head per wave) unless q/k RMSNorm comes first
-  const bool q_fused = kv_splits > 0 && !c.qk_norm && D == 128 && nq % 4 == 0 &&
+  // with split key/value columns the query product applies RoPE (after the
+  // q RMSNorm of q/k-norm models) in its epilogue (one 128-column head per
+  // wave)
+  const bool q_fused = kv_splits > 0 && (!c.qk_norm || st->q_norm_fused) && D == 128 &&
+                       nq % 4 == 0 &&
                        st->q_rope_fused;
   const int mq = rt ? 0 : mid_splits(st, T, qkvw, H), mo = rt ? 0 : mid_splits(st, T, H, qw),
             md = rt ? 0 : mid_splits(st, T, H, F);
@@ -613,7 +616,8 @@ stage_status run_step(stage* st, const stage_batch* pf, const stage_batch* dc, c
         if (q_fused)
           L(STAGE_OP_QKV, [&] {
             return gemm(dt, EPI_ROPE_Q, h, w.w_qkv, Tq, qw, H, q, ls,
-                        RopeRows{dm.tok_pos, cos_t, sin_t});
+                        RopeRows{dm.tok_pos, cos_t, sin_t, c.qk_norm ? w.q_norm : nullptr,
+                                 c.qk_rms_eps});
           });
         else
           L(STAGE_OP_QKV, [&] { return gemm(dt, EPI_STORE_F32, h, w.w_qkv, Tq, qw, H, qkv, ls); });
@@ -800,6 +804,7 @@ stage_status stage_create(const stage_model_config* cfg, int32_t layer_begin, in
     st->attn_scale = env_int("STAGE_ATTN_SCALE", 1) != 0;
     st->row_tail_on = env_int("STAGE_ROW_TAIL", 1) != 0;
     st->q_rope_fused = env_int("STAGE_Q_ROPE", 1) != 0;
+    st->q_norm_fused = env_int("STAGE_Q_NORM_EPI", 1) != 0;
     st->check_tables = env_int("STAGE_DEBUG", 0) != 0;
   }
   st->max_ditems = cfg->dtype == STAGE_BF16

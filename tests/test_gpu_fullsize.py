@@ -346,11 +346,17 @@ def test_l70_bench_prefill_schedule_sampled():
         st.close()
 
 
-def test_q32_mixed_step_sampled():
+@pytest.mark.parametrize("gain_std", [0.02, 0.5], ids=["workload-gains", "wide-gains"])
+def test_q32_mixed_step_sampled(gain_std):
+    """The Qwen3-32B mixed step at its launch configuration. Its 2048 prefill
+    rows take the query product with q RMSNorm and RoPE in the epilogue; with
+    norm gains 1 + N(0, 0.5^2) (instead of the workload's 1 + N(0, 0.02^2))
+    a gain applied to the wrong columns, or not at all, moves the queries by
+    tens of percent."""
     seed, shape, layer = 24, synth.QWEN32B, 24
-    log("qwen3-32b mixed step, one layer: 4 x 512 prefill + 128 decodes")
+    log(f"qwen3-32b mixed step, one layer: 4 x 512 prefill + 128 decodes, gain std {gain_std}")
     cfg = model_config(shape, "bf16")
-    w = device_layer_weights(shape, seed, layer, "bf16")
+    w = device_layer_weights(shape, seed, layer, "bf16", gain_std=gain_std)
     w64 = _host64(w)
     pc = np.array([0, 512, 1024, 1536], np.int32)
     pq = np.full(4, 512, np.int32)
