@@ -107,6 +107,7 @@ def bench_q32_mixed(args):
     torch.cuda.empty_cache()
     chunks = list(zip(pc.tolist(), pq.tolist()))
     roof = float(np.mean([step_roofline_ms(shape, nL, chunks, c) for c in ctx_timed]))
+    est_in = {"shape": shape, "n_layers": nL, "chunks": chunks, "dec_ctx": ctx_timed}
     # dominant kernel: the gate-up + SwiGLU product of the 2176-row step
     j = S.OP_NAMES.index("gate_up")
     gu_us = op_ms[j] / op_n[j] * 1e3
@@ -137,6 +138,7 @@ def bench_q32_mixed(args):
         res["cpu_baseline"] = cpu_block(2048 + 128, nL, sec, reps, spent,
                                         "one mixed step (4 x 512 prefill + 128 decode tokens; "
                                         "value counts both)")
+    res["_est"] = est_in
     return res
 
 
@@ -263,6 +265,50 @@ def bench_full_model(args):
     return res
 
 
+def estimator_check(args, result, configs, est_blocks):
+    """The static latency estimator (Sec. 4.1.1: Eq. 1 with a one-time
+    calibration, plus the per-launch cost) against the steps this run just
+    measured: the Llama-70B-shaped decode step and chunked prefill run, and
+    the Qwen3-32B-shaped mixed step. The calibration is measured here, on
+    the same GPU, with the gate-up projection of a one-layer stage."""
+    from paper_2606_18600_amd import estimator as E
+    from paper_2606_18600_amd import synth
+    t0 = time.time()
+    cal = E.calibrate(synth.LLAMA70B, args.seed, log=log)
+    out = {"calibration": {"tflops": round(cal.tflops, 1), "gbs": round(cal.gbs, 1),
+                           "launch_us": round(cal.launch_us, 2),
+                           "seconds": round(time.time() - t0, 1)}}
+    rows = []
+
+    def row(name, pred, meas):
+        rows.append((pred, meas))
+        out[name] = {"predicted_ms": round(pred, 3), "measured_ms": round(meas, 3),
+                     "error_pct": round(100.0 * (pred - meas) / meas, 2)}
+
+    l70, q32 = est_blocks
+    if l70 is not None:
+        sh, nL = l70["shape"], l70["n_layers"]
+        launches = E.step_launches(nL, "decode") * cal.launch_us * 1e-3
+        pred = float(np.mean([step_roofline_ms(sh, nL, [], c, cal.tflops, cal.gbs)
+                              for c in l70["dec_ctx"]])) + launches
+        row("l70_decode_step", pred, result["ms_per_step"])
+        if "prefill_steps" in l70 and "prefill" in result:
+            pred = sum(step_roofline_ms(sh, nL, stp, [], cal.tflops, cal.gbs)
+                       + E.step_launches(nL, "prefill") * cal.launch_us * 1e-3
+                       for stp in l70["prefill_steps"])
+            row("l70_prefill_run", pred, result["prefill"]["ms_total"])
+    if q32 is not None:
+        sh, nL = q32["shape"], q32["n_layers"]
+        launches = E.step_launches(nL, "prefill") * cal.launch_us * 1e-3
+        pred = float(np.mean([step_roofline_ms(sh, nL, q32["chunks"], c, cal.tflops, cal.gbs)
+                              for c in q32["dec_ctx"]])) + launches
+        row("q32_mixed_step", pred, configs["c4_q32_mixed"]["ms_per_step"])
+    if rows:
+        out["mape_pct"] = round(E.mape([p for p, _ in rows], [m for _, m in rows]), 2)
+    log(f"[bench] estimator: {out}")
+    return out
+
+
 def bench_default(args):
     """One line for all five configurations: the metric's workload (the
     20-layer Llama-3.1-70B-shaped decode, batch 64) as `value`, the chunked
@@ -289,6 +335,12 @@ def bench_default(args):
                   "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
                   "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
                   "config": {"workload": "partial run (--only)"}}
+    if not args.no_estimator and ("c2" in only or "c4" in only):
+        est_blocks = [result.pop("_est", None)] + [configs.get("c4_q32_mixed", {}).pop("_est", None)]
+        result["estimator"] = estimator_check(args, result, configs, est_blocks)
+    for c in configs.values():
+        c.pop("_est", None)
+    result.pop("_est", None)
     cal = calibrate(torch, S, stream)
     if "c2" in only:
         cal["gate_up_frac_of_copy"] = round(gu_gbs / cal["copy_GBs"], 4)
@@ -890,6 +942,7 @@ def bench_l70_stage(args):
         "ops_ms_per_step": {k: round(v["ms_per_step"], 4) for k, v in ops.items()},
     }
     result["roofline"]["traffic_note"] = traffic_note
+    result["_est"] = {"shape": shape, "n_layers": nL, "dec_ctx": ctx_timed}
 
     steps = []
     if not args.no_prefill:
@@ -936,6 +989,7 @@ def bench_l70_stage(args):
             "ops_ms": {S.OP_NAMES[k]: round(op_ms[k], 3) for k in range(len(op_ms))},
             "gate_up_tflops": round(gu_tfs, 1),
         }
+        result["_est"]["prefill_steps"] = [[(c, q) for _, c, q in stp] for stp in steps]
         log(f"[bench] prefill {pms:.1f} ms, {ptok / (pms / 1e3):.0f} tok/s, "
             f"{pfl / (pms / 1e3) / 1e12:.0f} TFLOP/s; gate_up {gu_tfs:.0f} TFLOP/s")
 
@@ -964,6 +1018,8 @@ def main():
     ap.add_argument("--seed", type=int, default=2606)
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-estimator", action="store_true",
+                    help="default run: skip the estimator's check against the measured steps")
     ap.add_argument("--only", default="",
                     help="default run: comma-separated subset of c1,c2,c4,c5 (c2 includes the "
                          "prefill, c3)")
@@ -1001,9 +1057,11 @@ def main():
         sys.exit(2)
 
     if args.workload == "q32-mixed":
+        res = bench_q32_mixed(args)
+        res.pop("_est", None)
         print(json.dumps({"metric": METRIC, "n_gpus": 1, "steps": args.steps,
                           "warmup": args.warmup, "dtype": "bf16", "data": "synthetic",
-                          **bench_q32_mixed(args)}), flush=True)
+                          **res}), flush=True)
         return
     if args.workload == "lm-head":
         print(json.dumps({"metric": METRIC, "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
