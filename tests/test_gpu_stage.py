@@ -417,3 +417,53 @@ def test_stage_composition(dtype):
         whole.close()
         first.close()
         second.close()
+
+
+@pytest.mark.parametrize("shape", [synth.TINY, QWEN_SMALL], ids=["tiny", "qwen-small"])
+def test_two_stages_on_two_streams(shape):
+    """Two stages over the same weights (each with its own KV pool and
+    workspace) driven step by step on two streams of default priority with
+    no synchronisation between them give, bit for bit, what one of them
+    gives alone: a stage keeps no state that another stage's calls touch."""
+    from paper_2606_18600_amd.harness import DeviceStage, upload_weights
+    seed, dtype = 2720, "bf16"
+    log(f"two stages on two streams: {shape.name}")
+    w = [upload_weights(synth.host_layer_weights(shape, seed, l), dtype) for l in range(2)]
+    lens = np.array([37, 150, 5, 64], np.int32)
+    bt = torch.from_numpy(synth.make_block_tables(lens + 8, 16, synth.BlockAllocator(64, seed)))
+    bt = bt.cuda()
+    steps = [(lens, np.zeros(4, np.int32), int(lens.sum()))]
+    steps += [(np.ones(4, np.int32), lens + i, 4) for i in range(6)]
+    xs = [torch.from_numpy(synth.hidden_states(seed, 10 + k, T, shape.hidden)).cuda()
+          .to(torch.bfloat16) for k, (_, _, T) in enumerate(steps)]
+
+    def step(st, k, s):
+        q, c, _ = steps[k]
+        with torch.cuda.stream(s):
+            if k == 0:
+                return st.prefill(q, c, bt, xs[k], stream=s.cuda_stream)
+            return st.decode(c, bt, xs[k], stream=s.cuda_stream)
+
+    alone = DeviceStage(shape, dtype, 0, w, 64, 256, 4)
+    a = DeviceStage(shape, dtype, 0, w, 64, 256, 4)
+    b = DeviceStage(shape, dtype, 0, w, 64, 256, 4)
+    try:
+        main = torch.cuda.current_stream()
+        ref = [step(alone, k, main) for k in range(len(steps))]
+        torch.cuda.synchronize()
+        s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+        s1.wait_stream(main)
+        s2.wait_stream(main)
+        ya, yb = [], []
+        for k in range(len(steps)):  # enqueued alternately, step by step
+            ya.append(step(a, k, s1))
+            yb.append(step(b, k, s2))
+        torch.cuda.synchronize()
+        for k in range(len(steps)):
+            assert torch.equal(ya[k], ref[k]), f"stream 1, step {k}"
+            assert torch.equal(yb[k], ref[k]), f"stream 2, step {k}"
+        log(f"  {len(steps)} steps bitwise equal on both streams")
+    finally:
+        alone.close()
+        a.close()
+        b.close()
