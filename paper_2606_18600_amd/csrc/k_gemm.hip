@@ -383,7 +383,7 @@ void gemm_skinny8_bf16(const bf16_t* __restrict__ A, const bf16_t* __restrict__ 
 template <int MT, int GW>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2)))
 void gemm_skinny_kp_bf16(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, int M, int N,
-                         int K, int kb_len, float* __restrict__ out) {
+                         int K, int kb_len, float* __restrict__ out, bool rotate) {
   constexpr int KP = 8 / GW;
   constexpr int AF = MT * KP;                        // A fragments per step
   constexpr int NA = (AF + 7) / 8;                   // A copies per wave and step
@@ -421,16 +421,22 @@ void gemm_skinny_kp_bf16(const bf16_t* __restrict__ A, const bf16_t* __restrict_
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   u32x4_t wx[4], wy[4];
+  // The block walks its K range from step rot on, wrapping around. The
+  // blocks of one K range read the same A fragments; walked in lockstep they
+  // ask the same L2 lines at the same moment (batch 128: QKV 45 -> 40, O 37
+  // -> 33 us, measured), so each starts at a step of its own.
+  const int rot = rotate ? (int)((blockIdx.x * 7u + blockIdx.y * 3u) % (unsigned)iters) : 0;
   // loads of step t, clamped to the last step past the end (as above)
   auto load = [&](u32x4_t (&w)[4], int t) {
     t = t < iters ? t : iters - 1;
     const int slot = t % 3;
+    const int ts = t + rot < iters ? t + rot : t + rot - iters;  // the step's data
 #pragma unroll
     for (int u = 0; u < NA; ++u)
-      __builtin_amdgcn_global_load_lds((const void*)(asrc[u] + (size_t)t * KP * 512),
+      __builtin_amdgcn_global_load_lds((const void*)(asrc[u] + (size_t)ts * KP * 512),
                                        (lds_ptr_t)&lds[(slot * SLOT + wave + 8 * u) * 64], 16, 0,
                                        0);
-    const bf16_t* q = wp + (size_t)t * KP * 4 * 512;
+    const bf16_t* q = wp + (size_t)ts * KP * 4 * 512;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
       w[j] = __builtin_nontemporal_load((const u32x4_t*)(q + j * 512));
@@ -866,6 +872,16 @@ __global__ __launch_bounds__(256) void gemm_tiled_f32(const float* __restrict__ 
   }
 }
 
+// Each block of the k-part kernel walks its K range from a step of its own
+// (wrapping around) unless STAGE_SKINNY_ROT=0 (read once).
+bool skinny_rot() {
+  static const bool on = [] {
+    const char* v = getenv("STAGE_SKINNY_ROT");
+    return !(v && *v && atoi(v) == 0);
+  }();
+  return on;
+}
+
 // 65..128 rows run on the 8-wave kernel unless STAGE_SKINNY8=0 (read once).
 bool skinny8_enabled() {
   static const bool on = [] {
@@ -881,7 +897,7 @@ hipError_t launch_skinny_kp(const bf16_t* a, const bf16_t* w, int M, int N, int 
   const int groups = N / 64;
   dim3 grid((groups + kSkinnyKpGroups - 1) / kSkinnyKpGroups, splits);
   gemm_skinny_kp_bf16<MT, kSkinnyKpGroups><<<grid, 512, 0, s>>>(a, w, M, N, K, kb_len,
-                                                                 (float*)out);
+                                                                 (float*)out, skinny_rot());
   return hipGetLastError();
 }
 
