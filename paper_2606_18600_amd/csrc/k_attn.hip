@@ -449,9 +449,13 @@ void attn_prefill_bf16(
         sc[i][bi] = s;
       }
     }
-    // softmax statistics of the stage (log2 units: score * scale); P as bf16
-    // B operands
-    u32x2_t pb[RT][BPS];
+    // softmax statistics of the stage (log2 units: score * scale). The
+    // maxima and the rescale of both row tiles come first, behind one
+    // (rarely taken) branch, so that the exponentials and the P V products
+    // below share one basic block and the compiler can overlap the
+    // exponentials of later key blocks with the products of earlier ones.
+    float mn[RT], alpha[RT];
+    bool grow_any = false;
 #pragma unroll
     for (int i = 0; i < RT; ++i) {
       float bm = -INFINITY;
@@ -461,23 +465,35 @@ void attn_prefill_bf16(
         for (int r = 0; r < 4; ++r) bm = vmax(bm, sc[i][bi][r]);
       bm = row4_max(bm) * scale;
       const bool grow = bm > st[i].m + kLazyRescale;
-      const float mn = grow ? bm : st[i].m;
-      const float alpha = fast_exp2(st[i].m - mn);  // 1 unless the maximum moved
-      float ps = 0.f;
+      mn[i] = grow ? bm : st[i].m;
+      alpha[i] = fast_exp2(st[i].m - mn[i]);  // exactly 1 unless the maximum moved
+      grow_any = grow_any || grow;
+    }
+    if (__builtin_amdgcn_ballot_w64(grow_any) != 0) {
 #pragma unroll
-      for (int bi = 0; bi < BPS; ++bi) {
+      for (int i = 0; i < RT; ++i)
+#pragma unroll
+        for (int t = 0; t < D / 16; ++t) oacc[i][t] *= alpha[i];
+    }
+    // P as bf16 B operands, key block by key block
+    u32x2_t pb[RT][BPS];
+    float ps[RT];
+#pragma unroll
+    for (int i = 0; i < RT; ++i) ps[i] = 0.f;
+#pragma unroll
+    for (int bi = 0; bi < BPS; ++bi)
+#pragma unroll
+      for (int i = 0; i < RT; ++i) {
         float p[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) p[r] = fast_exp2(fmaf(sc[i][bi][r], scale, -mn));
-        ps += (p[0] + p[1]) + (p[2] + p[3]);
+        for (int r = 0; r < 4; ++r) p[r] = fast_exp2(fmaf(sc[i][bi][r], scale, -mn[i]));
+        ps[i] += (p[0] + p[1]) + (p[2] + p[3]);
         pb[i][bi] = u32x2_t{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3])};
       }
-      st[i].l = st[i].l * alpha + row4_sum(ps);
-      st[i].m = mn;
-      if (__builtin_amdgcn_ballot_w64(grow) != 0) {
 #pragma unroll
-        for (int t = 0; t < D / 16; ++t) oacc[i][t] *= alpha;
-      }
+    for (int i = 0; i < RT; ++i) {
+      st[i].l = st[i].l * alpha[i] + row4_sum(ps[i]);
+      st[i].m = mn[i];
     }
     // O^T += V^T P^T, two key blocks per 16x16x32 product: the k index runs
     // over keys 4g..4g+3 of the first block and then of the second (g =
@@ -486,8 +502,7 @@ void attn_prefill_bf16(
     // The two 8-byte halves of each operand are read from LDS straight into
     // adjacent registers. (The reads are volatile so that the compiler does
     // not merge neighbouring halves into one 16-byte read and then assemble
-    // the operands with register moves; the reads of the next pair of d
-    // tiles are issued before the products of the current pair.)
+    // the operands with register moves.)
     typedef const volatile u32x2_t __attribute__((address_space(3)))* lds_u32x2_ptr;
     const lds_u32x2_ptr L2 = (lds_u32x2_ptr)L;
     auto vload = [&](int bp, int t) {
@@ -496,25 +511,35 @@ void attn_prefill_bf16(
       const u32x2_t a1 = L2[(((bp + 1) * FR + NJ + (t >> 1)) * 64 + lane) * 2 + h];
       return u32x4_t{a0[0], a0[1], a1[0], a1[1]};
     };
+    // Groups g of 2 * RT products (a pair of key blocks and a pair of d
+    // tiles, for every row tile); the V operands of group g + 2 are read
+    // while the products of group g run.
+    constexpr int NG = (BPS / 2) * (D / 32), PD = 2;
+    u32x4_t va[PD + 1], vb[PD + 1];
+    auto vgroup = [&](int g) {
+      const int bp = (g / (D / 32)) * 2, tp = g % (D / 32);
+      va[g % (PD + 1)] = vload(bp, 2 * tp);
+      vb[g % (PD + 1)] = vload(bp, 2 * tp + 1);
+    };
 #pragma unroll
-    for (int bp = 0; bp < BPS; bp += 2) {
-      u32x4_t cur0 = vload(bp, 0), cur1 = vload(bp, 1);
+    for (int g = 0; g < PD; ++g) vgroup(g);
+    // The compiler's scheduler would otherwise move each read down to just
+    // before its products (fewest live registers); these group barriers keep
+    // the order: the first PD groups' reads, then per group the reads of
+    // group g + PD followed by the products of group g.
+    __builtin_amdgcn_sched_group_barrier(0x100, 4 * PD, 0);
 #pragma unroll
-      for (int tp = 0; tp < D / 32; ++tp) {
-        u32x4_t nxt0 = cur0, nxt1 = cur1;
-        if (tp + 1 < D / 32) {
-          nxt0 = vload(bp, 2 * tp + 2);
-          nxt1 = vload(bp, 2 * tp + 3);
-        }
+    for (int g = 0; g < NG; ++g) {
+      if (g + PD < NG) vgroup(g + PD);
+      const int bp = (g / (D / 32)) * 2, tp = g % (D / 32);
 #pragma unroll
-        for (int i = 0; i < RT; ++i) {
-          const u32x4_t pp{pb[i][bp][0], pb[i][bp][1], pb[i][bp + 1][0], pb[i][bp + 1][1]};
-          oacc[i][2 * tp] = mfma16x16x32(cur0, pp, oacc[i][2 * tp]);
-          oacc[i][2 * tp + 1] = mfma16x16x32(cur1, pp, oacc[i][2 * tp + 1]);
-        }
-        cur0 = nxt0;
-        cur1 = nxt1;
+      for (int i = 0; i < RT; ++i) {
+        const u32x4_t pp{pb[i][bp][0], pb[i][bp][1], pb[i][bp + 1][0], pb[i][bp + 1][1]};
+        oacc[i][2 * tp] = mfma16x16x32(va[g % (PD + 1)], pp, oacc[i][2 * tp]);
+        oacc[i][2 * tp + 1] = mfma16x16x32(vb[g % (PD + 1)], pp, oacc[i][2 * tp + 1]);
       }
+      if (g + PD < NG) __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);  // 4 LDS reads
+      __builtin_amdgcn_sched_group_barrier(0x008, 2 * RT, 0);               // then the MFMAs
     }
     __builtin_amdgcn_s_waitcnt(0);  // the next stage has landed in LDS
     __syncthreads();

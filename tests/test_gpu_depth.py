@@ -51,7 +51,12 @@ def _sample_cache(st, li, bt_row, n_tok):
     return gpu_kv_to_oracle_layout(st.kv_view()[li:li + 1, ids])[0]
 
 
-def test_l70_80_layers_as_four_20_layer_stages():
+@pytest.fixture(scope="module")
+def depth_run():
+    """The GPU part: 80 layers as four 20-layer stages, the sampled
+    sequences' contexts written by the stages' chunked prefill, then a
+    decode step and a mixed step through all four; the boundary hidden
+    states of the sampled rows."""
     shape, nL, per, B = synth.LLAMA70B, 80, 20, 128
     H = shape.hidden
     cfg = model_config(shape, "bf16")
@@ -103,59 +108,70 @@ def test_l70_80_layers_as_four_20_layer_stages():
         rows2 = [b[[2048 + s for s in sample]].double().cpu().numpy() for b in b2]
         del b1, b2
         log(f"  GPU part done in {time.time() - t0:.0f} s")
-
-        oc = ocfg(shape)
-        nS = len(sample)
-        for k, st in enumerate(stages):
-            # rows of both steps in one oracle batch: step 1 (position ctx),
-            # then step 2 (position ctx + 1), each with its own cache copy
-            x0 = np.concatenate([rows1[k], rows2[k]])
-            x_ex, x_em = x0, x0
-            pos = [int(ctx[s]) for s in sample] + [int(ctx[s]) + 1 for s in sample]
-            for li in range(per):
-                l = k * per + li
-                rm = device_layer_weights(shape, SEED, l, "bf16")
-                again = pack_layer(cfg, rm)
-                for name in PACKED:
-                    assert torch.equal(again[name], packed[l][name]), (l, name)
-                del again
-                w64 = {n: v.to(torch.float64).cpu().numpy() for n, v in rm.items()}
-                del rm
-                parts = [_sample_cache(st, li, dbt_np[s], int(ctx[s]) + 2) for s in sample]
-                seqs, base = [], 0
-                kk, vv = [], []
-                for j in range(2 * nS):          # step-1 copies, then step-2 copies
-                    c = parts[j % nS]
-                    kk.append(c["k"])
-                    vv.append(c["v"])
-                    nb = c["k"].shape[0]
-                    seqs.append(O.SeqSpec(pos[j], 1, list(range(base, base + nb))))
-                    base += nb
-                gpu_k = [(c["k"][p // 16, p % 16].copy(), c["v"][p // 16, p % 16].copy())
-                         for c, p in zip(parts + parts, pos)]
-                cache_ex = {"k": np.concatenate(kk), "v": np.concatenate(vv)}
-                cache_em = {"k": cache_ex["k"].copy(), "v": cache_ex["v"].copy()}
-                x_ex = O.layer_forward(oc, w64, x_ex, seqs, cache_ex)
-                x_em = O.layer_forward(oc, w64, x_em, seqs, cache_em, rounding=O.round_to_bf16)
-                del w64
-                if li == 0:
-                    for j, sp in enumerate(seqs):
-                        p = sp.ctx_len
-                        b, o = sp.block_table[p // 16], p % 16
-                        ek = rel_l2(gpu_k[j][0], cache_ex["k"][b, o])
-                        ev = rel_l2(gpu_k[j][1], cache_ex["v"][b, o])
-                        assert ek <= TOL and ev <= TOL, (k, j, ek, ev)
-            for j in range(2 * nS):
-                gpu = (rows1 if j < nS else rows2)[k + 1][j % nS]
-                e_ex, e_em = rel_l2(gpu, x_ex[j]), rel_l2(gpu, x_em[j])
-                floor = rel_l2(x_em[j], x_ex[j])
-                s = sample[j % nS]
-                log(f"  layers [{k * per}, {(k + 1) * per}) step {1 + j // nS} seq {s} "
-                    f"ctx {int(ctx[s])}: vs exact {e_ex:.3e}, vs bf16-emulated {e_em:.3e}, "
-                    f"floor {floor:.3e}")
-                assert e_ex <= max(TOL, 1.25 * floor), (k, j, e_ex, floor)
-                assert e_em <= max(TOL, 1.25 * floor), (k, j, e_em, floor)
-        log(f"  done in {time.time() - t0:.0f} s")
+        yield dict(shape=shape, cfg=cfg, per=per, packed=packed, stages=stages, ctx=ctx,
+                   sample=sample, dbt_np=dbt_np, rows1=rows1, rows2=rows2)
     finally:
         for st in stages:
             st.close()
+
+
+# one test per sub-range, so that each runs its 20 oracle layers (about a
+# minute) on its own
+@pytest.mark.parametrize("k", [0, 1, 2, 3])
+def test_l70_80_layers_as_four_20_layer_stages(depth_run, k):
+    d = depth_run
+    shape, cfg, per, packed = d["shape"], d["cfg"], d["per"], d["packed"]
+    ctx, sample, dbt_np, rows1, rows2 = d["ctx"], d["sample"], d["dbt_np"], d["rows1"], d["rows2"]
+    st = d["stages"][k]
+    t0 = time.time()
+    oc = ocfg(shape)
+    nS = len(sample)
+    # rows of both steps in one oracle batch: step 1 (position ctx), then
+    # step 2 (position ctx + 1), each with its own cache copy
+    x0 = np.concatenate([rows1[k], rows2[k]])
+    x_ex, x_em = x0, x0
+    pos = [int(ctx[s]) for s in sample] + [int(ctx[s]) + 1 for s in sample]
+    for li in range(per):
+        l = k * per + li
+        rm = device_layer_weights(shape, SEED, l, "bf16")
+        again = pack_layer(cfg, rm)
+        for name in PACKED:
+            assert torch.equal(again[name], packed[l][name]), (l, name)
+        del again
+        w64 = {n: v.to(torch.float64).cpu().numpy() for n, v in rm.items()}
+        del rm
+        parts = [_sample_cache(st, li, dbt_np[s], int(ctx[s]) + 2) for s in sample]
+        seqs, base = [], 0
+        kk, vv = [], []
+        for j in range(2 * nS):          # step-1 copies, then step-2 copies
+            c = parts[j % nS]
+            kk.append(c["k"])
+            vv.append(c["v"])
+            nb = c["k"].shape[0]
+            seqs.append(O.SeqSpec(pos[j], 1, list(range(base, base + nb))))
+            base += nb
+        gpu_k = [(c["k"][p // 16, p % 16].copy(), c["v"][p // 16, p % 16].copy())
+                 for c, p in zip(parts + parts, pos)]
+        cache_ex = {"k": np.concatenate(kk), "v": np.concatenate(vv)}
+        cache_em = {"k": cache_ex["k"].copy(), "v": cache_ex["v"].copy()}
+        x_ex = O.layer_forward(oc, w64, x_ex, seqs, cache_ex)
+        x_em = O.layer_forward(oc, w64, x_em, seqs, cache_em, rounding=O.round_to_bf16)
+        del w64
+        if li == 0:
+            for j, sp in enumerate(seqs):
+                p = sp.ctx_len
+                b, o = sp.block_table[p // 16], p % 16
+                ek = rel_l2(gpu_k[j][0], cache_ex["k"][b, o])
+                ev = rel_l2(gpu_k[j][1], cache_ex["v"][b, o])
+                assert ek <= TOL and ev <= TOL, (k, j, ek, ev)
+    for j in range(2 * nS):
+        gpu = (rows1 if j < nS else rows2)[k + 1][j % nS]
+        e_ex, e_em = rel_l2(gpu, x_ex[j]), rel_l2(gpu, x_em[j])
+        floor = rel_l2(x_em[j], x_ex[j])
+        s = sample[j % nS]
+        log(f"  layers [{k * per}, {(k + 1) * per}) step {1 + j // nS} seq {s} "
+            f"ctx {int(ctx[s])}: vs exact {e_ex:.3e}, vs bf16-emulated {e_em:.3e}, "
+            f"floor {floor:.3e}")
+        assert e_ex <= max(TOL, 1.25 * floor), (k, j, e_ex, floor)
+        assert e_em <= max(TOL, 1.25 * floor), (k, j, e_em, floor)
+    log(f"  sub-range {k} done in {time.time() - t0:.0f} s")
