@@ -1,23 +1,24 @@
 // Causal grouped-query attention over the paged KV cache.
 //
 // Cache geometry per layer: [num_blocks][n_kv][2][16 * d]; plane 0 holds K,
-// plane 1 holds V, each as whole MFMA operand fragments (kv_k_offset and
-// kv_v_offset in packed.hpp), so every operand load is contiguous:
-//   S^T[key][row] = K[key][:] . Q[row][:]        v_mfma_f32_16x16x32_bf16
-//   O^T[d][row]  += V^T[d][key] . P^T[key][row]  v_mfma_f32_16x16x16_bf16
-// The C layout of the first product (lane l: row l%16, keys (l/16)*4 + r) is
-// exactly the B layout the second needs, and each lane keeps the online
-// softmax statistics of its own row, so no cross-lane shuffles are needed
-// beyond the 4-lane row reductions.
+// plane 1 holds V, each as whole 1 KB MFMA operand fragments (kv_k_offset
+// and kv_v_offset in packed.hpp).
 //
 // * attn_decode_bf16: one wave per (decode token, kv head, key split); the 16
 //   MFMA rows are the G query heads sharing the kv head (padded to 16).
-//   Partial (max, sum, unnormalised output) go to a workspace, and
-//   attn_merge_kernel combines the splits.
-// * attn_prefill_bf16: one wave per (query chunk of a sequence, kv head);
-//   rows are (position, head) pairs of the chunk, keys run from 0 to the
-//   last position of the chunk (the chunk's own keys are already in the
-//   cache), with the causal mask applied per row.
+//     S^T[key][row] = K[key][:] . Q[row][:]        v_mfma_f32_16x16x32_bf16
+//     O^T[d][row]  += V^T[d][key] . P^T[key][row]  v_mfma_f32_16x16x16_bf16
+//   Every operand is one contiguous fragment load. The C layout of the first
+//   product (lane l: row l%16, keys (l/16)*4 + r) is exactly the B layout
+//   the second needs, and each lane keeps the online softmax statistics of
+//   its own row (4-lane row reductions). Partial (max, sum, unnormalised
+//   output) go to a workspace, and attn_merge_kernel combines the splits.
+// * attn_prefill_bf16: one 4-wave workgroup per (128 rows of a chunk, kv
+//   head); rows are (position, head) pairs of the chunk, keys run from 0 to
+//   the last position of the chunk (the chunk's own keys are already in the
+//   cache), with the causal mask applied per row. Both products on
+//   v_mfma_f32_32x32x16_bf16, with operands gathered per lane from the same
+//   fragments (staged in LDS).
 // * attn_f32_kernel: plain fp32 SIMT attention, one wave per (token, head),
 //   for the fp32 mode.
 #include <type_traits>
@@ -324,27 +325,48 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const float* __restrict
 }
 
 // Prefill: one workgroup of kPfWaves waves per (item, kv head). Row r of
-// the workgroup (r < kPfWaves * RT * 16) is query position r / G of the item
-// and head kvh*G + r % G; wave w owns row tiles w*RT .. w*RT + RT - 1. Keys
-// run in stages of BPS 16-token blocks: each stage's K and V fragments are
-// copied once into LDS (direct loads, two buffers) and read by all waves, so
-// a key is fetched once per workgroup instead of once per 16 rows. Scores
-// of a whole stage are reduced together; the running maximum is only moved
-// (and the accumulators rescaled) when it grows by more than 2^8, so P stays
-// below 256 and the rescale is rare after the first stage.
+// the workgroup (r < kPfWaves * 32) is query position r / G of the item and
+// head kvh*G + r % G; wave w owns rows 32w .. 32w + 31 as one 32-row tile of
+// v_mfma_f32_32x32x16_bf16 (lane l: row l % 32). Keys run in stages of BPS
+// 16-token blocks: each stage's K and V fragments are copied once into LDS
+// (direct loads, two buffers) and read by all waves, so a key is fetched
+// once per workgroup instead of once per 32 rows. Scores of a whole stage
+// are reduced together; the running maximum is only moved (and the
+// accumulators rescaled) when it grows by more than 2^8, so P stays below
+// 256 and the rescale is rare after the first stage.
+//
+// The 32x32x16 form: one wave alone keeps the MFMA pipe nearly full with it
+// (2.37 PFLOP/s in a probe, against 1.4 for 16x16x32), which matters here
+// because a wave's MFMA work alternates with its softmax arithmetic.
+//   S^T[key][row] (32 keys = two blocks x 32 rows): A = K, lane l: key l % 32
+//     (block (l / 16) % 2, token l % 16), d 16 ds + 8 (l / 32) .. + 7, read
+//     per lane from the blocks' K fragments; B = Q^T, lane l: row l % 32,
+//     the same d. C, lane l, value v: row l % 32, key 8 (v / 4) + 4 (l / 32)
+//     + v % 4.
+//   O^T[d][row] += V^T[d][key] P^T[key][row], 16 keys (one block z of the
+//     pair) per product: B = P^T is values 8z .. 8z + 7 of the lane's S^T
+//     tile as they stand (k index 8 (l / 32) + e <-> key 8 (e / 4) + 4 (l /
+//     32) + e % 4), and A = V^T, lane l: d 32 t + l % 32, the same keys: two
+//     8-byte pieces of the block's V fragment t.
 constexpr int kPfWaves = 4;
 constexpr int kPfBPS = 4;
-// Row tiles per wave. Four tiles per wave do not fit the register budget of
-// two waves per SIMD and measured slower, so only two are built.
-constexpr int kPfRowTiles = 2;
-static_assert(kPfWaves * kPfRowTiles * 16 == kPrefillRows, "rows of a prefill work item");
+static_assert(kPfWaves * 32 == kPrefillRows, "rows of a prefill work item");
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+__device__ __forceinline__ float row2_max(float x) {
+  auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return vmax(__uint_as_float(a[0]), __uint_as_float(a[1]));
+}
+__device__ __forceinline__ float row2_sum(float x) {
+  auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(a[0]) + __uint_as_float(a[1]);
+}
 
 // Two workgroups per CU (64 KB of LDS each) need the register budget of two
 // waves per SIMD; one would leave no other wave to overlap a wave's
 // exponentials with MFMA work.
-template <int D, int RT>
+template <int D>
 __global__ __launch_bounds__(kPfWaves * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_prefill_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kv, int n_kv, SegTables tabs,
@@ -354,10 +376,14 @@ void attn_prefill_bf16(
   constexpr int FR = 2 * NJ;           // fragments per block
   constexpr int SF = BPS * FR;         // fragments per stage
   constexpr int PER = SF / kPfWaves;   // fragment copies per wave and stage
+  constexpr int NP = BPS / 2;          // 32-key tiles per stage
+  constexpr int ND = D / 16;           // 16-wide d slices (score products per tile)
+  constexpr int NT = D / 32;           // 32-wide d tiles of O^T
   static_assert(SF % kPfWaves == 0, "stage split");
-  static_assert(BPS % 2 == 0, "P V products take key blocks in pairs");
+  static_assert(BPS % 2 == 0, "score tiles take key blocks in pairs");
   __shared__ u32x4_t lds[2][SF * 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int l32 = lane & 31, hi = lane >> 5;
   // Workgroup b runs on XCD b % 8, each XCD with its own L2. Take the kv head
   // from the linear id modulo n_kv, so every XCD serves a fixed set of kv
   // heads and a sequence's K/V for one head is pulled into one L2 only (not
@@ -368,19 +394,16 @@ void attn_prefill_bf16(
   const int G = n_q / n_kv;
   const float scale = kLog2e / sqrtf((float)D);
 
-  int rpos[RT];  // position of this lane's row in each tile
-  bool rok[RT];
-  u32x4_t qf[RT][NJ];
+  const int r = wave * 32 + l32;  // this lane's row of the workgroup
+  const int pi = r / G;
+  const bool rok = pi < it.npos;
+  const int pc = rok ? pi : it.npos - 1;
+  const int rpos = it.p0 + pc;    // its position
+  u32x4_t qf[ND];
+  {
+    const bf16_t* qp = q + ((size_t)(it.t0 + pc) * n_q + kvh * G + r % G) * D + hi * 8;
 #pragma unroll
-  for (int i = 0; i < RT; ++i) {
-    const int r = (wave * RT + i) * 16 + (lane & 15);
-    const int pi = r / G;
-    rok[i] = pi < it.npos;
-    const int pc = rok[i] ? pi : it.npos - 1;
-    rpos[i] = it.p0 + pc;
-    const bf16_t* qp = q + ((size_t)(it.t0 + pc) * n_q + kvh * G + r % G) * D + (lane >> 4) * 8;
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) qf[i][j] = ldg128(qp + j * 32);
+    for (int s = 0; s < ND; ++s) qf[s] = ldg128(qp + s * 16);
   }
 
   const int32_t* bt = seq_table(tabs, it.seq);
@@ -389,14 +412,12 @@ void attn_prefill_bf16(
   const int nb = (kend + kBlock - 1) / kBlock;
   const int nst = (nb + BPS - 1) / BPS;
 
-  RowState st[RT];
-  f32x4_t oacc[RT][D / 16];
+  RowState st{-INFINITY, 0.f};
+  f32x16_t oacc[NT];
 #pragma unroll
-  for (int i = 0; i < RT; ++i) {
-    st[i] = RowState{-INFINITY, 0.f};
+  for (int t = 0; t < NT; ++t)
 #pragma unroll
-    for (int t = 0; t < D / 16; ++t) oacc[i][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  }
+    for (int v = 0; v < 16; ++v) oacc[t][v] = 0.f;
 
   // Block ids, 64 at a time (a multiple of BPS, so a stage never straddles
   // two windows).
@@ -415,6 +436,13 @@ void attn_prefill_bf16(
     }
   };
 
+  // lane offsets inside a block's fragments (u32x4 units): K of d slice s
+  // at (s / 2) * 64 + kslot + 32 (s % 2) of block 2 tile + kblk; V pieces
+  // at vslot and vslot + 32 (in 8-byte units, half vhalf)
+  const int kblk = (lane >> 4) & 1;
+  const int kslot = (lane & 15) + 16 * hi;
+  const int vslot = (lane & 15) + 16 * hi, vhalf = (lane >> 4) & 1;
+
   // One stage of BPS key blocks. Stages whose last key is at or before the
   // first query position of the item need no causal mask (for a long
   // context, nearly all of them).
@@ -429,117 +457,94 @@ void attn_prefill_bf16(
       issue(stg + 1, buf ^ 1);
     }
     const u32x4_t* L = lds[buf];
-    // raw scores of the stage: S^T tiles, lane l: row l%16, keys (l/16)*4 + r
-    f32x4_t sc[RT][BPS];
+    // raw scores of the stage, one 32-key tile per pair of blocks
+    f32x16_t sc[NP];
 #pragma unroll
-    for (int bi = 0; bi < BPS; ++bi) {
-      u32x4_t kf[NJ];
+    for (int t = 0; t < NP; ++t)
 #pragma unroll
-      for (int j = 0; j < NJ; ++j) kf[j] = L[(bi * FR + j) * 64 + lane];
-      const int key0 = (stg * BPS + bi) * kBlock + (lane >> 4) * 4;
+      for (int v = 0; v < 16; ++v) sc[t][v] = 0.f;
 #pragma unroll
-      for (int i = 0; i < RT; ++i) {
-        f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < ND; ++s)
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) s = mfma16x16x32(kf[j], qf[i][j], s);
-        if constexpr (kMask) {
+      for (int t = 0; t < NP; ++t) {
+        const u32x4_t kf = L[((2 * t + kblk) * FR + s / 2) * 64 + kslot + 32 * (s % 2)];
+        sc[t] = mfma32x32x16(kf, qf[s], sc[t]);
+      }
+    if constexpr (kMask) {
 #pragma unroll
-          for (int r = 0; r < 4; ++r) s[r] = key0 + r <= rpos[i] ? s[r] : -INFINITY;
+      for (int t = 0; t < NP; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int key = (stg * BPS + 2 * t) * kBlock + 8 * (v >> 2) + 4 * hi + (v & 3);
+          sc[t][v] = key <= rpos ? sc[t][v] : -INFINITY;
         }
-        sc[i][bi] = s;
+    }
+    // softmax statistics of the stage (log2 units: score * scale), then P
+    float bm = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < NP; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) bm = vmax(bm, sc[t][v]);
+    bm = row2_max(bm) * scale;
+    const bool grow = bm > st.m + kLazyRescale;
+    const float mn = grow ? bm : st.m;
+    const float alpha = fast_exp2(st.m - mn);  // exactly 1 unless the maximum moved
+    if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t) oacc[t] *= alpha;
+    }
+    u32x4_t pb[NP][2];
+    float ps = 0.f;
+#pragma unroll
+    for (int t = 0; t < NP; ++t)
+#pragma unroll
+      for (int z = 0; z < 2; ++z) {
+        float p[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) p[e] = fast_exp2(fmaf(sc[t][8 * z + e], scale, -mn));
+        ps += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+        pb[t][z] = u32x4_t{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
+                           pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])};
       }
-    }
-    // softmax statistics of the stage (log2 units: score * scale). The
-    // maxima and the rescale of both row tiles come first, behind one
-    // (rarely taken) branch, so that the exponentials and the P V products
-    // below share one basic block and the compiler can overlap the
-    // exponentials of later key blocks with the products of earlier ones.
-    float mn[RT], alpha[RT];
-    bool grow_any = false;
-#pragma unroll
-    for (int i = 0; i < RT; ++i) {
-      float bm = -INFINITY;
-#pragma unroll
-      for (int bi = 0; bi < BPS; ++bi)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) bm = vmax(bm, sc[i][bi][r]);
-      bm = row4_max(bm) * scale;
-      const bool grow = bm > st[i].m + kLazyRescale;
-      mn[i] = grow ? bm : st[i].m;
-      alpha[i] = fast_exp2(st[i].m - mn[i]);  // exactly 1 unless the maximum moved
-      grow_any = grow_any || grow;
-    }
-    if (__builtin_amdgcn_ballot_w64(grow_any) != 0) {
-#pragma unroll
-      for (int i = 0; i < RT; ++i)
-#pragma unroll
-        for (int t = 0; t < D / 16; ++t) oacc[i][t] *= alpha[i];
-    }
-    // P as bf16 B operands, key block by key block
-    u32x2_t pb[RT][BPS];
-    float ps[RT];
-#pragma unroll
-    for (int i = 0; i < RT; ++i) ps[i] = 0.f;
-#pragma unroll
-    for (int bi = 0; bi < BPS; ++bi)
-#pragma unroll
-      for (int i = 0; i < RT; ++i) {
-        float p[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) p[r] = fast_exp2(fmaf(sc[i][bi][r], scale, -mn[i]));
-        ps[i] += (p[0] + p[1]) + (p[2] + p[3]);
-        pb[i][bi] = u32x2_t{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3])};
-      }
-#pragma unroll
-    for (int i = 0; i < RT; ++i) {
-      st[i].l = st[i].l * alpha[i] + row4_sum(ps[i]);
-      st[i].m = mn[i];
-    }
-    // O^T += V^T P^T, two key blocks per 16x16x32 product: the k index runs
-    // over keys 4g..4g+3 of the first block and then of the second (g =
-    // lane / 16), in V^T and in P^T alike, which is how both already sit
-    // in registers.
-    // The two 8-byte halves of each operand are read from LDS straight into
-    // adjacent registers. (The reads are volatile so that the compiler does
-    // not merge neighbouring halves into one 16-byte read and then assemble
-    // the operands with register moves.)
+    st.l = st.l * alpha + row2_sum(ps);
+    st.m = mn;
+    // O^T += V^T P^T, block by block. The two 8-byte pieces of each V^T
+    // operand are read from LDS straight into adjacent registers (volatile
+    // reads, so that the compiler does not merge them with neighbouring
+    // pieces and then assemble the operands with register moves).
     typedef const volatile u32x2_t __attribute__((address_space(3)))* lds_u32x2_ptr;
     const lds_u32x2_ptr L2 = (lds_u32x2_ptr)L;
-    auto vload = [&](int bp, int t) {
-      const int h = t & 1;  // words 0-1 or 2-3 of the lane's 16 bytes
-      const u32x2_t a0 = L2[((bp * FR + NJ + (t >> 1)) * 64 + lane) * 2 + h];
-      const u32x2_t a1 = L2[(((bp + 1) * FR + NJ + (t >> 1)) * 64 + lane) * 2 + h];
+    auto vload = [&](int blk, int t) {
+      const int f = blk * FR + NJ + t;
+      const u32x2_t a0 = L2[(f * 64 + vslot) * 2 + vhalf];
+      const u32x2_t a1 = L2[(f * 64 + vslot + 32) * 2 + vhalf];
       return u32x4_t{a0[0], a0[1], a1[0], a1[1]};
     };
-    // Groups g of 2 * RT products (a pair of key blocks and a pair of d
-    // tiles, for every row tile); the V operands of group g + 2 are read
-    // while the products of group g run.
-    constexpr int NG = (BPS / 2) * (D / 32), PD = 2;
+    // Groups g of two products (one block, two d tiles); the V operands of
+    // group g + 2 are read while the products of group g run.
+    constexpr int NG = BPS * NT / 2, PD = 2;
     u32x4_t va[PD + 1], vb[PD + 1];
     auto vgroup = [&](int g) {
-      const int bp = (g / (D / 32)) * 2, tp = g % (D / 32);
-      va[g % (PD + 1)] = vload(bp, 2 * tp);
-      vb[g % (PD + 1)] = vload(bp, 2 * tp + 1);
+      const int blk = g / (NT / 2), t = 2 * (g % (NT / 2));
+      va[g % (PD + 1)] = vload(blk, t);
+      vb[g % (PD + 1)] = vload(blk, t + 1);
     };
 #pragma unroll
     for (int g = 0; g < PD; ++g) vgroup(g);
     // The compiler's scheduler would otherwise move each read down to just
-    // before its products (fewest live registers); these group barriers keep
+    // before its product (fewest live registers); these group barriers keep
     // the order: the first PD groups' reads, then per group the reads of
     // group g + PD followed by the products of group g.
     __builtin_amdgcn_sched_group_barrier(0x100, 4 * PD, 0);
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
       if (g + PD < NG) vgroup(g + PD);
-      const int bp = (g / (D / 32)) * 2, tp = g % (D / 32);
-#pragma unroll
-      for (int i = 0; i < RT; ++i) {
-        const u32x4_t pp{pb[i][bp][0], pb[i][bp][1], pb[i][bp + 1][0], pb[i][bp + 1][1]};
-        oacc[i][2 * tp] = mfma16x16x32(va[g % (PD + 1)], pp, oacc[i][2 * tp]);
-        oacc[i][2 * tp + 1] = mfma16x16x32(vb[g % (PD + 1)], pp, oacc[i][2 * tp + 1]);
-      }
+      const int blk = g / (NT / 2), t = 2 * (g % (NT / 2));
+      const u32x4_t pp = pb[blk / 2][blk % 2];
+      oacc[t] = mfma32x32x16(va[g % (PD + 1)], pp, oacc[t]);
+      oacc[t + 1] = mfma32x32x16(vb[g % (PD + 1)], pp, oacc[t + 1]);
       if (g + PD < NG) __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);  // 4 LDS reads
-      __builtin_amdgcn_sched_group_barrier(0x008, 2 * RT, 0);               // then the MFMAs
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);                    // then the MFMAs
     }
     __builtin_amdgcn_s_waitcnt(0);  // the next stage has landed in LDS
     __syncthreads();
@@ -554,23 +559,21 @@ void attn_prefill_bf16(
   for (; stg < nfull; ++stg) stage(std::false_type{}, stg);
   for (; stg < nst; ++stg) stage(std::true_type{}, stg);
 
+  if (!rok) return;
+  const float inv = 1.0f / st.l;
+  // packed activation layout (the O projection's input); 4 consecutive
+  // columns share one 8-byte piece of a fragment lane
+  const int row = it.t0 + pi;
+  const int col0 = (kvh * G + r % G) * D + 4 * hi;
 #pragma unroll
-  for (int i = 0; i < RT; ++i) {
-    if (!rok[i]) continue;
-    const int r = (wave * RT + i) * 16 + (lane & 15);
-    const float inv = 1.0f / st[i].l;
-    // packed activation layout (the O projection's input); 4 consecutive
-    // columns share one 8-byte piece of a fragment lane
-    const int row = it.t0 + r / G;
-    const int col0 = (kvh * G + r % G) * D + (lane >> 4) * 4;
+  for (int t = 0; t < NT; ++t)
 #pragma unroll
-    for (int t = 0; t < D / 16; ++t) {
+    for (int qd = 0; qd < 4; ++qd) {
       u32x2_t w;
-      w[0] = pack_bf16x2(oacc[i][t][0] * inv, oacc[i][t][1] * inv);
-      w[1] = pack_bf16x2(oacc[i][t][2] * inv, oacc[i][t][3] * inv);
-      *(u32x2_t*)(out + packed_a_offset(row, col0 + t * 16, n_q * D)) = w;
+      w[0] = pack_bf16x2(oacc[t][4 * qd] * inv, oacc[t][4 * qd + 1] * inv);
+      w[1] = pack_bf16x2(oacc[t][4 * qd + 2] * inv, oacc[t][4 * qd + 3] * inv);
+      *(u32x2_t*)(out + packed_a_offset(row, col0 + 32 * t + 8 * qd, n_q * D)) = w;
     }
-  }
 }
 
 // fp32 mode: one wave per (token, query head), keys [0, pos] of its sequence.
@@ -672,10 +675,10 @@ hipError_t attn_merge(DType dt, const float* part_o, const float* part_ml,
   return hipErrorInvalidValue;
 }
 
-template <int D, int RT>
+template <int D>
 static void launch_prefill(dim3 grid, hipStream_t s, const void* q, KVLayer kv, SegTables tabs,
                            const PrefillItem* items, int n_q, void* out) {
-  attn_prefill_bf16<D, RT><<<grid, kPfWaves * 64, 0, s>>>(
+  attn_prefill_bf16<D><<<grid, kPfWaves * 64, 0, s>>>(
       (const bf16_t*)q, (const bf16_t*)kv.base, kv.n_kv, tabs, items, n_q, (bf16_t*)out);
 }
 
@@ -687,9 +690,9 @@ hipError_t attn_prefill(DType dt, const void* q, KVLayer kv, SegTables tabs,
   if (kPrefillRows % (n_q / kv.n_kv) != 0) return hipErrorInvalidValue;
   dim3 grid(n_items, kv.n_kv);
   if (kv.head_dim == 128)
-    launch_prefill<128, kPfRowTiles>(grid, s, q, kv, tabs, items, n_q, out);
+    launch_prefill<128>(grid, s, q, kv, tabs, items, n_q, out);
   else if (kv.head_dim == 64)
-    launch_prefill<64, kPfRowTiles>(grid, s, q, kv, tabs, items, n_q, out);
+    launch_prefill<64>(grid, s, q, kv, tabs, items, n_q, out);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
