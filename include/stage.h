@@ -34,16 +34,18 @@
  *      [n_layers][num_blocks][n_kv][2][block_size * head_dim]
  *    in the mode dtype. Token p of a sequence with block table bt lives in
  *    block bt[p / block_size] at offset o = p % block_size. Plane 0 holds K,
- *    plane 1 holds V, both as whole MFMA operand fragments so that every
- *    load of the attention kernels is contiguous:
+ *    plane 1 holds V, both as whole 1 KB MFMA operand fragments, so that
+ *    the attention kernels read a block's K and V from HBM in contiguous
+ *    16-byte-per-lane loads:
  *      K[o][d] at (d / 32) * 512 + (o + 16 * ((d % 32) / 8)) * 8 + d % 8
  *      V[o][d] at (d / 32) * 512 + (d % 16 + 16 * (o / 4)) * 8 + ((d / 16) % 2) * 4 + o % 4
  *    Block ids index the same blocks in every layer of the stage. Slots a
  *    call has not written (past a sequence's length in its last block) are
  *    read but given zero weight; they must hold finite values (a pool
  *    zeroed when allocated, or finite data of earlier sequences), since an
- *    Inf or NaN times a zero weight is NaN. The entries a call reads (the first ceil((ctx_lens[i] + q_lens[i]) /
- *    block_size) of row i) must lie in [0, num_blocks): the kernels read
+ *    Inf or NaN times a zero weight is NaN. The block-table entries a call
+ *    reads (the first ceil((ctx_lens[i] + q_lens[i]) / block_size) of row
+ *    i) must lie in [0, num_blocks): the kernels read
  *    them on the device and do not check them, so an id outside that range
  *    is an out-of-bounds access of the pool. With the environment variable
  *    STAGE_DEBUG=1 set when a stage is created, every forward call first
