@@ -929,7 +929,7 @@ def bench_l70_stage(args):
         "config": {"workload": "l70-decode: Llama-3.1-70B-shaped stage, layers [20,40), "
                                "decode batch 64, contexts uniform 512-2048, KV block 16",
                    "layers": nL, "batch": B, "hidden": shape.hidden, "block": 16},
-        "roofline": {"bound": "hbm", "kernel": "gemm_skinny_bf16 (gate-up, split-K)",
+        "roofline": {"bound": "hbm", "kernel": "gemm_skinny_bf16 (gate-up + SwiGLU, one K range)",
                      "achieved": round(gu_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(gu_gbs / HBM_PEAK_GBS, 4), "traffic": gu_traffic,
                      "bytes_per_launch": gu_bytes, "us_per_launch": round(gu_avg_ms * 1e3, 2)},
