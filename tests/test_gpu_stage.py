@@ -134,6 +134,39 @@ def test_ragged_lengths_and_block_boundaries(dtype):
         pair.close()
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_tables_and_buffers_filled_to_capacity(dtype):
+    """Every limit at its maximum in one flow: a prompt of exactly
+    max_blocks_per_seq * 16 tokens (its table row full), a decode that
+    writes the last slot of its sequence's last block, a prefill of exactly
+    max_tokens rows from max_seqs sequences, and every block of the pool in
+    use by the end."""
+    seed = 53
+    shape = synth.TINY
+    mb = 4                                        # 64 tokens per table row
+    lens = np.array([63, 64, 48], np.int32)
+    final = lens + np.array([1, 0, 1], np.int32)  # sequences 0 and 2 decode once
+    n_blocks = int(((final + 15) // 16).sum())    # 12: all of them used
+    bt = synth.make_block_tables(final, mb, synth.BlockAllocator(n_blocks, seed))
+    T = int(lens.sum())
+    log(f"capacity dtype={dtype}: prompts {lens.tolist()} in rows of {mb} blocks, "
+        f"{n_blocks} blocks, max_tokens {T}")
+    pair = Pair(shape, dtype, 2, n_blocks, T, 3, seed)
+    try:
+        y, yr, x = pair.prefill(lens, np.zeros(3, np.int32), bt,
+                                synth.hidden_states(seed, 1, T, shape.hidden))
+        _check("prefill", y, yr, x, TOL[dtype])
+        y, yr, x = pair.decode(np.array([63, 48], np.int32), bt[[0, 2]],
+                               synth.hidden_states(seed, 2, 2, shape.hidden))
+        _check("decode", y, yr, x, TOL[dtype])
+        assert len(pair.written) == n_blocks * 16 - 15  # all slots but the last block's tail of seq 2
+        kv = pair.kv_errors()
+        log(f"  kv rel_l2={kv:.3e}")
+        assert kv <= TOL[dtype]
+    finally:
+        pair.close()
+
+
 def test_decode_of_a_first_token():
     """A decode token with no context (position 0) attends only to itself."""
     seed = 41
