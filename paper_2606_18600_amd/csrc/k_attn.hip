@@ -577,9 +577,12 @@ void attn_prefill_bf16(
 }
 
 // fp32 mode: one wave per (token, query head), keys [0, pos] of its sequence.
+// (D is a template argument so that the score and value loops unroll and
+// issue their loads ahead of the dependent FMA chains.)
+template <int D>
 __global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__ q,
                                                        const float* __restrict__ kv, int n_kv,
-                                                       int D, SegTables tabs,
+                                                       SegTables tabs,
                                                        const int32_t* __restrict__ tok_seq,
                                                        const int32_t* __restrict__ tok_pos,
                                                        int t_begin, int n_q,
@@ -601,6 +604,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__
     if (key <= pos) {
       const float* kp = kv + ((size_t)bt[key / kBlock] * n_kv + kvh) * 2 * plane;
       float acc = 0.f;
+#pragma unroll
       for (int e = 0; e < D; ++e) acc = fmaf(qp[e], kp[kv_k_offset(key % kBlock, e)], acc);
       s = acc * scale;
     }
@@ -612,6 +616,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__
     o0 *= alpha;
     o1 *= alpha;
     const int nk = min(64, pos + 1 - c0);
+#pragma unroll 8
     for (int j = 0; j < nk; ++j) {
       const float pj = __shfl(p, j, 64);
       const int kj = c0 + j;
@@ -704,8 +709,12 @@ hipError_t attn_f32(const float* q, KVLayer kv, SegTables tabs, const int32_t* t
   if (n_tok == 0) return hipSuccess;
   if (kv.head_dim != 64 && kv.head_dim != 128) return hipErrorInvalidValue;
   dim3 grid(n_tok, (n_q + 3) / 4);
-  attn_f32_kernel<<<grid, 256, 0, s>>>(q, (const float*)kv.base, kv.n_kv, kv.head_dim, tabs,
-                                       tok_seq, tok_pos, t_begin, n_q, out);
+  if (kv.head_dim == 128)
+    attn_f32_kernel<128><<<grid, 256, 0, s>>>(q, (const float*)kv.base, kv.n_kv, tabs, tok_seq,
+                                              tok_pos, t_begin, n_q, out);
+  else
+    attn_f32_kernel<64><<<grid, 256, 0, s>>>(q, (const float*)kv.base, kv.n_kv, tabs, tok_seq,
+                                             tok_pos, t_begin, n_q, out);
   return hipGetLastError();
 }
 

@@ -823,17 +823,20 @@ __global__ __launch_bounds__(WM * WN * 64, 512 / (WM * WN * 64)) void gemm_tiled
 // ---------------------------------------------------------------------------
 // fp32 SIMT tiled GEMM (fp32 mode, row-major operands)
 // ---------------------------------------------------------------------------
-constexpr int TF = 64, TF_K = 16;
+constexpr int TF_K = 16;
 
-template <int EPI>
+// Block tile TF x TF (64, or 32 when 64-wide tiles would leave most of the
+// chip idle), 16 x 16 threads of (TF / 16)^2 outputs each.
+template <int TF, int EPI>
 __global__ __launch_bounds__(256) void gemm_tiled_f32(const float* __restrict__ A,
                                                       const float* __restrict__ W, int M, int N,
                                                       int K, float* __restrict__ out) {
+  constexpr int R = TF / 16;
   __shared__ float As[TF_K][TF + 1];
   __shared__ float Bs[TF_K][TF + 1];
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   const int m0 = blockIdx.x * TF, n0 = blockIdx.y * TF;
-  float acc[4][4] = {};
+  float acc[R][R] = {};
   for (int k0 = 0; k0 < K; k0 += TF_K) {
     for (int q = threadIdx.x; q < TF * TF_K; q += 256) {
       const int r = q / TF_K, c = q % TF_K;
@@ -844,25 +847,25 @@ __global__ __launch_bounds__(256) void gemm_tiled_f32(const float* __restrict__ 
     __syncthreads();
 #pragma unroll
     for (int c = 0; c < TF_K; ++c) {
-      float a[4], b[4];
+      float a[R], b[R];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = As[c][ty * 4 + i];
+      for (int i = 0; i < R; ++i) a[i] = As[c][ty * R + i];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = Bs[c][tx * 4 + j];
+      for (int j = 0; j < R; ++j) b[j] = Bs[c][tx * R + j];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < R; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+        for (int j = 0; j < R; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int m = m0 + ty * 4 + i;
+  for (int i = 0; i < R; ++i) {
+    const int m = m0 + ty * R + i;
     if (m >= M) continue;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int n = n0 + tx * 4 + j;
+    for (int j = 0; j < R; ++j) {
+      const int n = n0 + tx * R + j;
       if (n >= N) continue;
       if (EPI == EPI_RESID_ADD)
         out[(size_t)m * N + n] += acc[i][j];
@@ -870,6 +873,74 @@ __global__ __launch_bounds__(256) void gemm_tiled_f32(const float* __restrict__ 
         out[(size_t)m * N + n] = acc[i][j];
     }
   }
+}
+
+template <int TF>
+hipError_t launch_tiled_f32(Epilogue epi, const float* A, const float* W, int M, int N, int K,
+                            float* out, hipStream_t s) {
+  dim3 grid((M + TF - 1) / TF, (N + TF - 1) / TF);
+  if (epi == EPI_RESID_ADD)
+    gemm_tiled_f32<TF, EPI_RESID_ADD><<<grid, 256, 0, s>>>(A, W, M, N, K, out);
+  else if (epi == EPI_STORE_F32)
+    gemm_tiled_f32<TF, EPI_STORE_F32><<<grid, 256, 0, s>>>(A, W, M, N, K, out);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+// fp32 products of at most kGemvRows rows (decode steps in the fp32 mode):
+// one wave per output column, its lanes striding over K for every row, each
+// row's sum then reduced across the wave in a fixed order. On 64 x 64 tiles
+// such a product runs N / 64 workgroups over the whole of K (the tiny
+// shape's down projection: 4 workgroups, 95 us).
+constexpr int kGemvRows = 8;
+
+template <int MR, int EPI>
+__global__ __launch_bounds__(256) void gemv_f32(const float* __restrict__ A,
+                                                const float* __restrict__ W, int N, int K,
+                                                float* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (n >= N) return;
+  const float* w = W + (size_t)n * K;
+  float acc[MR];
+#pragma unroll
+  for (int m = 0; m < MR; ++m) acc[m] = 0.f;
+  // unrolled so that several k steps' loads are in flight at once
+#pragma unroll 4
+  for (int k = lane; k < K; k += 64) {
+    const float wk = w[k];
+#pragma unroll
+    for (int m = 0; m < MR; ++m) acc[m] = fmaf(A[(size_t)m * K + k], wk, acc[m]);
+  }
+#pragma unroll
+  for (int m = 0; m < MR; ++m) {
+    const float v = wave_sum(acc[m]);
+    if (lane == 0) {
+      if (EPI == EPI_RESID_ADD)
+        out[(size_t)m * N + n] += v;
+      else
+        out[(size_t)m * N + n] = v;
+    }
+  }
+}
+
+template <int EPI>
+hipError_t launch_gemv_f32(const float* A, const float* W, int M, int N, int K, float* out,
+                           hipStream_t s) {
+  const int blocks = (N + 3) / 4;
+  switch (M) {
+    case 1: gemv_f32<1, EPI><<<blocks, 256, 0, s>>>(A, W, N, K, out); break;
+    case 2: gemv_f32<2, EPI><<<blocks, 256, 0, s>>>(A, W, N, K, out); break;
+    case 3: gemv_f32<3, EPI><<<blocks, 256, 0, s>>>(A, W, N, K, out); break;
+    case 4: gemv_f32<4, EPI><<<blocks, 256, 0, s>>>(A, W, N, K, out); break;
+    case 5: gemv_f32<5, EPI><<<blocks, 256, 0, s>>>(A, W, N, K, out); break;
+    case 6: gemv_f32<6, EPI><<<blocks, 256, 0, s>>>(A, W, N, K, out); break;
+    case 7: gemv_f32<7, EPI><<<blocks, 256, 0, s>>>(A, W, N, K, out); break;
+    case 8: gemv_f32<8, EPI><<<blocks, 256, 0, s>>>(A, W, N, K, out); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 // Each block of the k-part kernel walks its K range from a step of its own
@@ -1017,17 +1088,20 @@ hipError_t gemm(DType dt, Epilogue epi, const void* A, const void* W, int M, int
         (const bf16_t*)A, (const bf16_t*)W, M, N, K, out, N, K, 0, rope);
     return hipGetLastError();
   }
-  if (dt == DT_F32) {
-    dim3 grid((M + TF - 1) / TF, (N + TF - 1) / TF);
+  if (dt == DT_F32 && M <= kGemvRows) {
     if (epi == EPI_RESID_ADD)
-      gemm_tiled_f32<EPI_RESID_ADD><<<grid, 256, 0, s>>>((const float*)A, (const float*)W, M, N,
-                                                          K, (float*)out);
-    else if (epi == EPI_STORE_F32)
-      gemm_tiled_f32<EPI_STORE_F32><<<grid, 256, 0, s>>>((const float*)A, (const float*)W, M, N,
-                                                          K, (float*)out);
-    else
-      return hipErrorInvalidValue;
-    return hipGetLastError();
+      return launch_gemv_f32<EPI_RESID_ADD>((const float*)A, (const float*)W, M, N, K,
+                                            (float*)out, s);
+    if (epi == EPI_STORE_F32)
+      return launch_gemv_f32<EPI_STORE_F32>((const float*)A, (const float*)W, M, N, K,
+                                            (float*)out, s);
+    return hipErrorInvalidValue;
+  }
+  if (dt == DT_F32) {
+    const long tiles64 = (long)((M + 63) / 64) * ((N + 63) / 64);
+    if (tiles64 < 128)
+      return launch_tiled_f32<32>(epi, (const float*)A, (const float*)W, M, N, K, (float*)out, s);
+    return launch_tiled_f32<64>(epi, (const float*)A, (const float*)W, M, N, K, (float*)out, s);
   }
   if (N % 128 != 0 || K % 64 != 0) return hipErrorInvalidValue;
   // Three tilings: 256 x 256 and 192 x 256 (8 waves, one block per CU) and
