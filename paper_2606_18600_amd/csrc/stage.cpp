@@ -46,7 +46,13 @@ constexpr int kSplitMinBlocks = 4;   // at least 4 blocks (64 keys) per split
 constexpr int kSkinnyMaxRows = 128;  // decode-sized steps use split-K GEMMs
 constexpr int kMaxKvSplits = 4;      // K splits of the key/value columns of a prefill QKV
 constexpr int kMaxMidSplits = 8;     // K splits of the products of a small tiled step
-constexpr int kMidRows = 2048;       // partial-plane rows of such a step (splits x T)
+constexpr int kMidRows = 2048;       // partial-plane rows of such a step (splits x T) ...
+constexpr size_t kMidElems = 16u << 20;  // ... or this many fp32 values, if more (narrow N)
+
+// fp32 values the partial planes of a small tiled step's [T, N] product may
+// take: kMidRows rows, or kMidElems values for narrow products (tensor-
+// parallel shards), whose 256-wide tiles need more K ranges to fill a round.
+size_t mid_capacity(int N) { return std::max((size_t)kMidRows * N, kMidElems); }
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -242,8 +248,9 @@ void plan_workspace(stage* st) {
   take(st->r_x, T * H * 4);
   take(st->r_h, Tp * H * es);
   // split-K planes of small tiled steps (bf16)
-  const size_t mid_rows = c.dtype == STAGE_BF16 && T > R ? (size_t)kMidRows : 0;
-  take(st->r_qkv, std::max({T, (size_t)st->s_qkv * R, mid_rows}) * qkvw * 4);
+  const bool mid = c.dtype == STAGE_BF16 && T > R;
+  take(st->r_qkv, std::max({T * qkvw, (size_t)st->s_qkv * R * qkvw,
+                            mid ? mid_capacity(qkvw) : 0}) * 4);
   take(st->r_kvpart, c.dtype == STAGE_BF16 ? kMaxKvSplits * T * (qkvw - qw) * 4 : 0);
   take(st->r_q, T * qw * es);
   take(st->r_attn, Tp * qw * es);
@@ -253,8 +260,9 @@ void plan_workspace(stage* st) {
   // split-K planes of the O / down products of skinny steps and of the last
   // rows of a large step, the mid-split planes, and the QKV planes of the
   // last rows (only one of them is live at a time)
-  take(st->r_part_x, std::max({(size_t)std::max(st->s_o, st->s_down) * R * H, mid_rows * H,
-                               c.dtype == STAGE_BF16 && T > R ? (size_t)st->s_qkv * R * qkvw : 0}) *
+  take(st->r_part_x, std::max({(size_t)std::max(st->s_o, st->s_down) * R * H,
+                               mid ? mid_capacity(H) : 0,
+                               mid ? (size_t)st->s_qkv * R * qkvw : 0}) *
                          4);
   const size_t max_items = st->max_ditems;
   take(st->r_part_o, max_items * qw * 4);
@@ -400,7 +408,9 @@ int mid_splits(const stage* st, int T, int N, int K) {
   if (2 * tiles >= st->cus) return 0;
   int best = 0;
   for (int sp = 2; sp <= kMaxMidSplits; sp *= 2)
-    if (tiles * sp <= st->cus && K % (64 * sp) == 0 && sp * T <= kMidRows) best = sp;
+    if (tiles * sp <= st->cus && K % (64 * sp) == 0 &&
+        (size_t)sp * T * N <= mid_capacity(N))
+      best = sp;
   return best;
 }
 
