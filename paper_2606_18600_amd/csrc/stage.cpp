@@ -50,9 +50,14 @@ constexpr int kMidRows = 2048;       // partial-plane rows of such a step (split
 constexpr size_t kMidElems = 16u << 20;  // ... or this many fp32 values, if more (narrow N)
 
 // fp32 values the partial planes of a small tiled step's [T, N] product may
-// take: kMidRows rows, or kMidElems values for narrow products (tensor-
-// parallel shards), whose 256-wide tiles need more K ranges to fill a round.
-size_t mid_capacity(int N) { return std::max((size_t)kMidRows * N, kMidElems); }
+// take (T <= max_tokens): kMidRows rows, or for narrow products (tensor-
+// parallel shards, whose 256-wide tiles need more K ranges to fill a round)
+// up to kMidElems values, as far as kMaxMidSplits planes of max_tokens rows
+// need them.
+size_t mid_capacity(int max_tokens, int N) {
+  return std::max((size_t)kMidRows * N,
+                  std::min(kMidElems, (size_t)kMaxMidSplits * max_tokens * N));
+}
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -250,7 +255,7 @@ void plan_workspace(stage* st) {
   // split-K planes of small tiled steps (bf16)
   const bool mid = c.dtype == STAGE_BF16 && T > R;
   take(st->r_qkv, std::max({T * qkvw, (size_t)st->s_qkv * R * qkvw,
-                            mid ? mid_capacity(qkvw) : 0}) * 4);
+                            mid ? mid_capacity((int)T, (int)qkvw) : 0}) * 4);
   take(st->r_kvpart, c.dtype == STAGE_BF16 ? kMaxKvSplits * T * (qkvw - qw) * 4 : 0);
   take(st->r_q, T * qw * es);
   take(st->r_attn, Tp * qw * es);
@@ -261,7 +266,7 @@ void plan_workspace(stage* st) {
   // rows of a large step, the mid-split planes, and the QKV planes of the
   // last rows (only one of them is live at a time)
   take(st->r_part_x, std::max({(size_t)std::max(st->s_o, st->s_down) * R * H,
-                               mid ? mid_capacity(H) : 0,
+                               mid ? mid_capacity((int)T, (int)H) : 0,
                                mid ? (size_t)st->s_qkv * R * qkvw : 0}) *
                          4);
   const size_t max_items = st->max_ditems;
@@ -409,7 +414,7 @@ int mid_splits(const stage* st, int T, int N, int K) {
   int best = 0;
   for (int sp = 2; sp <= kMaxMidSplits; sp *= 2)
     if (tiles * sp <= st->cus && K % (64 * sp) == 0 &&
-        (size_t)sp * T * N <= mid_capacity(N))
+        (size_t)sp * T * N <= mid_capacity(st->max_tokens, N))
       best = sp;
   return best;
 }
