@@ -350,7 +350,8 @@ typedef enum {
 
 /* Enable (1) or disable (0) HIP-event timing of each op class. While
  * enabled, every launch of the stage is bracketed by events on the call's
- * stream (adding a little overhead). */
+ * stream (adding a little overhead). The events are timing-only: recording
+ * them makes no memory visible to the host or to other devices. */
 stage_status stage_set_op_timing(stage_t* st, int32_t enable);
 
 /* Synchronise the recorded events and return, per op class, the summed

@@ -615,14 +615,21 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__
     l = l * alpha + wave_sum(p);
     o0 *= alpha;
     o1 *= alpha;
-    const int nk = min(64, pos + 1 - c0);
-#pragma unroll 8
-    for (int j = 0; j < nk; ++j) {
+    auto pv = [&](int j) {
       const float pj = __shfl(p, j, 64);
       const int kj = c0 + j;
       const float* vp = kv + ((size_t)bt[kj / kBlock] * n_kv + kvh) * 2 * plane + plane;
       o0 = fmaf(pj, vp[kv_v_offset(kj % kBlock, lane)], o0);
       if (D > 64) o1 = fmaf(pj, vp[kv_v_offset(kj % kBlock, lane + 64)], o1);
+    };
+    // whole 64-key chunks unrolled (a loop with a shuffle and a run-time
+    // trip count is not), the last partial chunk key by key
+    const int nk = min(64, pos + 1 - c0);
+    if (nk == 64) {
+#pragma unroll 8
+      for (int j = 0; j < 64; ++j) pv(j);
+    } else {
+      for (int j = 0; j < nk; ++j) pv(j);
     }
     m = mn;
   }

@@ -377,8 +377,12 @@ hipEvent_t take_event(stage* st) {
     st->free_events.pop_back();
     return e;
   }
+  // Timing-only events: no system-scope release or acquire when they are
+  // recorded (only their timestamps are read, after hipEventSynchronize), so
+  // that the op timing does not add an L2 writeback and invalidation around
+  // every timed launch.
   hipEvent_t e = nullptr;
-  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
   return e;
 }
 
