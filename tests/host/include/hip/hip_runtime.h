@@ -37,6 +37,7 @@ typedef struct hipIpcMemHandle_st {
 
 #define hipHostMallocDefault 0x0
 #define hipEventDisableTiming 0x2
+#define hipEventDisableSystemFence 0x20000000
 #define hipIpcMemLazyEnablePeerAccess 0x01
 
 hipError_t hipGetDeviceCount(int* count);

@@ -362,6 +362,41 @@ def test_forward_calls_return_validation_codes():
         pair.close()
 
 
+def test_op_timing_hook():
+    """The op-timing hook: with timing on, every op class of a decode step is
+    timed (the four products once per layer) and the outputs are bitwise
+    those of the same step with timing off."""
+    seed, n_layers = 61, 2
+    shape = QWEN_SMALL
+    ctx = np.array([30, 5, 17, 64], np.int32)
+    bt_np = synth.make_block_tables(ctx + 1, 5, synth.BlockAllocator(24, seed))
+    pair = Pair(shape, "bf16", n_layers, 24, 64, 4, seed)
+    try:
+        h = pair.gpu.handle
+        bt = torch.from_numpy(bt_np).cuda()
+        x = torch.from_numpy(synth.hidden_states(seed, 1, 4, shape.hidden)).to("cuda",
+                                                                              torch.bfloat16)
+        y0 = pair.gpu.decode(ctx, bt, x).clone()
+        S.stage_set_op_timing(h, True)
+        y1 = pair.gpu.decode(ctx, bt, x).clone()
+        ms, n = S.stage_read_op_times(h)
+        S.stage_set_op_timing(h, False)
+        y2 = pair.gpu.decode(ctx, bt, x).clone()
+        ms2, n2 = S.stage_read_op_times(h)
+        log(f"  op ms: {dict(zip(S.OP_NAMES, np.round(ms, 4)))}")
+        for j, name in enumerate(S.OP_NAMES):
+            if name == "lm_head":
+                assert n[j] == 0
+            else:
+                assert n[j] >= n_layers and ms[j] > 0.0, name
+            if name in ("qkv", "o_proj", "gate_up", "down"):
+                assert n[j] == n_layers, name
+        assert sum(n2) == 0 and sum(ms2) == 0.0  # counters reset by the read; timing off
+        assert torch.equal(y0, y1) and torch.equal(y0, y2)
+    finally:
+        pair.close()
+
+
 @pytest.mark.parametrize("kind,shape_fn", [
     ("w_qkv", lambda s: (s.qkv_width, s.hidden)), ("w_o", lambda s: (s.hidden, s.q_width)),
     ("w_gate_up", lambda s: (2 * s.ffn, s.hidden)), ("w_down", lambda s: (s.hidden, s.ffn))])
