@@ -171,7 +171,7 @@ hipError_t attn_merge(DType dt, const float* part_o, const float* part_ml,
                       const int32_t* tok_item_start, const int32_t* tok_rows, int n_tok, int n_q,
                       int n_kv, int head_dim, void* out, hipStream_t s);
 // Prefill attention: one 4-wave workgroup per (item, kv head), each wave
-// holding 2 tiles of 16 (position, head) rows.
+// holding one tile of 32 (position, head) rows.
 hipError_t attn_prefill(DType dt, const void* q, KVLayer kv, SegTables tabs,
                         const PrefillItem* items, int n_items, int n_q, void* out,
                         hipStream_t s);
@@ -181,8 +181,8 @@ hipError_t attn_f32(const float* q, KVLayer kv, SegTables tabs, const int32_t* t
                     const int32_t* tok_pos, int t_begin, int n_tok, int n_q, float* out,
                     hipStream_t s);
 
-// (position, head) rows of one prefill attention work item: 4 waves of two
-// 16-row tiles.
+// (position, head) rows of one prefill attention work item: 4 waves of one
+// 32-row tile.
 constexpr int kPrefillRows = 128;
 // Positions handled by one prefill work item for a GQA group size.
 int prefill_item_positions(DType dt, int group);
