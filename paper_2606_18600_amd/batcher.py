@@ -29,7 +29,7 @@ class Request:
     prompt: int
     out: int
     arrival: float
-    blocks: List[int] = field(default_factory=list)
+    blocks: np.ndarray = field(default_factory=lambda: np.zeros(0, np.int32))
     prefilled: int = 0   # prompt tokens already in the cache
     decoded: int = 0     # decode steps done
 
@@ -66,7 +66,7 @@ class Batcher:
             need = r.need_blocks(self.block)
             if need > len(self.alloc.free) or need > self.max_blocks:
                 break
-            r.blocks = self.alloc.take(need)
+            r.blocks = self.take_blocks(need)
             self.running.append(self.queue.pop(0))
 
     def plan(self):
@@ -96,6 +96,12 @@ class Batcher:
             else:
                 keep.append(r)
         self.running = keep
+
+    def take_blocks(self, n: int) -> np.ndarray:
+        # int32 arrays, so that building a step's block tables is one row
+        # copy per request (a list of ids converts element by element: ~1 ms
+        # per step at 128 requests)
+        return np.asarray(self.alloc.take(n), np.int32)
 
     def tables(self, reqs) -> np.ndarray:
         bt = np.zeros((max(1, len(reqs)), self.max_blocks), np.int32)
@@ -153,7 +159,7 @@ def run_continuous(st, shape, n_layers: int, seed: int, steps: int, warm: int, n
     for i in range(n_init):
         r = Request(i, int(ctx0[i]), int(outs[i]), 0.0)
         r.prefilled = r.prompt
-        r.blocks = b.alloc.take(r.need_blocks(synth.BLOCK))
+        r.blocks = b.take_blocks(r.need_blocks(synth.BLOCK))
         b.running.append(r)
     for j in range(n_new):
         b.submit(Request(n_init + j, int(prompts[j]), int(outs[n_init + j]), float(arr[j])))

@@ -67,7 +67,7 @@ def test_block_tables_hold_each_requests_blocks():
     b.admit(0.0)
     bt = b.tables(b.running)
     for row, r in zip(bt, b.running):
-        assert list(row[: len(r.blocks)]) == r.blocks
+        assert list(row[: len(r.blocks)]) == list(r.blocks)
         assert (row[len(r.blocks):] == 0).all()
 
 
