@@ -240,8 +240,9 @@ def bench_full_model(args):
         B = 128
         byts = 2 * shape.ffn * shape.hidden * 2 + B * shape.hidden * 2 + B * shape.ffn * 2
         gbs = byts / (gu_us / 1e6) / 1e9
-        res["roofline"] = {"bound": "hbm", "kernel": "gemm_skinny_bf16 (gate-up + SwiGLU, "
-                                                     "decode-only steps, up to 128 rows)",
+        res["roofline"] = {"bound": "hbm", "kernel": "gemm_skinny8_bf16 (gate-up + SwiGLU of "
+                                                     "decode-only steps: 65-128 rows; "
+                                                     "gemm_skinny_bf16 below)",
                            "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                            "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
                            "bytes_per_launch": byts, "us_per_launch": round(gu_us, 1),
