@@ -1039,6 +1039,9 @@ def main():
                     help="print HBM traffic per launch from FETCH_SIZE / WRITE_SIZE runs and exit")
     ap.add_argument("--summary-title", default="")
     ap.add_argument("--summary-cmd", action="append", default=[])
+    ap.add_argument("--summary-algorithmic", default="",
+                    help="with --summarize-pmc: the algorithmic-bytes line (default: the "
+                         "decode gate-up's)")
     args = ap.parse_args()
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace, args.summary_title,
@@ -1047,8 +1050,9 @@ def main():
     if args.summarize_pmc:
         from paper_2606_18600_amd import synth
         sh = synth.LLAMA70B
-        alg = (f"decode gate-up + SwiGLU (M=64, N={2 * sh.ffn}, K={sh.hidden}) "
-               f"{gate_up_swiglu_bytes(sh, 64)} bytes")
+        alg = args.summary_algorithmic or (
+            f"decode gate-up + SwiGLU (M=64, N={2 * sh.ffn}, K={sh.hidden}) "
+            f"{gate_up_swiglu_bytes(sh, 64)} bytes")
         print(summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.summary_title,
                             args.summary_cmd, alg))
         return
