@@ -303,7 +303,7 @@ def estimator_check(args, result, configs, est_blocks):
         launches = E.step_launches(nL, "prefill") * cal.launch_us * 1e-3
         pred = float(np.mean([step_roofline_ms(sh, nL, q32["chunks"], c, cal.tflops, cal.gbs)
                               for c in q32["dec_ctx"]])) + launches
-        row("q32_mixed_step", pred, configs["c4_q32_mixed"]["ms_per_step"])
+        row("q32_mixed_step", pred, configs["q32_mixed"]["ms_per_step"])
     if rows:
         out["mape_pct"] = round(E.mape([p for p, _ in rows], [m for _, m in rows]), 2)
     log(f"[bench] estimator: {out}")
@@ -320,30 +320,33 @@ def bench_default(args):
     from paper_2606_18600_amd import stage as S
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    only = set(args.only.split(",")) if args.only else {"c1", "c2", "c4", "c5"}
+    parts = ("tiny", "l70-decode", "q32-mixed", "l70-full")
+    only = set(args.only.split(",")) if args.only else set(parts)
+    if not only <= set(parts):
+        raise SystemExit(f"--only takes a comma-separated subset of {', '.join(parts)}")
     configs = {}
     result = None
-    if "c1" in only:
-        configs["c1_tiny"] = bench_tiny(args)
-    if "c2" in only:
+    if "tiny" in only:
+        configs["tiny"] = bench_tiny(args)
+    if "l70-decode" in only:
         result, ms, step_bytes, gu_gbs = bench_l70_stage(args)
-    if "c4" in only:
-        configs["c4_q32_mixed"] = bench_q32_mixed(args)
-    if "c5" in only:
-        configs["c5_l70_full"] = bench_full_model(args)
+    if "q32-mixed" in only:
+        configs["q32_mixed"] = bench_q32_mixed(args)
+    if "l70-full" in only:
+        configs["l70_full"] = bench_full_model(args)
     if result is None:
         result = {"metric": METRIC, "value": None, "unit": "tok/s", "n_gpus": 1,
                   "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
                   "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
                   "config": {"workload": "partial run (--only)"}}
-    if not args.no_estimator and ("c2" in only or "c4" in only):
-        est_blocks = [result.pop("_est", None)] + [configs.get("c4_q32_mixed", {}).pop("_est", None)]
+    if not args.no_estimator and ("l70-decode" in only or "q32-mixed" in only):
+        est_blocks = [result.pop("_est", None)] + [configs.get("q32_mixed", {}).pop("_est", None)]
         result["estimator"] = estimator_check(args, result, configs, est_blocks)
     for c in configs.values():
         c.pop("_est", None)
     result.pop("_est", None)
     cal = calibrate(torch, S, stream)
-    if "c2" in only:
+    if "l70-decode" in only:
         cal["gate_up_frac_of_copy"] = round(gu_gbs / cal["copy_GBs"], 4)
         cal["decode_step_frac_of_copy"] = round(step_bytes / (ms / 1e3) / 1e9 / cal["copy_GBs"],
                                                 4)
@@ -836,8 +839,7 @@ def cpu_block(tokens_per_step, n_layers, sec_layer, reps, spent, what, unit="tok
 
 def bench_l70_stage(args):
     """The metric's workload: the 20-layer Llama-3.1-70B-shaped stage, decode
-    batch 64 (C2), then the chunked prefill of 8 prompts on the same stage
-    (C3)."""
+    batch 64, then the chunked prefill of 8 prompts on the same stage."""
     import torch
     from paper_2606_18600_amd import stage as S
     from paper_2606_18600_amd import synth
@@ -1022,8 +1024,8 @@ def main():
     ap.add_argument("--no-estimator", action="store_true",
                     help="default run: skip the estimator's check against the measured steps")
     ap.add_argument("--only", default="",
-                    help="default run: comma-separated subset of c1,c2,c4,c5 (c2 includes the "
-                         "prefill, c3)")
+                    help="default run: comma-separated subset of tiny, l70-decode (with the "
+                         "chunked prefill of the same stage), q32-mixed, l70-full")
     ap.add_argument("--requests", type=int, default=512,
                     help="l70-full: new requests queued behind the 128 running ones")
     ap.add_argument("--arrival-rate", type=float, default=0.0,

@@ -41,7 +41,7 @@ def test_tiny_prefill_then_16_decodes(dtype):
     decode steps with fresh N(0,1) inputs, shuffled block tables."""
     seed = 2606
     shape = synth.TINY
-    log(f"tiny C1 flow dtype={dtype} seed={seed}")
+    log(f"tiny-stage flow dtype={dtype} seed={seed}")
     lens = synth.uniform_lengths(seed, 0, 4, 16, 64)
     alloc = synth.BlockAllocator(64, seed)
     bt = synth.make_block_tables(lens + 16, 8, alloc)
