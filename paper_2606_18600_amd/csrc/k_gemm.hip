@@ -5,10 +5,11 @@
 //
 // * gemm_skinny_bf16: decode-sized M (<= 128). The product is bound by
 //   reading W once from HBM. Block = 4 waves on 4 adjacent 64-row groups of W
-//   over one K range (the A fragments they share come through L1). Each wave
-//   streams its group's fragments (contiguous in the packed layout) with
-//   non-temporal loads, two 64-wide k steps in flight, and writes an fp32
-//   partial tile per K split; the consumer kernel sums the splits. With one
+//   over one K range (the A fragments they share are copied once per block
+//   into an LDS ring). Each wave streams its group's fragments (contiguous
+//   in the packed layout) with non-temporal loads, two 64-wide k steps in
+//   flight, and writes an fp32 partial tile per K split; the consumer
+//   kernel sums the splits. With one
 //   split the gate-up GEMM applies SwiGLU in its epilogue. 65-128 rows run
 //   on 8 waves (gemm_skinny8_bf16); products split over K run on 8 waves
 //   over two weight groups and four k parts (gemm_skinny_kp_bf16), which
@@ -16,9 +17,11 @@
 // * gemm_tiled_bf16: many rows (prefill, mixed steps), compute-bound.
 //   256 x 256 (8 waves of 64 x 128), 192 x 256 or 128 x 128 block tiles;
 //   weight fragments copied HBM -> LDS with direct loads (64-wide k steps,
-//   double-buffered), A fragments loaded straight into registers a stage
-//   ahead; epilogues: fp32 store, residual add, SwiGLU, query RoPE.
-// * gemm_tiled_f32: plain fp32 SIMT tiles for the fp32 mode (row-major).
+//   double-buffered), A fragments loaded straight into registers one or two
+//   stages ahead; epilogues: fp32 store, residual add, SwiGLU, query RoPE.
+// * gemm_tiled_f32: plain fp32 SIMT tiles (32 or 64 wide) for the fp32 mode
+//   (row-major); gemv_f32: fp32 products of at most 8 rows, one wave per
+//   output column.
 #include <algorithm>
 #include <cstdlib>
 #include <type_traits>
